@@ -1,0 +1,199 @@
+"""TEST INFRASTRUCTURE — the CPU oracle for the calibration replay.
+
+Only ``tests/``, ``__graft_entry__.smoke()`` and ``bench.py``'s cpu_baseline
+leg may import this package.  It is a plain, slow reference written from the
+paper (Eq. 1, Eq. 3, Section 3.4, Appendices B and D); it shares no code with
+the HIP library and never imports it.
+
+``kvr_oracle.c`` holds the double loop, the closed form, the stable order and
+the selection; ``exact.py`` holds an exact rational event simulation used to
+pin the double loop on tiny inputs.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+from typing import Optional
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "kvr_oracle.c")
+_LIB = os.path.join(_HERE, "_build", "liboracle.so")
+_lib = None
+
+
+def build(force: bool = False) -> str:
+    """Compile the oracle with gcc (-O2, no FP contraction, no fast-math)."""
+    os.makedirs(os.path.dirname(_LIB), exist_ok=True)
+    if force or not os.path.exists(_LIB) or os.path.getmtime(_LIB) < os.path.getmtime(_SRC):
+        tmp = _LIB + f".tmp{os.getpid()}"
+        compile_library(_SRC, tmp)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+def _configure(lib):
+    """Declare the C signatures on a loaded copy of the oracle library."""
+    D, I32, I64 = ctypes.c_double, ctypes.c_int32, ctypes.c_int64
+    P = ctypes.c_void_p
+    lib.oracle_prices_from_platform.argtypes = [D, D, D, D, D, P, P, P]
+    lib.oracle_lambda_crit.argtypes = [D, D]
+    lib.oracle_lambda_crit.restype = D
+    lib.oracle_congestion_prices.argtypes = [P, I32, D, D, D, P]
+    lib.oracle_eq3_timer.argtypes = [D, D, D, D, D]
+    lib.oracle_eq3_timer.restype = D
+    lib.oracle_cost_grid.argtypes = [P, P, I64, P, I64, D, D, D, D, D,
+                                     P, I32, P, I32, P, I32, P]
+    lib.oracle_select.argtypes = [P, I64, I32, I32, I32, P, P, P, P]
+    lib.oracle_stable_order.argtypes = [P, I64, P]
+    lib.oracle_closed_form_grid.argtypes = [P, P, I64, P, P, I64, D, D, D, D, D,
+                                            P, I32, P, I32, P, I32, P]
+    lib.oracle_closed_form_bootstrap.argtypes = [P, P, I64, P, I64, I64, D, D, D,
+                                                 D, D, P, I32, P, I32, P, I32,
+                                                 P, P]
+    lib.oracle_num_threads.restype = ctypes.c_int
+    return lib
+
+
+def compile_library(src: str, out: str) -> None:
+    subprocess.check_call(["gcc", "-O2", "-ffp-contract=off", "-fno-fast-math",
+                           "-fopenmp", "-shared", "-fPIC", "-std=c11",
+                           "-Wall", "-Wextra", "-o", out, src, "-lm"])
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        build()
+        _lib = _configure(ctypes.CDLL(_LIB))
+    return _lib
+
+
+def _p(a: Optional[np.ndarray]):
+    return None if a is None else a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _f64(a):
+    return np.ascontiguousarray(a, dtype=np.float64)
+
+
+def _i32(a):
+    return np.ascontiguousarray(a, dtype=np.int32)
+
+
+class Prices:
+    """Per-token price vector plus host capacity and reference wait."""
+
+    def __init__(self, a1, b2, b3, c2=425.0, w_ref=1800.0):
+        self.a1, self.b2, self.b3 = float(a1), float(b2), float(b3)
+        self.c2, self.w_ref = float(c2), float(w_ref)
+
+    def tuple(self):
+        return (self.a1, self.b2, self.b3, self.c2, self.w_ref)
+
+    def __repr__(self):
+        return f"Prices(a1={self.a1!r}, b2={self.b2!r}, b3={self.b3!r}, c2={self.c2!r}, w_ref={self.w_ref!r})"
+
+
+def prices_from_platform(kv_bytes_per_token, hbm_usable_bytes, host_link_bytes_per_s,
+                         prefill_tokens_per_s, n_gpu=1.0, host_slots_c2=425.0,
+                         w_ref_s=1800.0) -> Prices:
+    """Appendix B price vector, per token."""
+    lib = _load()
+    a1, b2, b3 = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
+    lib.oracle_prices_from_platform(float(kv_bytes_per_token), float(hbm_usable_bytes),
+                                    float(host_link_bytes_per_s), float(prefill_tokens_per_s),
+                                    float(n_gpu), ctypes.byref(a1), ctypes.byref(b2),
+                                    ctypes.byref(b3))
+    return Prices(a1.value, b2.value, b3.value, host_slots_c2, w_ref_s)
+
+
+def workload_prices(wl) -> Prices:
+    pf = wl.platform
+    return prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
+                                pf["host_link_bytes_per_s"], pf["prefill_tokens_per_s"],
+                                pf["n_gpu"], pf["host_slots_c2"], pf["w_ref_s"])
+
+
+def lambda_crit(c2: float, w_ref: float) -> float:
+    return _load().oracle_lambda_crit(float(c2), float(w_ref))
+
+
+def congestion_prices(lam, b3, c2, w_ref) -> np.ndarray:
+    lam = _f64(lam)
+    out = np.empty_like(lam)
+    _load().oracle_congestion_prices(_p(lam), lam.size, float(b3), float(c2),
+                                     float(w_ref), _p(out))
+    return out
+
+
+def eq3_timer(lam, b2, b3, c2, w_ref) -> float:
+    return _load().oracle_eq3_timer(float(lam), float(b2), float(b3), float(c2),
+                                    float(w_ref))
+
+
+def cost_grid(wait_s, ctx, prices: Prices, t1, t2, lam, idx_row=None) -> np.ndarray:
+    """Double loop; returns cost[n_lam, n_t1, n_t2] (mean GPU-s per request)."""
+    w, T = _f64(wait_s), _i32(ctx)
+    t1, t2, lam = _f64(t1), _f64(t2), _f64(lam)
+    idx = None if idx_row is None else _i32(idx_row)
+    m = w.size if idx is None else idx.size
+    out = np.empty((lam.size, t1.size, t2.size), dtype=np.float64)
+    _load().oracle_cost_grid(_p(w), _p(T), w.size, _p(idx), m, *prices.tuple(),
+                             _p(t1), t1.size, _p(t2), t2.size, _p(lam), lam.size,
+                             _p(out))
+    return out
+
+
+def select(cost, t2):
+    """cost[..., n_lam, n_t1, n_t2] -> (best, best_cost, branch), each [..., n_lam]."""
+    cost = _f64(cost)
+    t2 = _f64(t2)
+    *lead, L, K1, K2 = cost.shape
+    batch = int(np.prod(lead)) if lead else 1
+    best = np.empty(batch * L, dtype=np.int32)
+    bc = np.empty(batch * L, dtype=np.float64)
+    br = np.empty(batch * L, dtype=np.int32)
+    _load().oracle_select(_p(cost), batch, L, K1, K2, _p(t2), _p(best), _p(bc), _p(br))
+    shape = tuple(lead) + (L,)
+    return best.reshape(shape), bc.reshape(shape), br.reshape(shape)
+
+
+def stable_order(wait_s) -> np.ndarray:
+    w = _f64(wait_s)
+    perm = np.empty(w.size, dtype=np.int32)
+    _load().oracle_stable_order(_p(w), w.size, _p(perm))
+    return perm
+
+
+def closed_form_grid(wait_s, ctx, prices: Prices, t1, t2, lam, idx_row=None,
+                     perm=None) -> np.ndarray:
+    w, T = _f64(wait_s), _i32(ctx)
+    t1, t2, lam = _f64(t1), _f64(t2), _f64(lam)
+    perm = stable_order(w) if perm is None else _i32(perm)
+    idx = None if idx_row is None else _i32(idx_row)
+    m = w.size if idx is None else idx.size
+    out = np.empty((lam.size, t1.size, t2.size), dtype=np.float64)
+    _load().oracle_closed_form_grid(_p(w), _p(T), w.size, _p(perm), _p(idx), m,
+                                    *prices.tuple(), _p(t1), t1.size, _p(t2), t2.size,
+                                    _p(lam), lam.size, _p(out))
+    return out
+
+
+def closed_form_bootstrap(wait_s, ctx, idx, prices: Prices, t1, t2, lam):
+    """Closed-form selection for every row of idx[R, m]: (best, best_cost) [R, n_lam]."""
+    w, T, idx = _f64(wait_s), _i32(ctx), _i32(idx)
+    t1, t2, lam = _f64(t1), _f64(t2), _f64(lam)
+    R, m = idx.shape
+    best = np.empty((R, lam.size), dtype=np.int32)
+    bc = np.empty((R, lam.size), dtype=np.float64)
+    _load().oracle_closed_form_bootstrap(_p(w), _p(T), w.size, _p(idx), R, m,
+                                         *prices.tuple(), _p(t1), t1.size, _p(t2),
+                                         t2.size, _p(lam), lam.size, _p(best), _p(bc))
+    return best, bc
+
+
+def num_threads() -> int:
+    return int(_load().oracle_num_threads())

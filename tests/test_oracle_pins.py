@@ -1,0 +1,372 @@
+"""Pins of the CPU oracle against what the paper and the mathematics fix.
+
+Each test names the passage it follows.  None of them compares the oracle
+with a retyped copy of its own formula: the pins are an exact rational event
+simulation, the sorted-prefix closed form, closed-form expectations of the
+wait families, the paper's printed numbers, invariances, and library sorts.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import workloads
+from oracle import exact
+from tests import helpers as H
+
+
+def _paper_prices(oracle_mod, alpha1=0.0176, beta2=0.02, beta3=1.91):
+    # per-request prices of Appendix B on T = 1 token contexts
+    return oracle_mod.Prices(alpha1, beta2, beta3, 425.0, 1800.0)
+
+
+# --------------------------------------------------------------------- P1 --
+def _tiny_cases():
+    rng = np.random.Generator(np.random.PCG64(7))
+    cases = []
+    for c in range(10):
+        n = int(rng.integers(1, 13))
+        k1 = int(rng.integers(1, 4))
+        k2f = int(rng.integers(1, 6))
+        L = int(rng.integers(1, 5))
+        t1 = np.sort(rng.choice([0.0, 0.5, 2.0, 30.0, 300.0], size=k1, replace=False))
+        t2 = np.sort(rng.choice([1.0, 7.0, 60.0, 450.0, 3000.0, 20000.0], size=k2f, replace=False))
+        if c % 2 == 0:
+            t2 = np.concatenate([t2, [np.inf]])
+        w = rng.exponential(400.0, n)
+        # crafted boundaries: on t1, on a deadline, zero, duplicates
+        if n >= 4:
+            w[0] = t1[-1]
+            w[1] = t1[0] + t2[0]
+            w[2] = 0.0
+            w[3] = w[1]
+        T = rng.integers(1, 50000, n).astype(np.int32)
+        lam = np.concatenate([[0.1, 425.0 / 1800.0], rng.uniform(0.3, 2.0, 2)])[:L]
+        cases.append((w, T, t1, t2, lam))
+    # all waits below every timer: structural ties everywhere
+    cases.append((np.array([0.5, 0.25, 0.75]), np.array([3, 1, 2], np.int32),
+                  np.array([0.0, 1.0]), np.array([2.0, 5.0, np.inf]), np.array([0.1, 0.9])))
+    # one request, every wait equal to a deadline
+    cases.append((np.array([12.0, 12.0]), np.array([7, 7], np.int32),
+                  np.array([2.0]), np.array([10.0, 11.0, np.inf]), np.array([0.5])))
+    return cases
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_p1_exact_event_simulation(oracle_mod, case):
+    """Oracle mean within 4 m 2^-53 of the exact rational simulation, and the
+    same selection (Eq. 1, Eq. 3, Appendix D semantics)."""
+    w, T, t1, t2, lam = _tiny_cases()[case]
+    pr = oracle_mod.workload_prices(workloads.make("tiny-exp-1k"))
+    pr = oracle_mod.Prices(pr.a1 * 100, pr.b2 * 10, pr.b3, 425.0, 1800.0)
+    got = oracle_mod.cost_grid(w, T, pr, t1, t2, lam)
+    ex = exact.cost_grid(w, T, pr, t1, t2, lam)
+    m = len(w)
+    for l in range(len(lam)):
+        for a in range(len(t1)):
+            for k in range(len(t2)):
+                e = float(ex[l][a][k])
+                assert abs(got[l, a, k] - e) <= 4 * m * H.EPS * abs(e) + 1e-300, (l, a, k)
+    best, _, _ = oracle_mod.select(got, t2)
+    assert list(best) == exact.select(ex)
+
+
+def test_p1_bootstrap_rows_exact(oracle_mod):
+    """Bootstrap rows (with repeats) against the exact simulation."""
+    rng = np.random.Generator(np.random.PCG64(11))
+    w = rng.exponential(300.0, 9)
+    T = rng.integers(1, 100, 9).astype(np.int32)
+    t1, t2, lam = np.array([0.0, 20.0]), np.array([5.0, 200.0, np.inf]), np.array([0.2, 1.5])
+    pr = oracle_mod.Prices(1e-3, 2e-2, 0.5, 425.0, 1800.0)
+    for r in range(3):
+        idx = rng.integers(0, 9, 11).astype(np.int32)
+        got = oracle_mod.cost_grid(w, T, pr, t1, t2, lam, idx_row=idx)
+        ex = exact.cost_grid(w, T, pr, t1, t2, lam, idx_row=idx)
+        np.testing.assert_allclose(got, np.array(ex, dtype=float), rtol=4 * 11 * H.EPS, atol=0)
+        assert list(oracle_mod.select(got, t2)[0]) == exact.select(ex)
+
+
+# --------------------------------------------------------------------- P2 --
+@pytest.mark.parametrize("seed,n,k1,k2,L,boot", [(1, 4096, 3, 33, 5, 0),
+                                                  (2, 3001, 1, 65, 4, 0),
+                                                  (3, 2048, 4, 17, 6, 3),
+                                                  (4, 1500, 2, 9, 3, 2)])
+def test_p2_double_loop_vs_closed_form(oracle_mod, seed, n, k1, k2, L, boot):
+    """Two derivations of the same mean agree: the per-sample double loop and
+    the sorted prefix-sum closed form (Eq. 1 integrated over the waits)."""
+    wl = workloads.random_case(seed, n, k1, k2, L, resamples=boot, ties=True)
+    pr = oracle_mod.workload_prices(wl)
+    rows = [None] if wl.idx is None else list(wl.idx)
+    for row in rows:
+        a = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam, idx_row=row)
+        b = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                        idx_row=row)
+        # bound: prefix sums of m positive terms plus one cancellation per term
+        tol = 8 * wl.m * H.EPS
+        assert np.max(H.rel_err(b, a)) <= tol
+        ba = oracle_mod.select(a, wl.t2)[0]
+        bb = oracle_mod.select(b, wl.t2)[0]
+        H.near_tie_ok(a, ba, bb, tol)
+
+
+def test_p2_closed_form_bootstrap_matches_rows(oracle_mod):
+    wl = workloads.random_case(5, 1200, 2, 12, 3, resamples=4)
+    pr = oracle_mod.workload_prices(wl)
+    best, bc = oracle_mod.closed_form_bootstrap(wl.wait_s, wl.ctx_tokens, wl.idx, pr,
+                                                wl.t1, wl.t2, wl.lam)
+    for r in range(4):
+        c = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                 idx_row=wl.idx[r])
+        b, cc, _ = oracle_mod.select(c, wl.t2)
+        np.testing.assert_allclose(bc[r], cc, rtol=8 * wl.m * H.EPS)
+        H.near_tie_ok(c[None], b[None], best[r][None], 8 * wl.m * H.EPS)
+
+
+# --------------------------------------------------------------------- P3 --
+def test_p3_price_vector_arithmetic(oracle_mod):
+    """Appendix B / Table 3: alpha_1 = GPUs x suffix tokens / pool tokens,
+    beta_3 = GPUs x re-prefill time, t_1 = beta_2/alpha_1, t* = beta_3/alpha_1
+    (Eq. 2), each to the printed precision."""
+    rows = H.read_table("price_vector.txt")
+    kv = None
+    for r in rows:
+        if r[0] == "KVBYTES":
+            kv = math.prod(int(x) for x in r[1:6])
+            assert kv == int(r[6])
+    for r in rows:
+        if r[0] in ("FULL", "KVBYTES", "TTFT"):
+            continue
+        gpus, toks, pool = float(r[1]), float(r[2]), float(r[3])
+        beta2, beta3, a1p, t1p, tsp = map(float, r[4:9])
+        # the pool is pool_tokens x kv bytes of HBM; per-token prices times T
+        pr = oracle_mod.prices_from_platform(kv, pool * kv, 1.0, 1.0, gpus)
+        alpha1 = pr.a1 * toks
+        assert abs(alpha1 - a1p) <= 0.5 * 10 ** -_decimals(r[6]) + 1e-12
+        # Eq. 2 from the unrounded alpha_1; beta_3 is printed to three
+        # significant digits, so t* carries that 0.5 % on top of its own rounding
+        assert abs(beta2 / alpha1 - t1p) <= 0.5 * 10 ** -_decimals(r[7]) + 1e-9
+        assert abs(beta3 / alpha1 - tsp) <= 0.5 * 10 ** -_decimals(r[8]) + 0.005 * tsp
+    full = [r for r in rows if r[0] == "FULL"][0]
+    pr = oracle_mod.prices_from_platform(kv, float(full[4]) * kv, 1.0, 1.0, float(full[2]))
+    assert abs(pr.a1 * float(full[3]) - float(full[5])) <= 5e-5
+    ttft = [r for r in rows if r[0] == "TTFT"][0]
+    # beta_3 per token at the measured rate (suffix tokens per TTFT), times T
+    pr = oracle_mod.prices_from_platform(kv, 1.0, 1.0, 3000.0 / float(ttft[1]), float(ttft[2]))
+    assert abs(pr.b3 * 3000.0 - float(ttft[3])) <= 0.01
+
+
+def _decimals(s):
+    return len(s.split(".")[1]) if "." in s else 0
+
+
+def test_p3_eq2_break_evens_through_the_cost_grid(oracle_mod):
+    """Eq. 2 via the oracle's own cost lines: one request of wait w, choose
+    between staying in HBM (t1 beyond w) and offloading at once (t1 = 0,
+    host-retain).  The choice flips at w = beta_2/alpha_1 (HBM-DRAM
+    break-even); versus discarding at once it flips at beta_3/alpha_1."""
+    a1, b2, b3 = 0.0176, 0.02, 1.91
+    pr = _paper_prices(oracle_mod, a1, b2, b3)
+    lam = np.array([0.1])            # uncongested
+    for w in (0.99 * b2 / a1, 1.01 * b2 / a1):
+        c = oracle_mod.cost_grid([w], [1], pr, np.array([0.0, 1e6]), np.array([np.inf]), lam)
+        best = oracle_mod.select(c, np.array([np.inf]))[0][0]
+        assert best == (1 if w < b2 / a1 else 0)
+    for w in (0.99 * b3 / a1, 1.01 * b3 / a1):
+        # t2 far below any wait: discard right after the offload
+        c = oracle_mod.cost_grid([w], [1], pr, np.array([0.0, 1e6]), np.array([1e-9]), lam)
+        best = oracle_mod.select(c, np.array([1e-9]))[0][0]
+        assert best == (1 if w < b3 / a1 else 0)
+
+
+# --------------------------------------------------------------------- P4 --
+def test_p4_eq3_congestion_and_timer(oracle_mod):
+    """Eq. 3 with the paper's constants (C2 = 425, W_ref = 1,800 s,
+    beta_2 = 0.02, beta_3 = 1.91): lambda_crit = 0.23611/s; the timer is
+    infinite at 0.5x and 1x lambda_crit, 1,781.15 s at 2x and 890.58 s at 3x."""
+    lc = oracle_mod.lambda_crit(425.0, 1800.0)
+    assert abs(lc - 0.2361111) < 1e-7
+    for mult, want in ((0.5, math.inf), (1.0, math.inf), (2.0, 1781.15), (3.0, 890.58)):
+        t = oracle_mod.eq3_timer(mult * lc, 0.02, 1.91, 425.0, 1800.0)
+        if math.isinf(want):
+            assert math.isinf(t)
+        else:
+            assert abs(t - want) < 0.01
+    # the timer is the DRAM-discard break-even of the oracle's own costs:
+    # one request of wait w, discard at once versus keep until resume
+    pr = _paper_prices(oracle_mod)
+    lam = 2.0 * lc
+    t2s = oracle_mod.eq3_timer(lam, 0.02, 1.91, 425.0, 1800.0)
+    for w in (0.98 * t2s, 1.02 * t2s):
+        grid_t2 = np.array([1e-9, np.inf])
+        c = oracle_mod.cost_grid([w], [1], pr, np.array([0.0]), grid_t2, np.array([lam]))
+        best = oracle_mod.select(c, grid_t2)[0][0]
+        assert best == (1 if w < t2s else 0)
+
+
+# --------------------------------------------------------------------- P5 --
+@pytest.mark.parametrize("family", ["lognormal", "exponential", "mixture"])
+def test_p5_table6_uncongested_rows(oracle_mod, family):
+    """Below lambda_crit the congestion price is zero, so a fixed timer costs
+    beta_2 + (beta_3 - beta_2) P(W > t2) and host-retain costs beta_2.
+    Stratified samples of the Section 4.1 families: within 1e-3 of that
+    expectation, and within 0.03 of Table 6's printed 0.5x row (a
+    4,000-request replay, so sampling error is expected)."""
+    rows = {r[0]: list(map(float, r[1:])) for r in H.read_table("table6_uncongested.txt")}
+    w = H.stratified_family(family, 40000)
+    T = np.ones(w.size, np.int32)
+    pr = _paper_prices(oracle_mod)
+    t2 = np.array([600.0, 1800.0, 3600.0, np.inf])
+    lc = 425.0 / 1800.0
+    c = oracle_mod.cost_grid(w, T, pr, np.array([0.0]), t2, np.array([0.5 * lc, lc]))
+    for li in range(2):
+        row = c[li, 0]
+        assert abs(row[3] - 0.02) < 1e-12
+        assert abs(row[3] - rows[family][0]) < 5e-4
+        for j, t in enumerate((600.0, 1800.0, 3600.0)):
+            expect = 0.02 + (1.91 - 0.02) * H.survival(family, t)
+            assert abs(row[j] - expect) < 1e-3, (family, t, row[j], expect)
+            assert abs(row[j] - rows[family][1 + j]) < 0.03, (family, t, row[j])
+
+
+# --------------------------------------------------------------------- P6 --
+def test_p6_memoryless_waits_expiry_only_adds_churn(oracle_mod):
+    """Section 1 / Eq. 3: for exponential waits of mean mu and t1 = 0,
+    E[C(t2)] - E[C(inf)] = T exp(-t2/mu) (b3 - b2 - a2 mu): one sign for every
+    t2, so no interior optimum; retain wins iff
+    lambda <= lambda_crit + C2 (1 - b2/b3) / mu (0.45984/s here)."""
+    wl = workloads.make("tiny-exp-1k")
+    pr = oracle_mod.workload_prices(wl)
+    mu = 1800.0
+    w = H.stratified_exponential(100000, mu)
+    T = np.full(w.size, 8192, np.int32)
+    lam = np.array([0.25, 0.455, 0.465, 0.5, 0.75, 1.0])
+    c = oracle_mod.cost_grid(w, T, pr, wl.t1, wl.t2, lam)
+    a2 = oracle_mod.congestion_prices(lam, pr.b3, pr.c2, pr.w_ref)
+    thr = 425.0 / 1800.0 + 425.0 * (1.0 - pr.b2 / pr.b3) / mu
+    assert abs(thr - 0.45984) < 1e-5
+    for l in range(lam.size):
+        diff = c[l, 0, :-1] - c[l, 0, -1]
+        expect = 8192 * np.exp(-wl.t2[:-1] / mu) * (pr.b3 - pr.b2 - a2[l] * mu)
+        assert np.max(np.abs(diff - expect)) < 1e-3 * 8192 * pr.b3
+        # stratified estimates of P(W > t2) and E[min(W, t2)] are off by at
+        # most ~1/n and ~t2/n; check the sign wherever it is resolved by that
+        bound = 8192 * ((pr.b3 - pr.b2) + a2[l] * wl.t2[:-1]) / w.size
+        sure = np.abs(expect) > 10 * bound
+        assert sure.sum() >= 40
+        assert np.all(np.sign(diff[sure]) == np.sign(expect[sure]))
+    best = oracle_mod.select(c, wl.t2)[0]
+    assert list(best) == [64, 64, 0, 0, 0, 0]
+
+
+def test_p6_tiny_workload_selection(oracle_mod):
+    """The same invariant on the seeded 1,000-wait draw: retain at 0.25/s,
+    the shortest timer at 0.5, 0.75 and 1.0/s."""
+    wl = workloads.make("tiny-exp-1k")
+    pr = oracle_mod.workload_prices(wl)
+    c = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    best = oracle_mod.select(c, wl.t2)[0]
+    assert list(best) == [64, 0, 0, 0]
+
+
+# --------------------------------------------------------------------- P7 --
+def test_p7_footprint_linear_and_monotone(oracle_mod):
+    """Every term is T times a T-free price, so doubling every T doubles every
+    cost bit for bit and keeps the selection; a larger KV footprint per token
+    (a1 and b2 up) never lowers a cost."""
+    wl = workloads.random_case(21, 700, 3, 20, 4, ties=True)
+    pr = oracle_mod.workload_prices(wl)
+    c1 = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    c2 = oracle_mod.cost_grid(wl.wait_s, 2 * wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    assert np.array_equal(c2, 2 * c1)
+    assert np.array_equal(oracle_mod.select(c1, wl.t2)[0], oracle_mod.select(c2, wl.t2)[0])
+    big = oracle_mod.Prices(pr.a1 * 2.5, pr.b2 * 2.5, pr.b3, pr.c2, pr.w_ref)
+    c3 = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, big, wl.t1, wl.t2, wl.lam)
+    assert np.all(c3 >= c1)
+
+
+# --------------------------------------------------------------------- P8 --
+def test_p8_load_monotone_and_affine(oracle_mod):
+    """Eq. 3: cost is non-decreasing in lambda, independent of lambda up to
+    lambda_crit, and affine in max(0, lambda - lambda_crit)."""
+    wl = workloads.random_case(22, 900, 2, 15, 1)
+    pr = oracle_mod.workload_prices(wl)
+    lc = 425.0 / 1800.0
+    lam = np.array([0.05, 0.15, lc, 0.3, 0.6, 1.1])
+    c = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, lam)
+    assert np.array_equal(c[0], c[1]) and np.array_equal(c[1], c[2])
+    assert np.all(np.diff(c, axis=0) >= 0)
+    p = np.maximum(lam - lc, 0)
+    pred = c[3] + (p[5] - p[3]) / (p[4] - p[3]) * (c[4] - c[3])
+    np.testing.assert_allclose(c[5], pred, rtol=1e-12)
+
+
+# --------------------------------------------------------------------- P9 --
+def test_p9_mean_field_occupancy(oracle_mod):
+    """Appendix D: a TTL policy keeps a context on the host for min(W, t2) on
+    average.  With T = 1, t1 = 0 and equal restore/recompute prices the cost
+    is b + a2 E[min(W, t2)], and E[min(W, t2)] = mu (1 - exp(-t2/mu)) for
+    exponential waits."""
+    mu = 1800.0
+    w = H.stratified_exponential(100000, mu)
+    pr = oracle_mod.Prices(0.01, 0.5, 0.5, 425.0, 1800.0)
+    t2 = np.array([60.0, 900.0, 1800.0, 7200.0, np.inf])
+    lam = np.array([1.0])
+    a2 = oracle_mod.congestion_prices(lam, pr.b3, pr.c2, pr.w_ref)[0]
+    c = oracle_mod.cost_grid(w, np.ones(w.size, np.int32), pr, np.array([0.0]), t2, lam)
+    occ = (c[0, 0] - 0.5) / a2
+    want = mu * (1.0 - np.exp(-t2 / mu))
+    np.testing.assert_allclose(occ, want, rtol=1e-3)
+
+
+# -------------------------------------------------------------------- P10 --
+def test_p10_identity_resample_and_permutation(oracle_mod):
+    """A bootstrap row that draws every sample once in order is the sample
+    itself (bit for bit); shuffling the sample keeps the selection."""
+    wl = workloads.random_case(23, 800, 2, 24, 3, ties=True)
+    pr = oracle_mod.workload_prices(wl)
+    base = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    ident = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                 idx_row=np.arange(wl.n, dtype=np.int32))
+    assert np.array_equal(base, ident)
+    perm = np.random.Generator(np.random.PCG64(5)).permutation(wl.n)
+    shuf = oracle_mod.cost_grid(wl.wait_s[perm], wl.ctx_tokens[perm], pr, wl.t1, wl.t2, wl.lam)
+    np.testing.assert_allclose(shuf, base, rtol=1e-13)
+    H.near_tie_ok(base, oracle_mod.select(base, wl.t2)[0], oracle_mod.select(shuf, wl.t2)[0],
+                  1e-13)
+
+
+# ------------------------------------------------------------------- sort --
+def test_stable_order_matches_library_sort(oracle_mod):
+    rng = np.random.Generator(np.random.PCG64(9))
+    w = rng.exponential(100.0, 5000)
+    w[rng.integers(0, 5000, 1500)] = w[3]
+    w[rng.integers(0, 5000, 100)] = 0.0
+    w[rng.integers(0, 5000, 100)] = -0.0
+    perm = oracle_mod.stable_order(w)
+    assert np.array_equal(perm, np.argsort(w, kind="stable"))
+    assert np.array_equal(oracle_mod.stable_order(w[:1]), [0])
+
+
+def test_selection_tie_rule(oracle_mod):
+    """Exact ties go to the larger flat index; branch is RETAIN iff the chosen
+    host timer is infinite."""
+    cost = np.array([[[3.0, 1.0, 1.0], [1.0, 2.0, 1.0]]])   # [L=1][K1=2][K2=3]
+    t2 = np.array([5.0, 9.0, np.inf])
+    best, bc, br = oracle_mod.select(cost, t2)
+    assert best[0] == 5 and bc[0] == 1.0 and br[0] == 0
+    cost2 = np.array([[[3.0, 0.5, 1.0], [1.0, 2.0, 1.0]]])
+    best, bc, br = oracle_mod.select(cost2, t2)
+    assert best[0] == 1 and br[0] == 1
+
+
+def test_workload_generator_is_deterministic():
+    a = workloads.make("boot-1024x64k", resamples=3)
+    b = workloads.make("boot-1024x64k", resamples=5)
+    assert np.array_equal(a.idx, b.idx[:3])
+    assert np.array_equal(a.wait_s, workloads.make("mix-64k").wait_s)
+    w3 = workloads.make("weibull-1m")
+    assert w3.n == 1 << 20 and w3.wait_s.max() <= 86400.0 and w3.wait_s.min() >= 0
+    assert w3.ctx_tokens.min() >= 1024 and w3.ctx_tokens.max() <= 131072
+    mix = workloads.make("mix-64k")
+    assert mix.ctx_tokens.min() >= 2048 and mix.ctx_tokens.max() <= 32768
+    assert abs(np.median(workloads.make("tiny-exp-1k").wait_s) - 1800 * math.log(2)) < 150
