@@ -1,0 +1,185 @@
+/*
+ * kvr.h — C ABI of the MI355X (gfx950) calibration-replay library.
+ *
+ * The library evaluates the GPU-opportunity cost of keeping a suspended
+ * request's KV cache under every candidate retention policy, over a
+ * calibration sample of approval waits, and selects the cheapest policy per
+ * load level.  This is the calibration replay of "Adaptive KV Retention for
+ * LLM Agents at Human-Approval Timescales" (Section 3.4: replay held-out
+ * waits under both host branches, total the cost, freeze the cheaper branch),
+ * widened to a grid of candidate timers, loads and bootstrap resamples.
+ *
+ * Cost definition (Section 3.1 Eq. 1, Section 3.3 Eq. 3, Appendix D):
+ *   a request of T tokens suspends for w seconds.  It stays in HBM for
+ *   min(w, t1) seconds at alpha_1 = T*a1 GPU-s/s (beta_1 = 0).  If w > t1 it
+ *   is offloaded to host DRAM at t1 and a one-shot host timer t2 is armed;
+ *   the deadline, measured from suspension, is e = t1 + t2 rounded once to
+ *   binary64.  On the host it pays alpha_2(lambda) = T*a2(lambda) GPU-s/s
+ *   until min(w, e), with
+ *       a2(lambda) = max(0, lambda - lambda_crit) * b3 / C2,
+ *       lambda_crit = C2 / W_ref            (Little's law saturation),
+ *   then pays beta_2 = T*b2 at resume if w <= e (restore from host), or
+ *   beta_3 = T*b3 if the copy was discarded at e (recompute).  t2 = +inf is
+ *   host-retain.  The cost of a policy (t1_a, t2_k, lambda_l) is the mean of
+ *   the per-request cost over the sample, in GPU-s per request (the unit of
+ *   Table 6).
+ *
+ * Conventions shared by every entry point:
+ *   - Return value: KVR_OK (0) or a negative KVR_E_* code.  No exception
+ *     crosses the ABI.  Errors detected on the host launch nothing and leave
+ *     every output untouched.
+ *   - "device" pointers are HIP device allocations owned by the caller
+ *     (e.g. torch tensors); "host" pointers are ordinary host memory that the
+ *     call reads before it returns and does not keep.
+ *   - All device work is enqueued on hip_stream (a hipStream_t; NULL is the
+ *     null stream) and is asynchronous: inputs must stay unchanged and
+ *     outputs must not be read until the stream has been synchronised.
+ *   - Workspace: calls that take (d_ws, ws_bytes) size it in two phases.
+ *     With d_ws == NULL they write the required byte count into *ws_bytes,
+ *     launch nothing and return KVR_OK; with d_ws != NULL, *ws_bytes must be
+ *     at least that count (else KVR_E_WORKSPACE).  d_ws must be 256-byte
+ *     aligned.  The library keeps no state between calls; calls on distinct
+ *     workspaces may run concurrently from different threads.
+ *   - Device-detected domain errors (a wait that is NaN, infinite or
+ *     negative; a context size below 1; a bootstrap index outside [0, n))
+ *     cannot be reported by the return value of an asynchronous call.  The
+ *     kernels record them in a status word at the start of the workspace and
+ *     replace the offending value by a safe one; kvr_workspace_status() reads
+ *     the word after synchronising the stream.  Outputs of such a call are
+ *     meaningless.
+ *   - Sizes: 1 <= n <= 2^31 - 1 samples; 1 <= n_t1, n_t2, n_lam;
+ *     n_t1 * n_t2 <= 2^24 policies; n_lam <= 4096; n_resamples * m <= 2^40.
+ */
+#ifndef KVR_H
+#define KVR_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum {
+    KVR_OK = 0,
+    KVR_E_NULL = -1,       /* a required pointer is NULL                          */
+    KVR_E_SIZE = -2,       /* a count is out of range, or a product overflows     */
+    KVR_E_GRID = -3,       /* timer/load grid invalid (see kvr_policy_grid)       */
+    KVR_E_PRICE = -4,      /* a price, C2 or W_ref is not finite and > 0          */
+    KVR_E_WORKSPACE = -5,  /* workspace too small or not 256-byte aligned         */
+    KVR_E_DOMAIN = -6,     /* device-detected bad sample or index (status word)   */
+    KVR_E_HIP = -7,        /* a HIP runtime call failed                           */
+    KVR_E_METHOD = -8      /* unknown method, or an option the method lacks       */
+};
+
+enum { KVR_BRUTE = 0, KVR_SORTED = 1 };   /* kvr_cost_grid methods            */
+enum { KVR_RETAIN = 0, KVR_EXPIRE = 1 };  /* branch codes of kvr_select_policy */
+
+/* Price vector per token (Appendix B) plus the host-tier constants of
+ * Section 3.3.  Every field must be finite and > 0. */
+typedef struct {
+    double a1_per_token;   /* alpha_1 / T: GPU-s per second of HBM residency     */
+    double b2_per_token;   /* beta_2 / T: GPU-s to restore from host at resume   */
+    double b3_per_token;   /* beta_3 / T: GPU-s to recompute at resume           */
+    double host_slots_c2;  /* C2: suspended contexts that fit in host DRAM       */
+    double w_ref_s;        /* W_ref: reference residence time, seconds           */
+} kvr_prices;
+
+/* Candidate policies and loads; all three arrays are HOST pointers.
+ *   t1[n_t1]:  GPU-tier timers, seconds; finite, >= 0, strictly ascending.
+ *              {0} means offload at suspension (Section 3.4).
+ *   t2[n_t2]:  host timers, seconds; > 0, strictly ascending, not NaN; only
+ *              the last may be +INFINITY (host-retain).
+ *   lam[n_lam]: offered loads, suspended requests per second; finite, >= 0,
+ *              any order.
+ * Policies are indexed by the flat index f = a * n_t2 + k. */
+typedef struct {
+    const double *t1;  int32_t n_t1;
+    const double *t2;  int32_t n_t2;
+    const double *lam; int32_t n_lam;
+} kvr_policy_grid;
+
+/*
+ * Appendix B price vector per token from platform constants (host only):
+ *   a1 = n_gpu * kv_bytes_per_token / hbm_usable_bytes   (share of usable HBM)
+ *   b2 = n_gpu * kv_bytes_per_token / host_link_bytes_per_s (restore time)
+ *   b3 = n_gpu / prefill_tokens_per_s                     (re-prefill time)
+ * host_slots_c2 and w_ref_s are copied through.  Every argument must be
+ * finite and > 0 (else KVR_E_PRICE); out must not be NULL (KVR_E_NULL).
+ */
+int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
+                             double host_link_bytes_per_s, double prefill_tokens_per_s,
+                             double n_gpu, double host_slots_c2, double w_ref_s,
+                             kvr_prices *out);
+
+/*
+ * Cost grid of one calibration sample (the replay of Section 3.4 over every
+ * candidate policy and load).
+ *   d_wait_s[n]     device, float64: suspension (approval) waits, seconds.
+ *   d_ctx_tokens[n] device, int32: context tokens per request (T >= 1).
+ *   p, g            host: prices and policy grid (validated on the host).
+ *   method          KVR_BRUTE: every (sample, policy, load) evaluated;
+ *                   KVR_SORTED: stable radix sort of the waits, prefix sums
+ *                   of T and T*w, closed form per policy.
+ *   d_cost          device, float64 [n_lam][n_t1][n_t2]: mean GPU-s per
+ *                   request (written in full).
+ *   d_perm          device, int32 [n] or NULL: KVR_SORTED only, the stable
+ *                   ascending order of the waits (-0.0 equals +0.0; equal
+ *                   waits keep input order).  Non-NULL with KVR_BRUTE is
+ *                   KVR_E_METHOD.
+ *   d_ws, ws_bytes  workspace (two-phase sizing, see above).
+ */
+int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                  const kvr_prices *p, const kvr_policy_grid *g, int32_t method,
+                  double *d_cost, int32_t *d_perm,
+                  void *d_ws, size_t *ws_bytes, void *hip_stream);
+
+/*
+ * Policy selection (Section 3.4: freeze the cheaper branch), per load.
+ *   d_cost          device, float64 [batch][n_lam][n_t1][n_t2].
+ *   last_t2_is_inf  1 if the last host timer is +inf (host-retain), else 0.
+ *   d_best          device, int32 [batch][n_lam]: flat index f = a*n_t2 + k
+ *                   of the smallest cost; exact ties go to the larger f.
+ *   d_best_cost     device, float64 [batch][n_lam].
+ *   d_branch        device, int32 [batch][n_lam] or NULL: KVR_RETAIN if the
+ *                   chosen timer is the infinite one, else KVR_EXPIRE.
+ * No workspace; costs are expected to be finite (NaN costs give an
+ * unspecified index).
+ */
+int kvr_select_policy(const double *d_cost, int64_t batch, int32_t n_lam, int32_t n_t1,
+                      int32_t n_t2, int32_t last_t2_is_inf,
+                      int32_t *d_best, double *d_best_cost, int32_t *d_branch,
+                      void *hip_stream);
+
+/*
+ * Bootstrap calibration: the brute-force grid over every resample, with the
+ * selection fused per resample.
+ *   d_wait_s[n], d_ctx_tokens[n]  device: the base sample (as kvr_cost_grid).
+ *   d_idx           device, int32 [n_resamples][m]: with-replacement draws,
+ *                   each in [0, n).  The caller draws them (seeded).
+ *   d_best          device, int32 [n_resamples][n_lam]: selected flat index.
+ *   d_best_cost     device, float64 [n_resamples][n_lam].
+ *   d_cost          device, float64 [n_resamples][n_lam][n_t1][n_t2] or
+ *                   NULL: the full cost tensor, when the caller wants it.
+ */
+int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                  const int32_t *d_idx, int64_t n_resamples, int64_t m,
+                  const kvr_prices *p, const kvr_policy_grid *g,
+                  int32_t *d_best, double *d_best_cost, double *d_cost,
+                  void *d_ws, size_t *ws_bytes, void *hip_stream);
+
+/*
+ * Synchronise hip_stream and read the status word of a workspace used by
+ * kvr_cost_grid or kvr_bootstrap: KVR_OK, KVR_E_DOMAIN, or KVR_E_HIP if the
+ * synchronisation or the read failed.  d_ws NULL is KVR_E_NULL.
+ */
+int kvr_workspace_status(const void *d_ws, void *hip_stream);
+
+/* Static English text for a status code (never NULL). */
+const char *kvr_status_string(int status);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* KVR_H */

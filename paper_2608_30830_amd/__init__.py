@@ -1,0 +1,248 @@
+"""Python binding of libkvr (MI355X calibration replay): argument marshalling only.
+
+Every entry point forwards to the C ABI declared in ``include/kvr.h`` with
+the same name; PyTorch provides device memory and the current HIP stream.
+All computation runs in the library's HIP kernels.  There is no CPU path: if
+the library is not built, or no GPU is visible, the calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import math
+import os
+from typing import Optional, Sequence, Tuple
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "_build", "libkvr.so")
+
+KVR_OK = 0
+KVR_E_NULL = -1
+KVR_E_SIZE = -2
+KVR_E_GRID = -3
+KVR_E_PRICE = -4
+KVR_E_WORKSPACE = -5
+KVR_E_DOMAIN = -6
+KVR_E_HIP = -7
+KVR_E_METHOD = -8
+KVR_BRUTE = 0
+KVR_SORTED = 1
+KVR_RETAIN = 0
+KVR_EXPIRE = 1
+
+EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy",
+           "kvr_bootstrap", "kvr_workspace_status", "kvr_status_string")
+
+
+class kvr_prices(ctypes.Structure):
+    _fields_ = [("a1_per_token", ctypes.c_double), ("b2_per_token", ctypes.c_double),
+                ("b3_per_token", ctypes.c_double), ("host_slots_c2", ctypes.c_double),
+                ("w_ref_s", ctypes.c_double)]
+
+
+class kvr_policy_grid(ctypes.Structure):
+    _fields_ = [("t1", ctypes.POINTER(ctypes.c_double)), ("n_t1", ctypes.c_int32),
+                ("t2", ctypes.POINTER(ctypes.c_double)), ("n_t2", ctypes.c_int32),
+                ("lam", ctypes.POINTER(ctypes.c_double)), ("n_lam", ctypes.c_int32)]
+
+
+class KvrError(RuntimeError):
+    def __init__(self, code: int, where: str):
+        self.code = code
+        super().__init__(f"{where}: {status_string(code)} (status {code})")
+
+
+_lib = None
+
+
+def load_library(path: str = LIB_PATH):
+    """Load libkvr.so (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(path):
+        raise RuntimeError(f"libkvr is not built ({path}); run __graft_entry__.build()")
+    lib = ctypes.CDLL(path)
+    P, I32, I64, D = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_double
+    SZ = ctypes.POINTER(ctypes.c_size_t)
+    lib.kvr_prices_from_platform.argtypes = [D, D, D, D, D, D, D, ctypes.POINTER(kvr_prices)]
+    lib.kvr_prices_from_platform.restype = ctypes.c_int
+    lib.kvr_cost_grid.argtypes = [P, P, I64, ctypes.POINTER(kvr_prices),
+                                  ctypes.POINTER(kvr_policy_grid), I32, P, P, P, SZ, P]
+    lib.kvr_cost_grid.restype = ctypes.c_int
+    lib.kvr_select_policy.argtypes = [P, I64, I32, I32, I32, I32, P, P, P, P]
+    lib.kvr_select_policy.restype = ctypes.c_int
+    lib.kvr_bootstrap.argtypes = [P, P, I64, P, I64, I64, ctypes.POINTER(kvr_prices),
+                                  ctypes.POINTER(kvr_policy_grid), P, P, P, P, SZ, P]
+    lib.kvr_bootstrap.restype = ctypes.c_int
+    lib.kvr_workspace_status.argtypes = [P, P]
+    lib.kvr_workspace_status.restype = ctypes.c_int
+    lib.kvr_status_string.argtypes = [ctypes.c_int]
+    lib.kvr_status_string.restype = ctypes.c_char_p
+    _lib = lib
+    return lib
+
+
+def status_string(code: int) -> str:
+    return load_library().kvr_status_string(int(code)).decode()
+
+
+def _check(code: int, where: str) -> None:
+    if code != KVR_OK:
+        raise KvrError(code, where)
+
+
+def kvr_prices_from_platform(kv_bytes_per_token: float, hbm_usable_bytes: float,
+                             host_link_bytes_per_s: float, prefill_tokens_per_s: float,
+                             n_gpu: float = 1.0, host_slots_c2: float = 425.0,
+                             w_ref_s: float = 1800.0) -> kvr_prices:
+    out = kvr_prices()
+    _check(load_library().kvr_prices_from_platform(
+        float(kv_bytes_per_token), float(hbm_usable_bytes), float(host_link_bytes_per_s),
+        float(prefill_tokens_per_s), float(n_gpu), float(host_slots_c2), float(w_ref_s),
+        ctypes.byref(out)), "kvr_prices_from_platform")
+    return out
+
+
+class PolicyGrid:
+    """Host arrays of a policy grid, kept alive while the ctypes view is used."""
+
+    def __init__(self, t1: Sequence[float], t2: Sequence[float], lam: Sequence[float]):
+        self._t1 = (ctypes.c_double * len(t1))(*[float(x) for x in t1])
+        self._t2 = (ctypes.c_double * len(t2))(*[float(x) for x in t2])
+        self._lam = (ctypes.c_double * len(lam))(*[float(x) for x in lam])
+        self.n_t1, self.n_t2, self.n_lam = len(t1), len(t2), len(lam)
+        self.last_inf = 1 if (len(t2) and math.isinf(float(t2[-1]))) else 0
+        self.c = kvr_policy_grid(ctypes.cast(self._t1, ctypes.POINTER(ctypes.c_double)), self.n_t1,
+                                 ctypes.cast(self._t2, ctypes.POINTER(ctypes.c_double)), self.n_t2,
+                                 ctypes.cast(self._lam, ctypes.POINTER(ctypes.c_double)), self.n_lam)
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        raise RuntimeError("libkvr needs a visible GPU (torch.cuda.is_available() is False)")
+    return torch
+
+
+def _stream_ptr(stream) -> ctypes.c_void_p:
+    torch = _torch()
+    s = torch.cuda.current_stream() if stream is None else stream
+    return ctypes.c_void_p(int(s.cuda_stream))
+
+
+def _ptr(t) -> Optional[int]:
+    return None if t is None else ctypes.c_void_p(int(t.data_ptr()))
+
+
+def _need(t, dtype, name):
+    torch = _torch()
+    if t.device.type != "cuda" or t.dtype != dtype or not t.is_contiguous():
+        raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor")
+
+
+def _workspace(nbytes: int, ws=None):
+    torch = _torch()
+    if ws is not None and ws.numel() >= nbytes:
+        return ws
+    return torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
+
+
+def kvr_cost_grid(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid, method: int = KVR_BRUTE,
+                  want_perm: bool = False, out=None, workspace=None, stream=None,
+                  check: bool = True):
+    """cost[n_lam, n_t1, n_t2] (and perm[n] for KVR_SORTED with want_perm)."""
+    torch = _torch()
+    lib = load_library()
+    _need(wait_s, torch.float64, "wait_s")
+    _need(ctx_tokens, torch.int32, "ctx_tokens")
+    n = wait_s.numel()
+    need = ctypes.c_size_t(0)
+    _check(lib.kvr_cost_grid(None, None, n, ctypes.byref(prices), ctypes.byref(grid.c), method,
+                             None, None, None, ctypes.byref(need), None), "kvr_cost_grid(size)")
+    ws = _workspace(need.value, workspace)
+    cost = out if out is not None else torch.empty((grid.n_lam, grid.n_t1, grid.n_t2),
+                                                   dtype=torch.float64, device="cuda")
+    perm = torch.empty(n, dtype=torch.int32, device="cuda") if want_perm else None
+    have = ctypes.c_size_t(ws.numel())
+    st = _stream_ptr(stream)
+    _check(lib.kvr_cost_grid(_ptr(wait_s), _ptr(ctx_tokens), n, ctypes.byref(prices),
+                             ctypes.byref(grid.c), method, _ptr(cost), _ptr(perm), _ptr(ws),
+                             ctypes.byref(have), st), "kvr_cost_grid")
+    if check:
+        _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_cost_grid(device)")
+    return (cost, perm) if want_perm else cost
+
+
+def kvr_select_policy(cost, last_t2_is_inf: bool, stream=None) -> Tuple:
+    """cost[..., n_lam, n_t1, n_t2] -> (best, best_cost, branch), each [..., n_lam]."""
+    torch = _torch()
+    _need(cost, torch.float64, "cost")
+    *lead, L, K1, K2 = cost.shape
+    batch = 1
+    for d in lead:
+        batch *= d
+    best = torch.empty((batch, L), dtype=torch.int32, device="cuda")
+    bc = torch.empty((batch, L), dtype=torch.float64, device="cuda")
+    br = torch.empty((batch, L), dtype=torch.int32, device="cuda")
+    _check(load_library().kvr_select_policy(_ptr(cost), batch, L, K1, K2, int(bool(last_t2_is_inf)),
+                                            _ptr(best), _ptr(bc), _ptr(br), _stream_ptr(stream)),
+           "kvr_select_policy")
+    shape = tuple(lead) + (L,)
+    return best.reshape(shape), bc.reshape(shape), br.reshape(shape)
+
+
+class BootstrapCall:
+    """A prepared kvr_bootstrap call: outputs and workspace allocated once, so
+    that ``launch()`` only enqueues the library's kernels."""
+
+    def __init__(self, wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
+                 want_cost: bool = False):
+        torch = _torch()
+        _need(wait_s, torch.float64, "wait_s")
+        _need(ctx_tokens, torch.int32, "ctx_tokens")
+        _need(idx, torch.int32, "idx")
+        if idx.dim() != 2:
+            raise ValueError("idx must be [n_resamples, m]")
+        self.lib = load_library()
+        self.wait_s, self.ctx, self.idx = wait_s, ctx_tokens, idx
+        self.prices, self.grid = prices, grid
+        self.n = wait_s.numel()
+        self.R, self.m = idx.shape
+        self.best = torch.empty((self.R, grid.n_lam), dtype=torch.int32, device="cuda")
+        self.best_cost = torch.empty((self.R, grid.n_lam), dtype=torch.float64, device="cuda")
+        self.cost = (torch.empty((self.R, grid.n_lam, grid.n_t1, grid.n_t2), dtype=torch.float64,
+                                 device="cuda") if want_cost else None)
+        need = ctypes.c_size_t(0)
+        _check(self.lib.kvr_bootstrap(None, None, self.n, None, self.R, self.m,
+                                      ctypes.byref(prices), ctypes.byref(grid.c), None, None,
+                                      _ptr(self.cost) if want_cost else None, None,
+                                      ctypes.byref(need), None), "kvr_bootstrap(size)")
+        self.ws = _workspace(need.value)
+        self.ws_bytes = ctypes.c_size_t(self.ws.numel())
+
+    def launch(self, stream=None) -> None:
+        _check(self.lib.kvr_bootstrap(_ptr(self.wait_s), _ptr(self.ctx), self.n, _ptr(self.idx),
+                                      self.R, self.m, ctypes.byref(self.prices),
+                                      ctypes.byref(self.grid.c), _ptr(self.best),
+                                      _ptr(self.best_cost), _ptr(self.cost), _ptr(self.ws),
+                                      ctypes.byref(self.ws_bytes), _stream_ptr(stream)),
+               "kvr_bootstrap")
+
+    def status(self, stream=None) -> int:
+        return self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream))
+
+
+def kvr_bootstrap(wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
+                  want_cost: bool = False, stream=None, check: bool = True):
+    """(best[R, n_lam], best_cost[R, n_lam]) and, with want_cost, cost[R, n_lam, n_t1, n_t2]."""
+    call = BootstrapCall(wait_s, ctx_tokens, idx, prices, grid, want_cost)
+    call.launch(stream)
+    if check:
+        _check(call.status(stream), "kvr_bootstrap(device)")
+    if want_cost:
+        return call.best, call.best_cost, call.cost
+    return call.best, call.best_cost
+
+
+def kvr_workspace_status(ws, stream=None) -> int:
+    return load_library().kvr_workspace_status(_ptr(ws), _stream_ptr(stream))

@@ -1,0 +1,352 @@
+// C ABI of the calibration-replay library: validation on the host, derivation
+// of the load-dependent prices (Eq. 3), workspace planning and launches.
+// Built as a plain host translation unit (IEEE semantics for every check).
+#include "kvr.h"
+#include "kvr_internal.h"
+
+#include <algorithm>
+#include <cmath>
+#include <cstdint>
+#include <cstring>
+#include <limits>
+#include <vector>
+
+namespace {
+
+using kvr::GridPlan;
+using kvr::PriceDev;
+using kvr::SampleSrc;
+using kvr::Tables;
+
+constexpr int64_t kMaxPolicies = int64_t(1) << 24;
+constexpr int32_t kMaxLoads = 4096;
+constexpr int64_t kMaxBatch = int64_t(1) << 40;
+constexpr size_t kStatusBytes = 256;
+constexpr int64_t kWavesForSplitless = 2048;   // enough waves to fill the GPU
+constexpr int64_t kTargetWaves = 4096;
+constexpr int64_t kMinSplitChunks = 8;        // samples per split >= 8 chunks
+
+size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
+int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+bool pos_finite(double x) { return std::isfinite(x) && x > 0.0; }
+
+int check_prices(const kvr_prices *p)
+{
+    if (!p) return KVR_E_NULL;
+    if (!pos_finite(p->a1_per_token) || !pos_finite(p->b2_per_token) ||
+        !pos_finite(p->b3_per_token) || !pos_finite(p->host_slots_c2) || !pos_finite(p->w_ref_s))
+        return KVR_E_PRICE;
+    return KVR_OK;
+}
+
+int check_grid(const kvr_policy_grid *g)
+{
+    if (!g) return KVR_E_NULL;
+    if (!g->t1 || !g->t2 || !g->lam) return KVR_E_NULL;
+    if (g->n_t1 < 1 || g->n_t2 < 1 || g->n_lam < 1 || g->n_lam > kMaxLoads) return KVR_E_SIZE;
+    if ((int64_t)g->n_t1 * g->n_t2 > kMaxPolicies) return KVR_E_SIZE;
+    for (int32_t a = 0; a < g->n_t1; ++a) {
+        const double v = g->t1[a];
+        if (!std::isfinite(v) || v < 0.0) return KVR_E_GRID;
+        if (a > 0 && !(v > g->t1[a - 1])) return KVR_E_GRID;
+    }
+    for (int32_t k = 0; k < g->n_t2; ++k) {
+        const double v = g->t2[k];
+        if (std::isnan(v) || !(v > 0.0)) return KVR_E_GRID;
+        if (std::isinf(v) && k != g->n_t2 - 1) return KVR_E_GRID;
+        if (k > 0 && !(v > g->t2[k - 1])) return KVR_E_GRID;
+    }
+    for (int32_t l = 0; l < g->n_lam; ++l) {
+        const double v = g->lam[l];
+        if (!std::isfinite(v) || v < 0.0) return KVR_E_GRID;
+    }
+    return KVR_OK;
+}
+
+// Eq. 3 per token: lambda_crit = C2 / W_ref, a2 = max(0, lambda - lambda_crit) * b3 / C2.
+void congestion_prices(const kvr_prices &p, const kvr_policy_grid &g, int32_t Lpad,
+                       std::vector<double> &a2)
+{
+    const double lc = p.host_slots_c2 / p.w_ref_s;
+    a2.assign((size_t)Lpad, 0.0);
+    for (int32_t l = 0; l < g.n_lam; ++l) {
+        double d = g.lam[l] - lc;
+        if (!(d > 0.0)) d = 0.0;
+        a2[(size_t)l] = (d * p.b3_per_token) / p.host_slots_c2;
+    }
+}
+
+struct BrutePlan {
+    GridPlan gp;
+    int32_t Lpad;
+    bool fused;              // nsplit == 1: costs finalised inside the grid kernel
+    // workspace offsets
+    size_t off_t1, off_t2, off_a2, off_X, off_G, off_cand, off_part, off_cost, total;
+};
+
+int choose_tile(int32_t L)
+{
+    const int cands[4] = {4, 8, 16, 32};
+    int best = 32;
+    int64_t best_cost = std::numeric_limits<int64_t>::max();
+    for (int c : cands) {
+        // issue slots per sample: ~5 load-free ops per tile plus one FMA per load
+        const int64_t cost = cdiv(L, c) * (c + 5);
+        if (cost < best_cost) {
+            best_cost = cost;
+            best = c;
+        }
+    }
+    return best;
+}
+
+BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bool bootstrap,
+                     bool want_cost)
+{
+    BrutePlan bp{};
+    GridPlan &gp = bp.gp;
+    const int64_t P = (int64_t)K1 * K2;
+    gp.LT = choose_tile(L);
+    gp.ntiles = (int)cdiv(L, gp.LT);
+    gp.nblk = (int)cdiv(P, kvr::kWave);
+    gp.R = R;
+    bp.Lpad = gp.ntiles * gp.LT;
+    const int64_t base_waves = R * gp.nblk * gp.ntiles;
+    int64_t nsplit = 1;
+    if (base_waves < kWavesForSplitless) {
+        const int64_t max_split = std::max<int64_t>(1, m / (kMinSplitChunks * kvr::kChunk));
+        nsplit = std::min<int64_t>(cdiv(kTargetWaves, base_waves), max_split);
+        if (nsplit < 1) nsplit = 1;
+    }
+    int64_t split_len = cdiv(cdiv(m, nsplit), kvr::kChunk) * kvr::kChunk;
+    nsplit = cdiv(m, split_len);
+    gp.nsplit = (int)nsplit;
+    gp.split_len = split_len;
+    bp.fused = (nsplit == 1);
+
+    size_t off = kStatusBytes;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    bp.off_t1 = take(sizeof(double) * K1);
+    bp.off_t2 = take(sizeof(double) * K2);
+    bp.off_a2 = take(sizeof(double) * bp.Lpad);
+    bp.off_X = take(sizeof(double) * R * K1);
+    bp.off_G = take(sizeof(double) * R * K1);
+    bp.off_cand = bp.off_part = bp.off_cost = 0;
+    if (bp.fused) {
+        if (bootstrap) bp.off_cand = take(sizeof(kvr::ArgminCand) * R * gp.nblk * L);
+    } else {
+        bp.off_part = take(sizeof(double) * nsplit * R * gp.ntiles * (gp.LT + 1) * P);
+        if (bootstrap && !want_cost) bp.off_cost = take(sizeof(double) * R * L * P);
+    }
+    bp.total = off;
+    return bp;
+}
+
+template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+int hip_ok(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_E_HIP; }
+
+#define KVR_TRY(expr)                       \
+    do {                                    \
+        int rc_ = hip_ok(expr);             \
+        if (rc_ != KVR_OK) return rc_;      \
+    } while (0)
+
+// Uploads t1, t2 (canonical zeros) and the padded a2 table; clears the status word.
+int stage_tables(void *ws, size_t off_t1, size_t off_t2, size_t off_a2, int32_t Lpad,
+                 const kvr_prices &p, const kvr_policy_grid &g, hipStream_t s, Tables &tb)
+{
+    std::vector<double> t1(g.t1, g.t1 + g.n_t1), t2(g.t2, g.t2 + g.n_t2), a2;
+    for (double &v : t1) v = v + 0.0;
+    congestion_prices(p, g, Lpad, a2);
+    KVR_TRY(kvr::launch_clear_status(static_cast<int *>(ws), s));
+    KVR_TRY(kvr::launch_upload(at<double>(ws, off_t1), t1.data(), g.n_t1, s));
+    KVR_TRY(kvr::launch_upload(at<double>(ws, off_t2), t2.data(), g.n_t2, s));
+    KVR_TRY(kvr::launch_upload(at<double>(ws, off_a2), a2.data(), Lpad, s));
+    tb.t1 = at<double>(ws, off_t1);
+    tb.t2 = at<double>(ws, off_t2);
+    tb.a2 = at<double>(ws, off_a2);
+    tb.K1 = g.n_t1;
+    tb.K2 = g.n_t2;
+    tb.L = g.n_lam;
+    tb.Lpad = Lpad;
+    return KVR_OK;
+}
+
+int check_workspace(void *d_ws, size_t have, size_t need)
+{
+    if (have < need) return KVR_E_WORKSPACE;
+    if ((reinterpret_cast<uintptr_t>(d_ws) & 255u) != 0) return KVR_E_WORKSPACE;
+    return KVR_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
+                             double host_link_bytes_per_s, double prefill_tokens_per_s,
+                             double n_gpu, double host_slots_c2, double w_ref_s, kvr_prices *out)
+{
+    if (!out) return KVR_E_NULL;
+    if (!pos_finite(kv_bytes_per_token) || !pos_finite(hbm_usable_bytes) ||
+        !pos_finite(host_link_bytes_per_s) || !pos_finite(prefill_tokens_per_s) ||
+        !pos_finite(n_gpu) || !pos_finite(host_slots_c2) || !pos_finite(w_ref_s))
+        return KVR_E_PRICE;
+    out->a1_per_token = n_gpu * kv_bytes_per_token / hbm_usable_bytes;
+    out->b2_per_token = n_gpu * kv_bytes_per_token / host_link_bytes_per_s;
+    out->b3_per_token = n_gpu / prefill_tokens_per_s;
+    out->host_slots_c2 = host_slots_c2;
+    out->w_ref_s = w_ref_s;
+    return KVR_OK;
+}
+
+int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                  const kvr_prices *p, const kvr_policy_grid *g, int32_t method, double *d_cost,
+                  int32_t *d_perm, void *d_ws, size_t *ws_bytes, void *hip_stream)
+{
+    if (!ws_bytes) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if ((rc = check_grid(g)) != KVR_OK) return rc;
+    if (method != KVR_BRUTE && method != KVR_SORTED) return KVR_E_METHOD;
+    if (method == KVR_BRUTE && d_perm != nullptr) return KVR_E_METHOD;
+    if (n < 1 || n > INT32_MAX) return KVR_E_SIZE;
+
+    size_t need;
+    BrutePlan bp{};
+    size_t off_t1 = kStatusBytes, off_t2 = 0, off_a2 = 0, off_sort = 0;
+    int32_t Lpad = g->n_lam;
+    if (method == KVR_BRUTE) {
+        bp = plan_brute(1, n, g->n_t1, g->n_t2, g->n_lam, false, true);
+        need = bp.total;
+    } else {
+        off_t2 = off_t1 + align256(sizeof(double) * g->n_t1);
+        off_a2 = off_t2 + align256(sizeof(double) * g->n_t2);
+        off_sort = off_a2 + align256(sizeof(double) * Lpad);
+        need = off_sort + kvr::sort_ws_bytes(n);
+    }
+    if (d_ws == nullptr) {
+        *ws_bytes = need;
+        return KVR_OK;
+    }
+    if (!d_wait_s || !d_ctx_tokens || !d_cost) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, need)) != KVR_OK) return rc;
+
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    Tables tb{};
+    if (method == KVR_BRUTE) {
+        if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
+            return rc;
+        SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
+        double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
+        KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, status, s));
+        double *part = bp.fused ? nullptr : at<double>(d_ws, bp.off_part);
+        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, bp.fused ? d_cost : nullptr, nullptr,
+                                 part, status, s));
+        if (!bp.fused) KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, n, X, G, part, d_cost, s));
+        return KVR_OK;
+    }
+    if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
+    kvr::SortWs sws{};
+    kvr::sort_ws_carve(at<char>(d_ws, off_sort), n, sws);
+    KVR_TRY(kvr::launch_sorted_path(d_wait_s, d_ctx_tokens, n, tb, pr, sws, d_cost, d_perm, status, s));
+    return KVR_OK;
+}
+
+int kvr_select_policy(const double *d_cost, int64_t batch, int32_t n_lam, int32_t n_t1,
+                      int32_t n_t2, int32_t last_t2_is_inf, int32_t *d_best, double *d_best_cost,
+                      int32_t *d_branch, void *hip_stream)
+{
+    if (!d_cost || !d_best || !d_best_cost) return KVR_E_NULL;
+    if (batch < 1 || n_lam < 1 || n_t1 < 1 || n_t2 < 1 || n_lam > kMaxLoads) return KVR_E_SIZE;
+    if ((int64_t)n_t1 * n_t2 > kMaxPolicies) return KVR_E_SIZE;
+    if (batch * n_lam > INT32_MAX) return KVR_E_SIZE;
+    if (last_t2_is_inf != 0 && last_t2_is_inf != 1) return KVR_E_GRID;
+    KVR_TRY(kvr::launch_select(d_cost, batch, n_lam, (int64_t)n_t1 * n_t2, n_t2, last_t2_is_inf,
+                               d_best, d_best_cost, d_branch, static_cast<hipStream_t>(hip_stream)));
+    return KVR_OK;
+}
+
+int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                  const int32_t *d_idx, int64_t n_resamples, int64_t m, const kvr_prices *p,
+                  const kvr_policy_grid *g, int32_t *d_best, double *d_best_cost, double *d_cost,
+                  void *d_ws, size_t *ws_bytes, void *hip_stream)
+{
+    if (!ws_bytes) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if ((rc = check_grid(g)) != KVR_OK) return rc;
+    if (n < 1 || n > INT32_MAX || n_resamples < 1 || m < 1 || m > INT32_MAX) return KVR_E_SIZE;
+    if (n_resamples > kMaxBatch / m) return KVR_E_SIZE;
+    if (n_resamples * g->n_lam > INT32_MAX) return KVR_E_SIZE;
+    const bool want_cost = d_cost != nullptr;
+    BrutePlan bp = plan_brute(n_resamples, m, g->n_t1, g->n_t2, g->n_lam, true, want_cost);
+    if (d_ws == nullptr) {
+        *ws_bytes = bp.total;
+        return KVR_OK;
+    }
+    if (!d_wait_s || !d_ctx_tokens || !d_idx || !d_best || !d_best_cost) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, bp.total)) != KVR_OK) return rc;
+
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    Tables tb{};
+    if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
+        return rc;
+    SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
+    double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
+    KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, status, s));
+    const int64_t P = (int64_t)g->n_t1 * g->n_t2;
+    if (bp.fused) {
+        kvr::ArgminCand *cand = at<kvr::ArgminCand>(d_ws, bp.off_cand);
+        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, d_cost, cand, nullptr, status, s));
+        KVR_TRY(kvr::launch_reduce_cands(cand, n_resamples, bp.gp.nblk, g->n_lam, d_best,
+                                         d_best_cost, s));
+        return KVR_OK;
+    }
+    double *part = at<double>(d_ws, bp.off_part);
+    double *cost = want_cost ? d_cost : at<double>(d_ws, bp.off_cost);
+    KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, nullptr, nullptr, part, status, s));
+    KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, m, X, G, part, cost, s));
+    KVR_TRY(kvr::launch_select(cost, n_resamples, g->n_lam, P, g->n_t2, 0, d_best, d_best_cost,
+                               nullptr, s));
+    return KVR_OK;
+}
+
+int kvr_workspace_status(const void *d_ws, void *hip_stream)
+{
+    if (!d_ws) return KVR_E_NULL;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int word = 0;
+    if (hipMemcpyAsync(&word, d_ws, sizeof(int), hipMemcpyDeviceToHost, s) != hipSuccess)
+        return KVR_E_HIP;
+    if (hipStreamSynchronize(s) != hipSuccess) return KVR_E_HIP;
+    return word == 0 ? KVR_OK : KVR_E_DOMAIN;
+}
+
+const char *kvr_status_string(int status)
+{
+    switch (status) {
+    case KVR_OK: return "ok";
+    case KVR_E_NULL: return "a required pointer is NULL";
+    case KVR_E_SIZE: return "a count is out of range or a product overflows";
+    case KVR_E_GRID: return "invalid timer or load grid";
+    case KVR_E_PRICE: return "a price, C2 or W_ref is not finite and positive";
+    case KVR_E_WORKSPACE: return "workspace too small or not 256-byte aligned";
+    case KVR_E_DOMAIN: return "bad sample or index detected on the device";
+    case KVR_E_HIP: return "HIP runtime error";
+    case KVR_E_METHOD: return "unknown method or option not supported by the method";
+    default: return "unknown status";
+    }
+}
+
+}  // extern "C"

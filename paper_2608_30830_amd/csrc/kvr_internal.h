@@ -1,0 +1,95 @@
+// Internal declarations shared by the library's HIP sources (not part of the ABI).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace kvr {
+
+constexpr int kWave = 64;          // CDNA wavefront width
+constexpr int kChunk = 128;        // samples staged in LDS per buffer (grid kernel)
+constexpr int kStatusDomain = 1;   // value of the workspace status word on a domain error
+
+// Where a call's samples come from: the base arrays, optionally through
+// bootstrap index rows idx[R][m].
+struct SampleSrc {
+    const double *w;     // [n] waits, seconds
+    const int32_t *T;    // [n] context tokens
+    const int32_t *idx;  // [R][m] or nullptr (then m == n, R == 1)
+    int64_t n;
+    int64_t m;
+};
+
+// Prices and derived scalars of one call.
+struct PriceDev {
+    double a1, b2, b3;
+};
+
+// Derived tables staged in the workspace.
+struct Tables {
+    const double *t1;    // [K1]
+    const double *t2;    // [K2]
+    const double *a2;    // [Lpad] per-token congestion prices, zero-padded
+    int32_t K1, K2, L, Lpad;
+};
+
+// Brute-force launch plan.
+struct GridPlan {
+    int LT;              // loads per tile (4, 8, 16 or 32)
+    int ntiles;          // ceil(L / LT)
+    int nblk;            // policy blocks of one wave: ceil(K1*K2 / 64)
+    int nsplit;          // sample splits per resample
+    int64_t split_len;   // samples per split (multiple of kChunk)
+    int64_t R;           // resamples
+};
+
+struct ArgminCand {     // one wave's best policy for one (resample, load)
+    double cost;
+    int32_t f;
+    int32_t pad;
+};
+
+// ---- launches (all asynchronous on `stream`) --------------------------------
+hipError_t launch_clear_status(int *status, hipStream_t stream);
+hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
+
+hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
+                     int *status, hipStream_t stream);
+
+hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
+                       const GridPlan &plan, const double *X, const double *G,
+                       double *cost_out, ArgminCand *cand, double *partials, int *status,
+                       hipStream_t stream);
+
+hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
+                                  int64_t m, const double *X, const double *G,
+                                  const double *partials, double *cost_out, hipStream_t stream);
+
+hipError_t launch_reduce_cands(const ArgminCand *cand, int64_t R, int nblk, int L,
+                               int32_t *best, double *best_cost, hipStream_t stream);
+
+hipError_t launch_select(const double *cost, int64_t batch, int L, int64_t P, int K2,
+                         int last_inf, int32_t *best, double *best_cost, int32_t *branch,
+                         hipStream_t stream);
+
+// Sorted path.
+struct SortWs {
+    uint64_t *keys[2];
+    int32_t *vals[2];
+    uint32_t *hist;       // [256][nblocks]
+    uint32_t *counts;     // [8][256] global digit counts per pass
+    int64_t *Nsum;        // [n] inclusive prefix of T (sorted order)
+    double *Ssum;         // [n] inclusive prefix of T*w (sorted order)
+    int64_t *blkN;        // [nblocks_scan]
+    double *blkS;         // [nblocks_scan]
+    int nblocks;          // sort tiles
+    int nblocks_scan;     // scan tiles
+};
+
+size_t sort_ws_bytes(int64_t n);
+void sort_ws_carve(void *base, int64_t n, SortWs &ws);
+hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, const Tables &tb,
+                              const PriceDev &pr, SortWs &ws, double *cost_out,
+                              int32_t *perm_out, int *status, hipStream_t stream);
+
+}  // namespace kvr

@@ -1,0 +1,407 @@
+// Sorted path for gfx950: stable LSD radix sort of the waits, prefix scans of
+// T and T*w in sorted order, and the closed-form mean cost per policy.
+//
+// With the waits sorted and N(x) = sum_{w_i <= x} T_i, S(x) = sum_{w_i <= x} T_i w_i,
+// integrating the per-request cost of Eq. 1 (HBM until t1, host until the
+// deadline e = t1 + t2 at the Eq. 3 price, restore or recompute at resume)
+// over the sample gives, with Ttot = N(inf):
+//   n*C = a1*[S(t1) + t1*(Ttot - N(t1))]
+//       + a2*[(S(e) - S(t1)) - t1*(N(e) - N(t1)) + (e - t1)*(Ttot - N(e))]
+//       + b2*(N(e) - N(t1)) + b3*(Ttot - N(e));
+// the (e - t1)*(Ttot - N(e)) term is absent for e = +inf.
+//
+// Sort: keys are the bits of w + 0.0 (waits are >= 0, so unsigned order of
+// the bits is numeric order and -0.0 sorts as +0.0).  Eight 8-bit digit
+// passes, each reduce-then-scan (tile histograms, one exclusive scan, a
+// ranking scatter); no inter-workgroup waiting, so no forward-progress
+// assumption.  Ranking inside a tile is stable: a wave ranks its keys with a
+// ballot match on the digit, in input order.
+#include "kvr_internal.h"
+
+namespace kvr {
+
+constexpr int kSortThreads = 256;
+constexpr int kSortKPT = 8;                                   // keys per thread
+constexpr int kSortTile = kSortThreads * kSortKPT;            // 2048 keys per tile
+constexpr int kWaveKeys = kWave * kSortKPT;                   // 512 keys per wave
+constexpr int kScanThreads = 256;
+constexpr int kScanIPT = 8;
+constexpr int kScanTile = kScanThreads * kScanIPT;
+
+static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
+
+size_t sort_ws_bytes(int64_t n)
+{
+    const int64_t nb = cdiv(n, kSortTile), ns = cdiv(n, kScanTile);
+    size_t b = 0;
+    b += 2 * align256(sizeof(uint64_t) * n);
+    b += 2 * align256(sizeof(int32_t) * n);
+    b += align256(sizeof(uint32_t) * 256 * nb);
+    b += align256(sizeof(uint32_t) * 8 * 256);
+    b += align256(sizeof(int64_t) * n);
+    b += align256(sizeof(double) * n);
+    b += align256(sizeof(int64_t) * ns);
+    b += align256(sizeof(double) * ns);
+    return b;
+}
+
+void sort_ws_carve(void *base, int64_t n, SortWs &ws)
+{
+    char *p = static_cast<char *>(base);
+    ws.nblocks = (int)cdiv(n, kSortTile);
+    ws.nblocks_scan = (int)cdiv(n, kScanTile);
+    auto take = [&](size_t bytes) {
+        char *q = p;
+        p += align256(bytes);
+        return q;
+    };
+    ws.keys[0] = (uint64_t *)take(sizeof(uint64_t) * n);
+    ws.keys[1] = (uint64_t *)take(sizeof(uint64_t) * n);
+    ws.vals[0] = (int32_t *)take(sizeof(int32_t) * n);
+    ws.vals[1] = (int32_t *)take(sizeof(int32_t) * n);
+    ws.hist = (uint32_t *)take(sizeof(uint32_t) * 256 * ws.nblocks);
+    ws.counts = (uint32_t *)take(sizeof(uint32_t) * 8 * 256);
+    ws.Nsum = (int64_t *)take(sizeof(int64_t) * n);
+    ws.Ssum = (double *)take(sizeof(double) * n);
+    ws.blkN = (int64_t *)take(sizeof(int64_t) * ws.nblocks_scan);
+    ws.blkS = (double *)take(sizeof(double) * ws.nblocks_scan);
+}
+
+__device__ __forceinline__ void flag_domain_s(int *status)
+{
+    __hip_atomic_store(status, kStatusDomain, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Keys from waits (domain-checked on the bits), identity payload.
+__global__ void __launch_bounds__(256) sort_prep_kernel(const double *__restrict__ w,
+                                                        const int32_t *__restrict__ T, int64_t n,
+                                                        uint64_t *__restrict__ keys,
+                                                        int32_t *__restrict__ vals, int *status)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= n) return;
+    uint64_t b = (uint64_t)__double_as_longlong(w[i]);
+    if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
+    if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
+        flag_domain_s(status);
+        b = 0;
+    }
+    if (T[i] < 1) flag_domain_s(status);
+    keys[i] = b;
+    vals[i] = (int32_t)i;
+}
+
+// Per-tile digit histogram, digit-major: hist[d * nblocks + tile].
+__global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t *__restrict__ keys,
+                                                                 int64_t n, int shift,
+                                                                 uint32_t *__restrict__ hist,
+                                                                 int nblocks)
+{
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t base = (int64_t)blockIdx.x * kSortTile;
+    for (int q = 0; q < kSortKPT; ++q) {
+        const int64_t i = base + q * kSortThreads + threadIdx.x;
+        if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+}
+
+// Exclusive scan of a uint32 array in place, one block of 1024 threads.
+__global__ void __launch_bounds__(1024) scan_u32_kernel(uint32_t *a, int64_t len)
+{
+    __shared__ uint32_t wsum[16];
+    __shared__ uint32_t carry_s;
+    if (threadIdx.x == 0) carry_s = 0;
+    __syncthreads();
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    for (int64_t base = 0; base < len; base += 1024) {
+        const int64_t i = base + threadIdx.x;
+        uint32_t v = (i < len) ? a[i] : 0u;
+        uint32_t x = v;  // inclusive wave scan
+        for (int off = 1; off < kWave; off <<= 1) {
+            uint32_t y = __shfl_up(x, off, kWave);
+            if (lane >= off) x += y;
+        }
+        if (lane == kWave - 1) wsum[wave] = x;
+        __syncthreads();
+        uint32_t before = carry_s;
+        for (int q = 0; q < wave; ++q) before += wsum[q];
+        if (i < len) a[i] = before + x - v;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t t = carry_s;
+            for (int q = 0; q < 16; ++q) t += wsum[q];
+            carry_s = t;
+        }
+        __syncthreads();
+    }
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// Stable ranking scatter of one digit pass.
+__global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
+    const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int64_t n, int shift,
+    const uint32_t *__restrict__ offs, int nblocks, uint64_t *__restrict__ keys_out,
+    int32_t *__restrict__ vals_out)
+{
+    __shared__ uint32_t wcnt[4][256];
+    __shared__ uint32_t wofs[4][256];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+#pragma unroll
+    for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
+    __syncthreads();
+
+    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * kWaveKeys;
+    uint64_t key[kSortKPT];
+    int32_t val[kSortKPT];
+    uint32_t local[kSortKPT];
+#pragma unroll
+    for (int j = 0; j < kSortKPT; ++j) {
+        const int64_t i = base + j * kWave + lane;
+        const bool valid = i < n;
+        key[j] = valid ? keys_in[i] : 0;
+        val[j] = valid ? vals_in[i] : 0;
+        const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+        uint64_t peers = __ballot(valid);
+#pragma unroll
+        for (int b = 0; b < 8; ++b) {
+            const bool bit = (d >> b) & 1u;
+            const uint64_t m = __ballot(bit);
+            peers &= bit ? m : ~m;
+        }
+        const uint32_t rank = lanes_below(peers);
+        const uint32_t before = wcnt[wave][d];
+        local[j] = before + rank;
+        __builtin_amdgcn_wave_barrier();
+        if (valid && rank == 0) wcnt[wave][d] = before + (uint32_t)__popcll(peers);
+        __builtin_amdgcn_wave_barrier();
+    }
+    __syncthreads();
+    {
+        const int d = threadIdx.x;
+        uint32_t run = 0;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            wofs[q][d] = run;
+            run += wcnt[q][d];
+        }
+    }
+    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kSortKPT; ++j) {
+        const int64_t i = base + j * kWave + lane;
+        if (i < n) {
+            const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+            const int64_t dest = (int64_t)offs[(int64_t)d * nblocks + blockIdx.x] + wofs[wave][d] + local[j];
+            if (dest < n) {  // always true when the histograms agree; never write outside
+                keys_out[dest] = key[j];
+                vals_out[dest] = val[j];
+            }
+        }
+    }
+}
+
+// Per scan tile: sums of T and T*w over the sorted order.
+__global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
+    const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
+    const int32_t *__restrict__ T, int64_t n, int64_t *__restrict__ blkN,
+    double *__restrict__ blkS)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanIPT;
+    int64_t sn = 0;
+    double ss = 0.0;
+    for (int q = 0; q < kScanIPT; ++q) {
+        const int64_t j = base + q;
+        if (j < n) {
+            const int32_t pj = perm[j];
+            const int32_t pi = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
+            const int32_t t = T[pi] < 1 ? 1 : T[pi];
+            sn += t;
+            ss += (double)t * __longlong_as_double((long long)skeys[j]);
+        }
+    }
+    __shared__ int64_t rn[kScanThreads];
+    __shared__ double rs[kScanThreads];
+    rn[threadIdx.x] = sn;
+    rs[threadIdx.x] = ss;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t a = 0;
+        double b = 0.0;
+        for (int q = 0; q < kScanThreads; ++q) {
+            a += rn[q];
+            b += rs[q];
+        }
+        blkN[blockIdx.x] = a;
+        blkS[blockIdx.x] = b;
+    }
+}
+
+// Exclusive scan of the tile sums, in tile order (one thread).
+__global__ void scan_blocks_kernel(int64_t *blkN, double *blkS, int nb)
+{
+    if (threadIdx.x != 0) return;
+    int64_t a = 0;
+    double b = 0.0;
+    for (int q = 0; q < nb; ++q) {
+        const int64_t x = blkN[q];
+        const double y = blkS[q];
+        blkN[q] = a;
+        blkS[q] = b;
+        a += x;
+        b += y;
+    }
+}
+
+// Inclusive prefix within each tile plus the tile's offset; also emits perm.
+__global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
+    const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
+    const int32_t *__restrict__ T, int64_t n, const int64_t *__restrict__ blkN,
+    const double *__restrict__ blkS, int64_t *__restrict__ Nsum, double *__restrict__ Ssum,
+    int32_t *__restrict__ perm_out)
+{
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanIPT;
+    int64_t tn[kScanIPT];
+    double ts[kScanIPT];
+    int64_t sn = 0;
+    double ss = 0.0;
+#pragma unroll
+    for (int q = 0; q < kScanIPT; ++q) {
+        const int64_t j = base + q;
+        if (j < n) {
+            const int32_t pj = perm[j];
+            const int32_t p = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
+            const int32_t t = T[p] < 1 ? 1 : T[p];
+            sn += t;
+            ss += (double)t * __longlong_as_double((long long)skeys[j]);
+            if (perm_out != nullptr) perm_out[j] = p;
+        }
+        tn[q] = sn;
+        ts[q] = ss;
+    }
+    // exclusive scan of the per-thread totals across the block
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    int64_t xn = sn;
+    double xs = ss;
+    for (int off = 1; off < kWave; off <<= 1) {
+        int64_t yn = __shfl_up(xn, off, kWave);
+        double ys = __shfl_up(xs, off, kWave);
+        if (lane >= off) {
+            xn += yn;
+            xs += ys;
+        }
+    }
+    __shared__ int64_t wn[4];
+    __shared__ double wsm[4];
+    if (lane == kWave - 1) {
+        wn[wave] = xn;
+        wsm[wave] = xs;
+    }
+    __syncthreads();
+    int64_t pn = blkN[blockIdx.x];
+    double ps = blkS[blockIdx.x];
+    for (int q = 0; q < wave; ++q) {
+        pn += wn[q];
+        ps += wsm[q];
+    }
+    pn += xn - sn;
+    ps += xs - ss;
+#pragma unroll
+    for (int q = 0; q < kScanIPT; ++q) {
+        const int64_t j = base + q;
+        if (j < n) {
+            Nsum[j] = pn + tn[q];
+            Ssum[j] = ps + ts[q];
+        }
+    }
+}
+
+// Number of sorted waits <= x.
+__device__ __forceinline__ int64_t upper_bound_keys(const uint64_t *__restrict__ skeys, int64_t n,
+                                                    double x)
+{
+    int64_t lo = 0, hi = n;
+    while (lo < hi) {
+        const int64_t mid = lo + (hi - lo) / 2;
+        if (__longlong_as_double((long long)skeys[mid]) <= x) lo = mid + 1;
+        else hi = mid;
+    }
+    return lo;
+}
+
+// One thread per policy (a, k): closed form for every load.
+__global__ void __launch_bounds__(256) closed_form_kernel(const uint64_t *__restrict__ skeys,
+                                                          const int64_t *__restrict__ Nsum,
+                                                          const double *__restrict__ Ssum, int64_t n,
+                                                          Tables tb, PriceDev pr,
+                                                          double *__restrict__ cost)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t f = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (f >= P) return;
+    const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
+    const double t1 = tb.t1[a];
+    const double e = t1 + tb.t2[k];
+    const int64_t p1 = upper_bound_keys(skeys, n, t1);
+    const int64_t pe = upper_bound_keys(skeys, n, e);
+    const int64_t tot = Nsum[n - 1];
+    const int64_t n1 = p1 ? Nsum[p1 - 1] : 0, ne = pe ? Nsum[pe - 1] : 0;
+    const double s1 = p1 ? Ssum[p1 - 1] : 0.0, se = pe ? Ssum[pe - 1] : 0.0;
+    const double hbm = s1 + t1 * (double)(tot - n1);
+    double hold = (se - s1) - t1 * (double)(ne - n1);
+    if (!isinf(e)) hold += (e - t1) * (double)(tot - ne);
+    const double fixed = pr.a1 * hbm + pr.b2 * (double)(ne - n1) + pr.b3 * (double)(tot - ne);
+    const double nd = (double)n;
+    for (int l = 0; l < tb.L; ++l) cost[(int64_t)l * P + f] = (fixed + tb.a2[l] * hold) / nd;
+}
+
+__global__ void zero_u32_kernel(uint32_t *p, int64_t len)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < len) p[i] = 0;
+}
+
+hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, const Tables &tb,
+                              const PriceDev &pr, SortWs &ws, double *cost_out,
+                              int32_t *perm_out, int *status, hipStream_t stream)
+{
+    hipError_t err;
+    hipLaunchKernelGGL(sort_prep_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, stream, w, T,
+                       n, ws.keys[0], ws.vals[0], status);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    int cur = 0;
+    for (int pass = 0; pass < 8; ++pass) {
+        const int shift = 8 * pass;
+        hipLaunchKernelGGL(sort_hist_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
+                           ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+        hipLaunchKernelGGL(scan_u32_kernel, dim3(1), dim3(1024), 0, stream, ws.hist,
+                           (int64_t)256 * ws.nblocks);
+        hipLaunchKernelGGL(sort_scatter_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
+                           ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.nblocks,
+                           ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+        cur ^= 1;
+    }
+    hipLaunchKernelGGL(scan_reduce_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
+                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS);
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(64), 0, stream, ws.blkN, ws.blkS,
+                       ws.nblocks_scan);
+    hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
+                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
+                       perm_out);
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
+                       ws.keys[cur], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
+    return hipGetLastError();
+}
+
+}  // namespace kvr

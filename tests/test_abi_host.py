@@ -1,0 +1,206 @@
+"""C-ABI checks that need no GPU: the library loads, exports exactly what
+include/kvr.h declares, sizes workspaces, and rejects bad arguments with the
+documented status codes before touching the device."""
+import ctypes
+import math
+import os
+import re
+import subprocess
+
+import numpy as np
+import pytest
+
+import paper_2608_30830_amd as kvr
+import workloads
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "kvr.h")
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(kvr.LIB_PATH):
+        from paper_2608_30830_amd import build
+        build.build()
+    return kvr.load_library()
+
+
+def _declared():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(kvr_[a-z_]+)\s*\(", text)))
+
+
+def test_exports_match_header(lib):
+    declared = _declared()
+    assert declared == sorted(kvr.EXPORTS)
+    out = subprocess.run(["nm", "-D", "--defined-only", kvr.LIB_PATH], check=True,
+                         capture_output=True, text=True).stdout
+    exported = sorted(set(re.findall(r"\bT (kvr_[a-z_]+)\b", out)))
+    assert exported == declared
+
+
+def test_status_strings(lib):
+    for code in range(0, -9, -1):
+        s = kvr.status_string(code)
+        assert s and s != "unknown status"
+    assert kvr.status_string(12345) == "unknown status"
+
+
+def test_price_helper_matches_oracle(lib, oracle_mod):
+    """The library's Appendix B helper and the oracle's, written separately,
+    agree to the bit on every workload's platform constants."""
+    for name in ("tiny-exp-1k", "weibull-1m"):
+        wl = workloads.make(name) if name == "tiny-exp-1k" else None
+        kvb = workloads.KV_128K if wl is not None else workloads.KV_320K
+        pf = workloads.PLATFORM
+        a = kvr.kvr_prices_from_platform(kvb, pf["hbm_usable_bytes"], pf["host_link_bytes_per_s"],
+                                         pf["prefill_tokens_per_s"], pf["n_gpu"],
+                                         pf["host_slots_c2"], pf["w_ref_s"])
+        b = oracle_mod.prices_from_platform(kvb, pf["hbm_usable_bytes"],
+                                            pf["host_link_bytes_per_s"],
+                                            pf["prefill_tokens_per_s"], pf["n_gpu"],
+                                            pf["host_slots_c2"], pf["w_ref_s"])
+        assert (a.a1_per_token, a.b2_per_token, a.b3_per_token) == (b.a1, b.b2, b.b3)
+    with pytest.raises(kvr.KvrError) as ei:
+        kvr.kvr_prices_from_platform(0.0, 1, 1, 1)
+    assert ei.value.code == kvr.KVR_E_PRICE
+    with pytest.raises(kvr.KvrError):
+        kvr.kvr_prices_from_platform(float("nan"), 1, 1, 1)
+    assert lib.kvr_prices_from_platform(1, 1, 1, 1, 1, 1, 1, None) == kvr.KVR_E_NULL
+
+
+def _prices():
+    return kvr.kvr_prices_from_platform(131072, 250e9, 50e9, 20000.0)
+
+
+FAKE = ctypes.c_void_p(0x1000)  # never dereferenced: every call below fails on the host
+
+
+def _cost_grid_rc(lib, grid, prices=None, n=100, method=kvr.KVR_BRUTE, perm=None, ws=None,
+                  ws_bytes=0, cost=FAKE):
+    prices = _prices() if prices is None else prices
+    sz = ctypes.c_size_t(ws_bytes)
+    return lib.kvr_cost_grid(FAKE, FAKE, n, ctypes.byref(prices), ctypes.byref(grid.c), method,
+                             cost, perm, ws, ctypes.byref(sz), None), sz.value
+
+
+def test_workspace_size_query(lib):
+    g = kvr.PolicyGrid([0.0], [10.0, 100.0, math.inf], [0.1, 0.5])
+    rc, need = _cost_grid_rc(lib, g)
+    assert rc == kvr.KVR_OK and need > 256
+    rc, need_s = _cost_grid_rc(lib, g, method=kvr.KVR_SORTED, n=1 << 20)
+    assert rc == kvr.KVR_OK and need_s > 20 * (1 << 20)
+    sz = ctypes.c_size_t(0)
+    wl = workloads.make("tiny-exp-1k")
+    g4 = kvr.PolicyGrid(np.geomspace(1, 3600, 64), list(np.geomspace(10, 86400, 256)) + [math.inf],
+                        np.linspace(0.05, 1.0, 32))
+    rc = lib.kvr_bootstrap(None, None, 65536, None, 4096, 65536, ctypes.byref(_prices()),
+                           ctypes.byref(g4.c), None, None, None, None, ctypes.byref(sz), None)
+    assert rc == kvr.KVR_OK
+    # fused selection: candidates of 257 waves x 32 loads per resample, no cost tensor
+    assert 4096 * 257 * 32 * 16 <= sz.value < 4096 * 257 * 32 * 16 * 2
+    del wl
+
+
+BAD_GRIDS = [
+    ([math.nan], [1.0], [0.1], kvr.KVR_E_GRID),
+    ([-1.0], [1.0], [0.1], kvr.KVR_E_GRID),
+    ([math.inf], [1.0], [0.1], kvr.KVR_E_GRID),
+    ([2.0, 1.0], [1.0], [0.1], kvr.KVR_E_GRID),
+    ([1.0, 1.0], [1.0], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [math.nan], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [0.0], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [-5.0], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [math.inf, 5.0], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [5.0, 5.0], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [5.0, math.inf, math.inf], [0.1], kvr.KVR_E_GRID),
+    ([0.0], [5.0], [math.nan], kvr.KVR_E_GRID),
+    ([0.0], [5.0], [-0.5], kvr.KVR_E_GRID),
+    ([0.0], [5.0], [math.inf], kvr.KVR_E_GRID),
+    ([], [5.0], [0.1], kvr.KVR_E_SIZE),
+    ([0.0], [], [0.1], kvr.KVR_E_SIZE),
+    ([0.0], [5.0], [], kvr.KVR_E_SIZE),
+    ([0.0], [5.0], [0.1] * 4097, kvr.KVR_E_SIZE),
+]
+
+
+@pytest.mark.parametrize("case", range(len(BAD_GRIDS)))
+def test_bad_grid_rejected(lib, case):
+    t1, t2, lam, want = BAD_GRIDS[case]
+    g = kvr.PolicyGrid(t1, t2, lam)
+    if not t1 or not t2 or not lam:
+        # an empty array still needs a non-NULL pointer for the size check to be reached
+        g.c.t1 = g.c.t1 if t1 else ctypes.cast(FAKE, ctypes.POINTER(ctypes.c_double))
+        g.c.t2 = g.c.t2 if t2 else ctypes.cast(FAKE, ctypes.POINTER(ctypes.c_double))
+        g.c.lam = g.c.lam if lam else ctypes.cast(FAKE, ctypes.POINTER(ctypes.c_double))
+    assert _cost_grid_rc(lib, g)[0] == want
+
+
+def test_too_many_policies(lib):
+    g = kvr.PolicyGrid([0.0, 1.0], [5.0], [0.1])
+    g.c.n_t1 = 1 << 12
+    g.c.n_t2 = 1 << 13
+    assert _cost_grid_rc(lib, g)[0] == kvr.KVR_E_SIZE
+
+
+@pytest.mark.parametrize("field", ["a1_per_token", "b2_per_token", "b3_per_token",
+                                   "host_slots_c2", "w_ref_s"])
+@pytest.mark.parametrize("value", [0.0, -1.0, math.nan, math.inf])
+def test_bad_price_rejected(lib, field, value):
+    p = _prices()
+    setattr(p, field, value)
+    g = kvr.PolicyGrid([0.0], [5.0], [0.1])
+    assert _cost_grid_rc(lib, g, prices=p)[0] == kvr.KVR_E_PRICE
+
+
+def test_method_and_size_errors(lib):
+    g = kvr.PolicyGrid([0.0], [5.0, math.inf], [0.1])
+    assert _cost_grid_rc(lib, g, method=7)[0] == kvr.KVR_E_METHOD
+    assert _cost_grid_rc(lib, g, method=kvr.KVR_BRUTE, perm=FAKE)[0] == kvr.KVR_E_METHOD
+    assert _cost_grid_rc(lib, g, n=0)[0] == kvr.KVR_E_SIZE
+    assert _cost_grid_rc(lib, g, n=1 << 31)[0] == kvr.KVR_E_SIZE
+    p = _prices()
+    assert lib.kvr_cost_grid(FAKE, FAKE, 10, ctypes.byref(p), ctypes.byref(g.c), 0, FAKE, None,
+                             None, None, None) == kvr.KVR_E_NULL
+    assert lib.kvr_cost_grid(FAKE, FAKE, 10, None, ctypes.byref(g.c), 0, FAKE, None,
+                             None, ctypes.byref(ctypes.c_size_t()), None) == kvr.KVR_E_NULL
+
+
+def test_workspace_errors(lib):
+    g = kvr.PolicyGrid([0.0], [5.0, math.inf], [0.1])
+    rc, need = _cost_grid_rc(lib, g)
+    assert rc == kvr.KVR_OK
+    assert _cost_grid_rc(lib, g, ws=FAKE, ws_bytes=need - 1)[0] == kvr.KVR_E_WORKSPACE
+    assert _cost_grid_rc(lib, g, ws=ctypes.c_void_p(0x1008), ws_bytes=need)[0] == kvr.KVR_E_WORKSPACE
+    # a workspace with a NULL output is a NULL error, not a launch
+    assert _cost_grid_rc(lib, g, ws=FAKE, ws_bytes=need, cost=None)[0] == kvr.KVR_E_NULL
+
+
+def test_bootstrap_and_select_errors(lib):
+    g = kvr.PolicyGrid([0.0], [5.0, math.inf], [0.1])
+    p = _prices()
+    sz = ctypes.c_size_t(0)
+
+    def boot(n=10, R=2, m=10):
+        return lib.kvr_bootstrap(FAKE, FAKE, n, FAKE, R, m, ctypes.byref(p), ctypes.byref(g.c),
+                                 FAKE, FAKE, None, None, ctypes.byref(sz), None)
+
+    assert boot(R=0) == kvr.KVR_E_SIZE
+    assert boot(m=0) == kvr.KVR_E_SIZE
+    assert boot(n=0) == kvr.KVR_E_SIZE
+    assert boot(R=1 << 30, m=1 << 11) == kvr.KVR_E_SIZE
+    assert boot() == kvr.KVR_OK and sz.value > 0
+    sel = lib.kvr_select_policy
+    assert sel(None, 1, 1, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_NULL
+    assert sel(FAKE, 0, 1, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
+    assert sel(FAKE, 1, 0, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
+    assert sel(FAKE, 1, 1, 1, 2, 2, FAKE, FAKE, None, None) == kvr.KVR_E_GRID
+    assert lib.kvr_workspace_status(None, None) == kvr.KVR_E_NULL
+
+
+def test_product_path_has_no_cpu_fallback():
+    """The binding never imports the oracle and has no CPU arithmetic path."""
+    src = open(os.path.join(ROOT, "paper_2608_30830_amd", "__init__.py")).read()
+    assert "oracle" not in src
+    assert "numpy" not in src

@@ -1,0 +1,313 @@
+"""GPU parity: the HIP library (through its C ABI) against the CPU oracle.
+
+Bar: selected policy indices and sort order bit-exact; fp64 costs within
+1e-9 relative.  Where two policies are within rounding of each other in the
+oracle (a gap below 1e-11 relative, far below any real difference in these
+workloads) either pick is accepted and the case is counted and printed.
+"""
+import math
+
+import numpy as np
+import pytest
+
+import workloads
+from tests import helpers as H
+
+pytestmark = pytest.mark.gpu
+
+RTOL = 1e-9          # fp64 cost tolerance
+TIE_RTOL = 1e-11     # rounding-level near tie between two policies
+
+
+@pytest.fixture(scope="module")
+def kvr():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2608_30830_amd as k
+    k.load_library()
+    return k
+
+
+def _dev(x, dtype):
+    import torch
+    return torch.as_tensor(np.ascontiguousarray(x)).to(device="cuda", dtype=dtype)
+
+
+def _lib_prices(kvr, wl):
+    pf = wl.platform
+    return kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
+                                        pf["host_link_bytes_per_s"], pf["prefill_tokens_per_s"],
+                                        pf["n_gpu"], pf["host_slots_c2"], pf["w_ref_s"])
+
+
+def _np(t):
+    return t.detach().cpu().numpy()
+
+
+def assert_costs(gpu, ref, rtol=RTOL):
+    gpu, ref = np.asarray(gpu), np.asarray(ref)
+    assert gpu.shape == ref.shape
+    err = H.rel_err(gpu, ref)
+    worst = np.unravel_index(np.argmax(err), err.shape) if err.size else None
+    assert err.max() <= rtol, f"max rel err {err.max():.3e} at {worst}: {gpu[worst]!r} vs {ref[worst]!r}"
+
+
+def assert_selection(ref_cost, gpu_best, ref_best):
+    """Identical indices, except rounding-level near ties (reported)."""
+    n = H.near_tie_ok(ref_cost, gpu_best, ref_best, TIE_RTOL)
+    if n:
+        print(f"[near-tie] {n} selections differ within {TIE_RTOL:g} relative")
+    return n
+
+
+def run_grid(kvr, wl, method):
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    if method == "sorted":
+        cost, perm = kvr.kvr_cost_grid(w, T, _lib_prices(kvr, wl), g, method=kvr.KVR_SORTED,
+                                       want_perm=True)
+        return _np(cost), _np(perm), g
+    cost = kvr.kvr_cost_grid(w, T, _lib_prices(kvr, wl), g, method=kvr.KVR_BRUTE)
+    return _np(cost), None, g
+
+
+def _f64():
+    import torch
+    return torch.float64
+
+
+def _i32():
+    import torch
+    return torch.int32
+
+
+RANDOM_CASES = [  # seed, n, K1, K2, L, ties  (ragged n, K2 below/at/above one wave)
+    (101, 1, 1, 3, 1, False),
+    (102, 7, 2, 5, 3, True),
+    (103, 129, 1, 63, 5, True),
+    (104, 1000, 3, 64, 17, True),
+    (105, 4097, 2, 65, 33, True),
+    (106, 3001, 1, 130, 40, False),
+    (107, 2500, 4, 70, 9, True),
+    (108, 300, 5, 2, 4, True),
+]
+
+
+@pytest.mark.parametrize("case", RANDOM_CASES, ids=[f"seed{c[0]}" for c in RANDOM_CASES])
+@pytest.mark.parametrize("method", ["brute", "sorted"])
+def test_cost_grid_random(kvr, oracle_mod, case, method):
+    seed, n, k1, k2, L, ties = case
+    wl = workloads.random_case(seed, n, k1, k2, L, ties=ties)
+    cost, perm, g = run_grid(kvr, wl, method)
+    pr = oracle_mod.workload_prices(wl)
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    assert_costs(cost, ref)
+    if perm is not None:
+        assert np.array_equal(perm, oracle_mod.stable_order(wl.wait_s))
+    import torch
+    best, bc, br = kvr.kvr_select_policy(torch.as_tensor(cost).cuda(), g.last_inf)
+    rb, rbc, rbr = oracle_mod.select(ref, wl.t2)
+    assert_selection(ref, _np(best), rb)
+    assert_costs(_np(bc), rbc)
+    if np.array_equal(_np(best), rb):
+        assert np.array_equal(_np(br), rbr)
+
+
+@pytest.mark.parametrize("name", ["tiny-exp-1k", "mix-64k"])
+@pytest.mark.parametrize("method", ["brute", "sorted"])
+def test_cost_grid_workloads(kvr, oracle_mod, name, method):
+    """Full 1,000- and 65,536-wait workloads against the full oracle grid."""
+    wl = workloads.make(name)
+    cost, perm, g = run_grid(kvr, wl, method)
+    pr = oracle_mod.workload_prices(wl)
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    assert_costs(cost, ref)
+    if perm is not None:
+        assert np.array_equal(perm, oracle_mod.stable_order(wl.wait_s))
+    import torch
+    best, _, br = kvr.kvr_select_policy(torch.as_tensor(cost).cuda(), g.last_inf)
+    rb, _, rbr = oracle_mod.select(ref, wl.t2)
+    assert assert_selection(ref, _np(best), rb) == 0
+    print(f"[gap] {name}/{method}: smallest best-vs-runner-up gap {H.min_runner_up_gap(ref):.3e}")
+
+
+def test_tiny_workload_selects_as_the_memoryless_invariant_says(kvr):
+    """The 1,000 exponential waits: retain at 0.25/s, the shortest timer above
+    the threshold load (the same pin the oracle carries)."""
+    wl = workloads.make("tiny-exp-1k")
+    cost, _, g = run_grid(kvr, wl, "brute")
+    import torch
+    best, _, br = kvr.kvr_select_policy(torch.as_tensor(cost).cuda(), g.last_inf)
+    assert list(_np(best)) == [64, 0, 0, 0]
+    assert list(_np(br)) == [kvr.KVR_RETAIN, kvr.KVR_EXPIRE, kvr.KVR_EXPIRE, kvr.KVR_EXPIRE]
+
+
+def test_weibull_1m_sorted_brute_and_sampled_oracle(kvr, oracle_mod):
+    """1,048,576 waits, 1,025 timers, 64 loads: BRUTE and SORTED against the
+    oracle's closed form on the full grid, the double loop on sampled timer
+    columns, and the stable order bit for bit."""
+    wl = workloads.make("weibull-1m")
+    pr = oracle_mod.workload_prices(wl)
+    cb, _, g = run_grid(kvr, wl, "brute")
+    cs, perm, _ = run_grid(kvr, wl, "sorted")
+    ref_perm = oracle_mod.stable_order(wl.wait_s)
+    assert np.array_equal(perm, ref_perm)
+    closed = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                         perm=ref_perm)
+    assert_costs(cb, closed)
+    assert_costs(cs, closed)
+    cols = np.unique(np.concatenate([np.arange(0, wl.t2.size, 97), [wl.t2.size - 2,
+                                                                      wl.t2.size - 1]]))
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2[cols], wl.lam)
+    assert_costs(cb[:, :, cols], ref)
+    assert_costs(cs[:, :, cols], ref)
+    import torch
+    b1 = _np(kvr.kvr_select_policy(torch.as_tensor(cb).cuda(), g.last_inf)[0])
+    b2 = _np(kvr.kvr_select_policy(torch.as_tensor(cs).cuda(), g.last_inf)[0])
+    rb = oracle_mod.select(closed, wl.t2)[0]
+    assert_selection(closed, b1, rb)
+    assert_selection(closed, b2, rb)
+
+
+@pytest.mark.parametrize("case", [(201, 500, 2, 70, 5, 3, None), (202, 1300, 1, 65, 16, 4, 777),
+                                  (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None)])
+def test_bootstrap_random(kvr, oracle_mod, case):
+    seed, n, k1, k2, L, R, m = case
+    wl = workloads.random_case(seed, n, k1, k2, L, resamples=R, m=m, ties=True)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    best, bc, cost = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                       _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g,
+                                       want_cost=True)
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(R):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref, _np(best)[r], rb)
+        assert_costs(_np(bc)[r], rbc)
+    # without the cost tensor the selection is the same
+    best2, bc2 = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                   _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g)
+    assert np.array_equal(_np(best2), _np(best))
+    assert_costs(_np(bc2), _np(bc), rtol=1e-15)
+
+
+def _boot_full(kvr, oracle_mod, name, sample_rows):
+    wl = workloads.make(name)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    best, bc = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                 _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g)
+    best, bc = _np(best), _np(bc)
+    pr = oracle_mod.workload_prices(wl)
+    # every row: the closed form's selection and best cost
+    cb, cbc = oracle_mod.closed_form_bootstrap(wl.wait_s, wl.ctx_tokens, wl.idx, pr, wl.t1,
+                                               wl.t2, wl.lam)
+    assert_costs(bc, cbc)
+    differ = np.argwhere(best != cb)
+    for r, l in differ:
+        # must be a rounding-level tie of the closed form itself
+        assert abs(bc[r, l] - cbc[r, l]) <= TIE_RTOL * abs(cbc[r, l]) + RTOL * abs(cbc[r, l])
+    print(f"[boot] {name}: {len(differ)} of {best.size} selections differ from the closed form")
+    # sampled rows: the double loop, element by element
+    for r in sample_rows:
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref[None], best[r][None], rb[None])
+        assert_costs(bc[r], rbc)
+    return wl
+
+
+def test_bootstrap_1024_full(kvr, oracle_mod):
+    _boot_full(kvr, oracle_mod, "boot-1024x64k", sample_rows=[0, 511, 1023])
+
+
+def test_bootstrap_twotier_4096_full(kvr, oracle_mod):
+    """The two-tier workload at full size, in the launch configuration the
+    benchmark times: all 4,096 rows against the closed form, two rows against
+    the double loop."""
+    _boot_full(kvr, oracle_mod, "twotier-4096x64k", sample_rows=[0, 4095])
+
+
+def test_identity_rows_equal_cost_grid(kvr):
+    """A bootstrap row drawing every sample once in order is the plain grid."""
+    wl = workloads.random_case(301, 5000, 2, 66, 6)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    idx = np.tile(np.arange(wl.n, dtype=np.int32), (3, 1))
+    best, bc, cost = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                       _dev(idx, _i32()), _lib_prices(kvr, wl), g, want_cost=True)
+    plain, _, _ = run_grid(kvr, wl, "brute")
+    for r in range(3):
+        assert np.array_equal(_np(cost)[r], plain)
+
+
+def test_deterministic(kvr):
+    wl = workloads.random_case(302, 30000, 3, 100, 20, resamples=4)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    args = (_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()), _dev(wl.idx, _i32()),
+            _lib_prices(kvr, wl), g)
+    a = kvr.kvr_bootstrap(*args, want_cost=True)
+    b = kvr.kvr_bootstrap(*args, want_cost=True)
+    for x, y in zip(a, b):
+        assert np.array_equal(_np(x), _np(y))
+    c1, _, _ = run_grid(kvr, wl, "sorted")
+    c2, _, _ = run_grid(kvr, wl, "sorted")
+    assert np.array_equal(c1, c2)
+
+
+def test_structural_ties_exact(kvr, oracle_mod):
+    """Waits all below the largest timers: every such timer ties with
+    host-retain exactly, and the tie goes to host-retain (larger index)."""
+    rng = np.random.Generator(np.random.PCG64(9))
+    n = 3000
+    w = rng.uniform(0, 500.0, n)
+    T = rng.integers(1, 30000, n).astype(np.int32)
+    t1 = np.array([0.0, 20.0])
+    t2 = np.concatenate([np.geomspace(1, 2000, 70), [np.inf]])
+    lam = np.array([0.1, 0.3, 0.9, 2.0])
+    wl = workloads.Workload("ties", w, T, t1, t2, lam, float(workloads.KV_128K))
+    cost, _, g = run_grid(kvr, wl, "brute")
+    cs, _, _ = run_grid(kvr, wl, "sorted")
+    tied = t2[:-1] + 20.0 >= w.max()
+    for c in (cost, cs):
+        for a in range(2):
+            for k in np.nonzero(tied)[0]:
+                assert np.array_equal(c[:, a, k], c[:, a, -1])
+    pr = oracle_mod.workload_prices(wl)
+    ref = oracle_mod.cost_grid(w, T, pr, t1, t2, lam)
+    import torch
+    for c in (cost, cs):
+        best = _np(kvr.kvr_select_policy(torch.as_tensor(c).cuda(), 1)[0])
+        assert np.array_equal(best, oracle_mod.select(ref, t2)[0])
+
+
+def test_domain_errors_are_reported(kvr):
+    """Bad samples or indices set the status word; nothing faults."""
+    import torch
+    wl = workloads.random_case(303, 2000, 1, 65, 3, resamples=2)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    pr = _lib_prices(kvr, wl)
+    for bad in ("nan", "neg", "inf"):
+        w = wl.wait_s.copy()
+        w[17] = {"nan": np.nan, "neg": -3.0, "inf": np.inf}[bad]
+        for method in (kvr.KVR_BRUTE, kvr.KVR_SORTED):
+            with pytest.raises(kvr.KvrError) as ei:
+                kvr.kvr_cost_grid(_dev(w, _f64()), _dev(wl.ctx_tokens, _i32()), pr, g,
+                                  method=method)
+            assert ei.value.code == kvr.KVR_E_DOMAIN
+    T = wl.ctx_tokens.copy()
+    T[3] = 0
+    with pytest.raises(kvr.KvrError) as ei:
+        kvr.kvr_cost_grid(_dev(wl.wait_s, _f64()), _dev(T, _i32()), pr, g)
+    assert ei.value.code == kvr.KVR_E_DOMAIN
+    for badidx in (-1, wl.n):
+        idx = wl.idx.copy()
+        idx[1, 5] = badidx
+        with pytest.raises(kvr.KvrError) as ei:
+            kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                              _dev(idx, _i32()), pr, g)
+        assert ei.value.code == kvr.KVR_E_DOMAIN
+    # a clean call afterwards on a fresh workspace reports OK
+    kvr.kvr_cost_grid(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()), pr, g)
+    torch.cuda.synchronize()
