@@ -6,15 +6,22 @@ host-retain) x 32 loads = 1.413e14 (sample, policy, load) cost evaluations,
 with the per-resample selection fused.  Inputs are resident in HBM before
 the timed region.  Prints one JSON line.
 
-The roofline of the dominant kernel (the brute-force grid) is the fp64
-vector ALU: one FMA (2 flops) per evaluation is the algorithmic work; the
-peak is MI355X's 78.6 TFLOP/s fp64 vector rate (256 CUs x 4 SIMDs x 16 lanes
-x 2 flops x 2.4 GHz).  The cpu_baseline leg times the CPU oracle, as it
-stands, on a bounded sample of the same workload.
+The roofline of the dominant kernel (the brute-force grid kernel) is the
+fp64 vector ALU: one FMA (2 flops) per evaluation is the algorithmic work;
+the peak is MI355X's 78.6 TFLOP/s fp64 vector rate (256 CUs x 4 SIMDs x 16
+lanes x 2 flops x 2.4 GHz).  Its duration is taken with HIP events that the
+library records on the launch stream right before and after that kernel.
+The cpu_baseline leg times the CPU oracle, as it stands, on a bounded sample
+of the same workload.
+
+``--copy-calibration`` instead runs one plain device-to-device copy of
+2 GiB, the reference dispatch for scaling the HBM byte counters.
 """
 from __future__ import annotations
 
 import argparse
+import ctypes
+import hashlib
 import json
 import os
 import sys
@@ -25,11 +32,79 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 FP64_PEAK_TFLOPS = 78.6
-HBM_PEAK_GBS = 8000.0
+GRID_SOURCES = ("paper_2608_30830_amd/csrc/kvr_grid.hip",
+                "paper_2608_30830_amd/csrc/kvr_device.h",
+                "paper_2608_30830_amd/csrc/kvr_internal.h")
+COUNTERS_FILE = os.path.join(ROOT, "profiles", "grid_kernel_twotier-4096x64k_counters.txt")
 
 
 def log(msg: str) -> None:
     print(msg, file=sys.stderr, flush=True)
+
+
+def grid_source_hash() -> str:
+    h = hashlib.sha256()
+    for rel in GRID_SOURCES:
+        with open(os.path.join(ROOT, rel), "rb") as fh:
+            h.update(fh.read())
+    return h.hexdigest()
+
+
+def counter_traffic(workload: str, resamples: int):
+    """HBM bytes per launch of the grid kernel from the committed counter
+    summary, or None if it is for another workload or an older kernel."""
+    if not os.path.exists(COUNTERS_FILE):
+        return None
+    kv = {}
+    with open(COUNTERS_FILE) as fh:
+        for line in fh:
+            if ":" in line and not line.startswith("#"):
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+    if kv.get("source_sha256") != grid_source_hash():
+        return None
+    if kv.get("workload") != workload or kv.get("resamples") != str(resamples):
+        return None
+    return float(kv["traffic_bytes_per_launch"])
+
+
+class HipEvents:
+    """Raw hipEvent_t handles (the library records them on its stream)."""
+
+    def __init__(self, count: int):
+        self.hip = ctypes.CDLL("libamdhip64.so")
+        self.hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+        self.hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                 ctypes.c_void_p]
+        self.hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+        self.ev = []
+        for _ in range(count):
+            e = ctypes.c_void_p()
+            if self.hip.hipEventCreate(ctypes.byref(e)) != 0:
+                raise RuntimeError("hipEventCreate failed")
+            self.ev.append(e)
+
+    def elapsed_ms(self, a: int, b: int) -> float:
+        ms = ctypes.c_float()
+        if self.hip.hipEventElapsedTime(ctypes.byref(ms), self.ev[a], self.ev[b]) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return float(ms.value)
+
+    def close(self):
+        for e in self.ev:
+            self.hip.hipEventDestroy(e)
+
+
+def copy_calibration() -> int:
+    import torch
+    n = 1 << 28  # 2 GiB of float64
+    x = torch.empty(n, dtype=torch.float64, device="cuda")
+    y = torch.empty_like(x)
+    torch.cuda.synchronize()
+    y.copy_(x)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_read": 8 * n, "copy_bytes_written": 8 * n}), flush=True)
+    return 0
 
 
 def main() -> int:
@@ -44,18 +119,18 @@ def main() -> int:
     ap.add_argument("--cpu-rows", type=int, default=1,
                     help="bootstrap rows the CPU oracle evaluates for cpu_baseline")
     ap.add_argument("--paths", action="store_true",
-                    help="also time the other paths (sorted closed form, plain grid)")
-    ap.add_argument("--traffic-json", default=os.path.join(ROOT, "profiles", "traffic.json"),
-                    help="HBM bytes per launch of the grid kernel from rocprofv3 counters")
+                    help="also time the other entry points on their workloads")
+    ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
         print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
                                    "(the bootstrap batch would shard by resample with no "
-                                   "exchange, see DESIGN.md)"}))
+                                   "exchange; this build has no multi-GPU path)"}))
         return 2
+    if args.copy_calibration:
+        return copy_calibration()
 
-    import numpy as np
     import torch
 
     import paper_2608_30830_amd as kvr
@@ -76,7 +151,6 @@ def main() -> int:
     idx = torch.as_tensor(wl.idx, dtype=torch.int32).to(dev)
     call = kvr.BootstrapCall(w, T, idx, prices, grid)
     evals = wl.evaluations
-    stream = torch.cuda.current_stream()
 
     log(f"[bench] warmup {args.warmup} step(s)")
     for _ in range(args.warmup):
@@ -87,28 +161,25 @@ def main() -> int:
         raise kvr.KvrError(st, "warmup")
 
     log(f"[bench] timing {args.steps} step(s)")
-    starts = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
-    stops = [torch.cuda.Event(enable_timing=True) for _ in range(args.steps)]
+    ev = HipEvents(2 * args.steps)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for i in range(args.steps):
-        starts[i].record(stream)
+        kvr.kvr_set_profile_events(ev.ev[2 * i].value, ev.ev[2 * i + 1].value)
         call.launch()
-        stops[i].record(stream)
+    kvr.kvr_set_profile_events(None, None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
-    ev_ms = [a.elapsed_time(b) for a, b in zip(starts, stops)]
+    st = call.status()
+    if st != kvr.KVR_OK:
+        raise kvr.KvrError(st, "timed steps")
+    kern_ms = [ev.elapsed_ms(2 * i, 2 * i + 1) for i in range(args.steps)]
+    ev.close()
     ms_per_step = 1000.0 * wall / args.steps
-    launch_ms = sum(ev_ms) / len(ev_ms)
-    log(f"[bench] {ms_per_step:.1f} ms/step wall, {launch_ms:.1f} ms/launch (events)")
+    kernel_ms = sum(kern_ms) / len(kern_ms)
+    log(f"[bench] {ms_per_step:.1f} ms/step wall, grid kernel {kernel_ms:.1f} ms/launch")
 
-    achieved = 2.0 * evals / (launch_ms * 1e-3) / 1e12
-    traffic = None
-    if os.path.exists(args.traffic_json):
-        with open(args.traffic_json) as fh:
-            tj = json.load(fh)
-        if tj.get("workload") == args.workload and tj.get("resamples") == wl.n_resamples:
-            traffic = tj.get("bytes_per_launch")
+    achieved = 2.0 * evals / (kernel_ms * 1e-3) / 1e12
     out = {
         "metric": "sample×policy cost evaluations/sec at 1 GPU; % of HBM/FP64 roofline",
         "value": evals / (ms_per_step * 1e-3),
@@ -128,10 +199,9 @@ def main() -> int:
                    "evaluations_per_step": evals, "method": "brute-force grid, fused selection"},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": FP64_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFLOPS,
-                     "traffic": traffic, "kernel": "grid_kernel<32,true>",
-                     "launch_ms": launch_ms,
-                     "note": "2 flops (one fp64 FMA) per evaluation; launch_ms spans the whole "
-                             "call (grid kernel plus four small kernels)"},
+                     "traffic": counter_traffic(args.workload, wl.n_resamples),
+                     "kernel": "grid_kernel<32,true>", "kernel_ms": kernel_ms,
+                     "flops_per_launch": 2.0 * evals},
     }
 
     if args.paths:
@@ -145,10 +215,14 @@ def main() -> int:
 
 
 def time_paths(kvr, workloads, torch):
-    """Milliseconds per call of the other entry points on their workloads."""
+    """Median milliseconds per call of the other entry points on their
+    workloads (whole call, inputs resident)."""
     res = {}
-    for name, method in (("weibull-1m", kvr.KVR_BRUTE), ("weibull-1m", kvr.KVR_SORTED),
-                         ("mix-64k", kvr.KVR_BRUTE), ("mix-64k", kvr.KVR_SORTED)):
+    cases = (("weibull-1m", kvr.KVR_BRUTE), ("weibull-1m", kvr.KVR_SORTED),
+             ("mix-64k", kvr.KVR_BRUTE), ("mix-64k", kvr.KVR_SORTED),
+             ("tiny-exp-1k", kvr.KVR_BRUTE), ("tiny-exp-1k", kvr.KVR_SORTED),
+             ("boot-1024x64k", None))
+    for name, method in cases:
         wl = workloads.make(name)
         pf = wl.platform
         pr = kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
@@ -157,20 +231,31 @@ def time_paths(kvr, workloads, torch):
         g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
-        out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64, device="cuda")
-        kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out)
-        ws = None
+        if method is None:
+            call = kvr.BootstrapCall(w, T, torch.as_tensor(wl.idx).cuda(), pr, g)
+            run = call.launch
+            key = f"{name}/bootstrap"
+        else:
+            out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
+                              device="cuda")
+            kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out)
+
+            def run(w=w, T=T, pr=pr, g=g, method=method, out=out):
+                kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out, check=False)
+            key = f"{name}/{'sorted' if method == kvr.KVR_SORTED else 'brute'}"
+        run()
+        torch.cuda.synchronize()
         times = []
-        for _ in range(5):
+        for _ in range(7):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out, workspace=ws, check=False)
+            run()
             b.record()
             torch.cuda.synchronize()
             times.append(a.elapsed_time(b))
         ms = sorted(times)[len(times) // 2]
-        key = f"{name}/{'sorted' if method == kvr.KVR_SORTED else 'brute'}"
-        res[key] = {"ms": ms, "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
+        res[key] = {"ms": ms, "evaluations": wl.evaluations,
+                    "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
     return res
 

@@ -38,8 +38,10 @@
  *     With d_ws == NULL they write the required byte count into *ws_bytes,
  *     launch nothing and return KVR_OK; with d_ws != NULL, *ws_bytes must be
  *     at least that count (else KVR_E_WORKSPACE).  d_ws must be 256-byte
- *     aligned.  The library keeps no state between calls; calls on distinct
- *     workspaces may run concurrently from different threads.
+ *     aligned.  Apart from the optional profiling events of
+ *     kvr_set_profile_events, the library keeps no state between calls;
+ *     calls on distinct workspaces may run concurrently from different
+ *     threads.
  *   - Device-detected domain errors (a wait that is NaN, infinite or
  *     negative; a context size below 1; a bootstrap index outside [0, n))
  *     cannot be reported by the return value of an asynchronous call.  The
@@ -174,6 +176,19 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
  * synchronisation or the read failed.  d_ws NULL is KVR_E_NULL.
  */
 int kvr_workspace_status(const void *d_ws, void *hip_stream);
+
+/*
+ * Instrumentation for benchmarks.  After this call, every kvr_cost_grid and
+ * kvr_bootstrap call made from the same host thread records ev_begin (a
+ * hipEvent_t) on its stream right before its main kernel -- the brute-force
+ * grid kernel, or the first kernel of the sorted path -- and ev_end right
+ * after the last kernel of that stage, so hipEventElapsedTime(ev_begin,
+ * ev_end) is that stage's device time.  kvr_set_profile_events(NULL, NULL)
+ * stops it.  These two handles, kept per host thread, are the only state the
+ * library holds between calls; the events stay owned by the caller.
+ * Returns KVR_E_NULL if exactly one of the two is NULL.
+ */
+int kvr_set_profile_events(void *ev_begin, void *ev_end);
 
 /* Static English text for a status code (never NULL). */
 const char *kvr_status_string(int status);

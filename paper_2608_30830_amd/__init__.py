@@ -30,7 +30,8 @@ KVR_RETAIN = 0
 KVR_EXPIRE = 1
 
 EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy",
-           "kvr_bootstrap", "kvr_workspace_status", "kvr_status_string")
+           "kvr_bootstrap", "kvr_workspace_status", "kvr_set_profile_events",
+           "kvr_status_string")
 
 
 class kvr_prices(ctypes.Structure):
@@ -76,6 +77,8 @@ def load_library(path: str = LIB_PATH):
     lib.kvr_bootstrap.restype = ctypes.c_int
     lib.kvr_workspace_status.argtypes = [P, P]
     lib.kvr_workspace_status.restype = ctypes.c_int
+    lib.kvr_set_profile_events.argtypes = [P, P]
+    lib.kvr_set_profile_events.restype = ctypes.c_int
     lib.kvr_status_string.argtypes = [ctypes.c_int]
     lib.kvr_status_string.restype = ctypes.c_char_p
     _lib = lib
@@ -242,6 +245,14 @@ def kvr_bootstrap(wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
     if want_cost:
         return call.best, call.best_cost, call.cost
     return call.best, call.best_cost
+
+
+def kvr_set_profile_events(ev_begin, ev_end) -> None:
+    """Record raw hipEvent_t handles (ints) around the main kernel of later
+    calls from this thread; (None, None) stops."""
+    b = None if ev_begin is None else ctypes.c_void_p(int(ev_begin))
+    e = None if ev_end is None else ctypes.c_void_p(int(ev_end))
+    _check(load_library().kvr_set_profile_events(b, e), "kvr_set_profile_events")
 
 
 def kvr_workspace_status(ws, stream=None) -> int:

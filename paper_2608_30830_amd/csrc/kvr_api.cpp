@@ -23,8 +23,8 @@ constexpr int32_t kMaxLoads = 4096;
 constexpr int64_t kMaxBatch = int64_t(1) << 40;
 constexpr size_t kStatusBytes = 256;
 constexpr int64_t kWavesForSplitless = 2048;   // enough waves to fill the GPU
-constexpr int64_t kTargetWaves = 4096;
-constexpr int64_t kMinSplitChunks = 8;        // samples per split >= 8 chunks
+constexpr int64_t kTargetWaves = 16384;        // many short waves: small tail
+constexpr int64_t kMinSplitChunks = 4;        // samples per split >= 4 chunks
 
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
@@ -178,6 +178,22 @@ int stage_tables(void *ws, size_t off_t1, size_t off_t2, size_t off_a2, int32_t 
     return KVR_OK;
 }
 
+// Optional profiling events of the calling host thread (kvr_set_profile_events).
+thread_local hipEvent_t g_prof_begin = nullptr;
+thread_local hipEvent_t g_prof_end = nullptr;
+
+int prof_mark(hipEvent_t ev, hipStream_t s)
+{
+    if (ev == nullptr) return KVR_OK;
+    return hipEventRecord(ev, s) == hipSuccess ? KVR_OK : KVR_E_HIP;
+}
+
+#define KVR_MARK(ev, s)                          \
+    do {                                         \
+        int rc_ = prof_mark((ev), (s));          \
+        if (rc_ != KVR_OK) return rc_;           \
+    } while (0)
+
 int check_workspace(void *d_ws, size_t have, size_t need)
 {
     if (have < need) return KVR_E_WORKSPACE;
@@ -249,15 +265,19 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
         double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
         KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, status, s));
         double *part = bp.fused ? nullptr : at<double>(d_ws, bp.off_part);
+        KVR_MARK(g_prof_begin, s);
         KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, bp.fused ? d_cost : nullptr, nullptr,
                                  part, status, s));
+        KVR_MARK(g_prof_end, s);
         if (!bp.fused) KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, n, X, G, part, d_cost, s));
         return KVR_OK;
     }
     if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
     kvr::SortWs sws{};
     kvr::sort_ws_carve(at<char>(d_ws, off_sort), n, sws);
+    KVR_MARK(g_prof_begin, s);
     KVR_TRY(kvr::launch_sorted_path(d_wait_s, d_ctx_tokens, n, tb, pr, sws, d_cost, d_perm, status, s));
+    KVR_MARK(g_prof_end, s);
     return KVR_OK;
 }
 
@@ -308,17 +328,29 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     const int64_t P = (int64_t)g->n_t1 * g->n_t2;
     if (bp.fused) {
         kvr::ArgminCand *cand = at<kvr::ArgminCand>(d_ws, bp.off_cand);
+        KVR_MARK(g_prof_begin, s);
         KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, d_cost, cand, nullptr, status, s));
+        KVR_MARK(g_prof_end, s);
         KVR_TRY(kvr::launch_reduce_cands(cand, n_resamples, bp.gp.nblk, g->n_lam, d_best,
                                          d_best_cost, s));
         return KVR_OK;
     }
     double *part = at<double>(d_ws, bp.off_part);
     double *cost = want_cost ? d_cost : at<double>(d_ws, bp.off_cost);
+    KVR_MARK(g_prof_begin, s);
     KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, nullptr, nullptr, part, status, s));
+    KVR_MARK(g_prof_end, s);
     KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, m, X, G, part, cost, s));
     KVR_TRY(kvr::launch_select(cost, n_resamples, g->n_lam, P, g->n_t2, 0, d_best, d_best_cost,
                                nullptr, s));
+    return KVR_OK;
+}
+
+int kvr_set_profile_events(void *ev_begin, void *ev_end)
+{
+    if ((ev_begin == nullptr) != (ev_end == nullptr)) return KVR_E_NULL;
+    g_prof_begin = static_cast<hipEvent_t>(ev_begin);
+    g_prof_end = static_cast<hipEvent_t>(ev_end);
     return KVR_OK;
 }
 

@@ -1,0 +1,242 @@
+// Auxiliary kernels of the calibration replay for gfx950: status and table
+// staging, the per-timer sums X and G, the reduction of sample splits, and the
+// selection kernels (arg-min under the total order "smaller cost, then larger
+// flat index").
+#include "kvr_device.h"
+
+#include <math.h>
+
+namespace kvr {
+
+// ------------------------------------------------------------ small kernels --
+__global__ void clear_status_kernel(int *status)
+{
+    if (threadIdx.x == 0) status[0] = 0;
+}
+
+constexpr int kUploadMax = 384;
+struct UploadPayload {
+    double v[kUploadMax];
+};
+
+// Host tables travel as kernel arguments, so the caller's host buffers are
+// captured at launch and no pinned staging or host synchronisation is needed.
+__global__ void upload_kernel(double *dst, int n, UploadPayload p)
+{
+    for (int i = threadIdx.x; i < n; i += blockDim.x) dst[i] = p.v[i];
+}
+
+hipError_t launch_clear_status(int *status, hipStream_t stream)
+{
+    hipLaunchKernelGGL(clear_status_kernel, dim3(1), dim3(64), 0, stream, status);
+    return hipGetLastError();
+}
+
+hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream)
+{
+    for (int64_t off = 0; off < count; off += kUploadMax) {
+        int c = (int)((count - off) < kUploadMax ? (count - off) : kUploadMax);
+        UploadPayload p;
+        for (int i = 0; i < c; ++i) p.v[i] = host_src[off + i];
+        for (int i = c; i < kUploadMax; ++i) p.v[i] = 0.0;
+        hipLaunchKernelGGL(upload_kernel, dim3(1), dim3(256), 0, stream, dst + off, c, p);
+        hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    return hipSuccess;
+}
+
+// ------------------------------------------------------------------- X, G --
+// X[r][a] = sum_j T*min(w, t1_a), G[r][a] = sum_j T*[w > t1_a] over the
+// samples of resample r.  One 256-thread block per (resample, tile of kAT
+// timers); threads stride over samples, then a fixed-order reduction.
+constexpr int kAT = 8;
+
+__global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, double *X, double *G,
+                                                 int *status)
+{
+    const int natiles = (tb.K1 + kAT - 1) / kAT;
+    const int64_t r = blockIdx.x / natiles;
+    const int a0 = (int)(blockIdx.x % natiles) * kAT;
+    double t1v[kAT], xs[kAT], gs[kAT];
+#pragma unroll
+    for (int q = 0; q < kAT; ++q) {
+        t1v[q] = (a0 + q < tb.K1) ? tb.t1[a0 + q] : 0.0;
+        xs[q] = 0.0;
+        gs[q] = 0.0;
+    }
+    const int64_t row_off = r * src.m;
+    for (int64_t j = threadIdx.x; j < src.m; j += blockDim.x) {
+        Sample s = fetch_sample(src, row_off, j, status);
+#pragma unroll
+        for (int q = 0; q < kAT; ++q) {
+            xs[q] = fma(s.T, fmin(s.w, t1v[q]), xs[q]);
+            gs[q] += (s.w > t1v[q]) ? s.T : 0.0;
+        }
+    }
+    __shared__ double red[4][2 * kAT];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int q = 0; q < kAT; ++q) {
+        double x = wave_sum(xs[q]);
+        double g = wave_sum(gs[q]);
+        if (lane == 0) {
+            red[wave][q] = x;
+            red[wave][kAT + q] = g;
+        }
+    }
+    __syncthreads();
+    if (threadIdx.x < kAT && a0 + (int)threadIdx.x < tb.K1) {
+        const int q = threadIdx.x;
+        double x = ((red[0][q] + red[1][q]) + red[2][q]) + red[3][q];
+        double g = ((red[0][kAT + q] + red[1][kAT + q]) + red[2][kAT + q]) + red[3][kAT + q];
+        X[r * tb.K1 + a0 + q] = x;
+        G[r * tb.K1 + a0 + q] = g;
+    }
+}
+
+hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
+                     int *status, hipStream_t stream)
+{
+    const int natiles = (tb.K1 + kAT - 1) / kAT;
+    hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * natiles)), dim3(256), 0, stream, src, tb, X,
+                       G, status);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------- split reduce, finalize --
+// Partials are laid out [split][resample][tile][value][policy] with LT load
+// accumulators and the recompute weight R3 as values.  Stage 1: one thread per
+// element of split 0 sums it over the splits, in split order, in place.
+__global__ void __launch_bounds__(256) reduce_splits_kernel(int64_t nsplit, int64_t slice,
+                                                            double *__restrict__ partials)
+{
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= slice) return;
+    double s = partials[gid];
+    for (int64_t q = 1; q < nsplit; ++q) s += partials[q * slice + gid];
+    partials[gid] = s;
+}
+
+// Stage 2: one thread per (resample, tile, policy) turns the sums into mean
+// costs, with the same expression the fused grid kernel uses.
+template <int LT>
+__global__ void __launch_bounds__(256) finalize_kernel(GridPlan plan, Tables tb, PriceDev pr,
+                                                       double md, const double *__restrict__ X,
+                                                       const double *__restrict__ G,
+                                                       const double *__restrict__ sums,
+                                                       double *__restrict__ cost_out)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (gid >= plan.R * plan.ntiles * P) return;
+    const int64_t f = gid % P;
+    const int tile = (int)((gid / P) % plan.ntiles);
+    const int64_t r = gid / (P * plan.ntiles);
+    const int a = (int)(f / tb.K2);
+    const int64_t base_row = (r * plan.ntiles + tile) * (LT + 1);
+    const double r3 = sums[(base_row + LT) * P + f];
+    const double base = pr.a1 * X[r * tb.K1 + a] + (pr.b2 * (G[r * tb.K1 + a] - r3) + pr.b3 * r3);
+#pragma unroll
+    for (int l = 0; l < LT; ++l) {
+        const int lg = tile * LT + l;
+        if (lg < tb.L) cost_out[(r * tb.L + lg) * P + f] = (base + sums[(base_row + l) * P + f]) / md;
+    }
+}
+
+hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
+                                  int64_t m, const double *X, const double *G,
+                                  double *partials, double *cost_out, hipStream_t stream)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t slice = plan.R * plan.ntiles * (int64_t)(plan.LT + 1) * P;
+    hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((slice + 255) / 256)), dim3(256), 0,
+                       stream, (int64_t)plan.nsplit, slice, partials);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    const int64_t threads = plan.R * plan.ntiles * P;
+    const unsigned blocks = (unsigned)((threads + 255) / 256);
+    const double md = (double)m;
+    switch (plan.LT) {
+    case 4: hipLaunchKernelGGL(finalize_kernel<4>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
+    case 8: hipLaunchKernelGGL(finalize_kernel<8>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
+    case 16: hipLaunchKernelGGL(finalize_kernel<16>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
+    case 32: hipLaunchKernelGGL(finalize_kernel<32>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
+    default: return hipErrorInvalidValue;
+    }
+    return hipGetLastError();
+}
+
+// ------------------------------------------------------- selection kernels --
+// Per (resample, load): best of the per-wave candidates.  One wave per row.
+__global__ void __launch_bounds__(256) reduce_cands_kernel(const ArgminCand *__restrict__ cand,
+                                                           int64_t rows, int nblk, int L,
+                                                           int32_t *__restrict__ best,
+                                                           double *__restrict__ best_cost)
+{
+    const int64_t row = (int64_t)blockIdx.x * 4 + threadIdx.x / kWave;
+    const int lane = threadIdx.x % kWave;
+    if (row >= rows) return;
+    const int64_t r = row / L;
+    const int l = (int)(row % L);
+    double bc = INFINITY;
+    int32_t bf = -1;
+    for (int b = lane; b < nblk; b += kWave) {
+        const ArgminCand c = cand[(r * nblk + b) * L + l];
+        argmin_merge(bc, bf, c.cost, c.f);
+    }
+    wave_argmin(bc, bf);
+    if (lane == 0) {
+        best[row] = bf;
+        best_cost[row] = bc;
+    }
+}
+
+hipError_t launch_reduce_cands(const ArgminCand *cand, int64_t R, int nblk, int L, int32_t *best,
+                               double *best_cost, hipStream_t stream)
+{
+    const int64_t rows = R * L;
+    hipLaunchKernelGGL(reduce_cands_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
+                       cand, rows, nblk, L, best, best_cost);
+    return hipGetLastError();
+}
+
+// Per (batch, load) row of P costs: one 256-thread block per row.
+__global__ void __launch_bounds__(256) select_kernel(const double *__restrict__ cost, int64_t P,
+                                                     int K2, int last_inf,
+                                                     int32_t *__restrict__ best,
+                                                     double *__restrict__ best_cost,
+                                                     int32_t *__restrict__ branch)
+{
+    const int64_t row = blockIdx.x;
+    const double *c = cost + row * P;
+    double bc = INFINITY;
+    int32_t bf = -1;
+    for (int64_t f = threadIdx.x; f < P; f += blockDim.x) argmin_merge(bc, bf, c[f], (int32_t)f);
+    wave_argmin(bc, bf);
+    __shared__ double sc[4];
+    __shared__ int32_t sf[4];
+    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+    if (lane == 0) {
+        sc[wave] = bc;
+        sf[wave] = bf;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        for (int q = 1; q < 4; ++q) argmin_merge(bc, bf, sc[q], sf[q]);
+        best[row] = bf;
+        best_cost[row] = bc;
+        if (branch != nullptr) branch[row] = (last_inf && (bf % K2) == K2 - 1) ? 0 : 1;
+    }
+}
+
+hipError_t launch_select(const double *cost, int64_t batch, int L, int64_t P, int K2, int last_inf,
+                         int32_t *best, double *best_cost, int32_t *branch, hipStream_t stream)
+{
+    const int64_t rows = batch * L;
+    hipLaunchKernelGGL(select_kernel, dim3((unsigned)rows), dim3(256), 0, stream, cost, P, K2,
+                       last_inf, best, best_cost, branch);
+    return hipGetLastError();
+}
+
+}  // namespace kvr

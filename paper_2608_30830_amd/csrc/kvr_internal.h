@@ -61,9 +61,10 @@ hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &p
                        double *cost_out, ArgminCand *cand, double *partials, int *status,
                        hipStream_t stream);
 
+// Sums the split partials in place (split order) and writes mean costs.
 hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
                                   int64_t m, const double *X, const double *G,
-                                  const double *partials, double *cost_out, hipStream_t stream);
+                                  double *partials, double *cost_out, hipStream_t stream);
 
 hipError_t launch_reduce_cands(const ArgminCand *cand, int64_t R, int nblk, int L,
                                int32_t *best, double *best_cost, hipStream_t stream);

@@ -16,7 +16,7 @@
 // ranking scatter); no inter-workgroup waiting, so no forward-progress
 // assumption.  Ranking inside a tile is stable: a wave ranks its keys with a
 // ballot match on the digit, in input order.
-#include "kvr_internal.h"
+#include "kvr_device.h"
 
 namespace kvr {
 
@@ -68,11 +68,6 @@ void sort_ws_carve(void *base, int64_t n, SortWs &ws)
     ws.blkS = (double *)take(sizeof(double) * ws.nblocks_scan);
 }
 
-__device__ __forceinline__ void flag_domain_s(int *status)
-{
-    __hip_atomic_store(status, kStatusDomain, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-}
-
 // Keys from waits (domain-checked on the bits), identity payload.
 __global__ void __launch_bounds__(256) sort_prep_kernel(const double *__restrict__ w,
                                                         const int32_t *__restrict__ T, int64_t n,
@@ -84,10 +79,10 @@ __global__ void __launch_bounds__(256) sort_prep_kernel(const double *__restrict
     uint64_t b = (uint64_t)__double_as_longlong(w[i]);
     if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
     if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
-        flag_domain_s(status);
+        flag_domain(status);
         b = 0;
     }
-    if (T[i] < 1) flag_domain_s(status);
+    if (T[i] < 1) flag_domain(status);
     keys[i] = b;
     vals[i] = (int32_t)i;
 }
