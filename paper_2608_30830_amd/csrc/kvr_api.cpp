@@ -22,12 +22,26 @@ constexpr int64_t kMaxPolicies = int64_t(1) << 24;
 constexpr int32_t kMaxLoads = 4096;
 constexpr int64_t kMaxBatch = int64_t(1) << 40;
 constexpr size_t kStatusBytes = 256;
-constexpr int64_t kWavesForSplitless = 2048;   // enough waves to fill the GPU
-constexpr int64_t kTargetWaves = 16384;        // many short waves: small tail
-constexpr int64_t kMinSplitChunks = 4;        // samples per split >= 4 chunks
-
 size_t align256(size_t x) { return (x + 255) & ~size_t(255); }
 int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
+
+// Sample splits per resample for the grid kernel (measured on MI355X: 1,024
+// SIMDs, 4 resident grid waves each).  With at least 32K waves already there
+// is no split (the selection is fused into the grid kernel).  Otherwise the
+// samples are cut into splits of >= 4,096 samples, or of >= 512 samples when
+// that is what it takes to give every resident slot a wave; never more than
+// 16 rounds of waves, and never more than 1 GiB of split partials.
+int64_t choose_splits(int64_t base_waves, int64_t m, int64_t partial_doubles_per_split)
+{
+    constexpr int64_t kSlots = 4096, kFull = 32768, kMaxRounds = 16;
+    if (base_waves >= kFull) return 1;
+    int64_t ns = std::max<int64_t>(1, m / 4096);
+    if (base_waves * ns < kSlots)
+        ns = std::max<int64_t>(1, std::min<int64_t>(m / 512, cdiv(kSlots, base_waves)));
+    ns = std::min<int64_t>(ns, cdiv(kMaxRounds * kSlots, base_waves));
+    const int64_t mem_cap = std::max<int64_t>(1, (int64_t(1) << 30) / 8 / partial_doubles_per_split);
+    return std::max<int64_t>(1, std::min<int64_t>(ns, mem_cap));
+}
 
 bool pos_finite(double x) { return std::isfinite(x) && x > 0.0; }
 
@@ -82,7 +96,7 @@ struct BrutePlan {
     int32_t Lpad;
     bool fused;              // nsplit == 1: costs finalised inside the grid kernel
     // workspace offsets
-    size_t off_t1, off_t2, off_a2, off_X, off_G, off_cand, off_part, off_cost, total;
+    size_t off_t1, off_t2, off_a2, off_X, off_G, off_xgp, off_cand, off_part, off_cost, total;
 };
 
 int choose_tile(int32_t L)
@@ -112,15 +126,16 @@ BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bo
     gp.nblk = (int)cdiv(P, kvr::kWave);
     gp.R = R;
     bp.Lpad = gp.ntiles * gp.LT;
-    const int64_t base_waves = R * gp.nblk * gp.ntiles;
-    int64_t nsplit = 1;
-    if (base_waves < kWavesForSplitless) {
-        const int64_t max_split = std::max<int64_t>(1, m / (kMinSplitChunks * kvr::kChunk));
-        nsplit = std::min<int64_t>(cdiv(kTargetWaves, base_waves), max_split);
-        if (nsplit < 1) nsplit = 1;
-    }
-    int64_t split_len = cdiv(cdiv(m, nsplit), kvr::kChunk) * kvr::kChunk;
-    nsplit = cdiv(m, split_len);
+    // a group of 64 lanes spans at most two t1 rows only when K2 >= 64; it never
+    // straddles a resample when P is a multiple of 64 or there is one resample
+    if (K2 < kvr::kWave) gp.mode = kvr::kModePerLane;
+    else if (P % kvr::kWave == 0 || R == 1) gp.mode = kvr::kModeRows1;
+    else gp.mode = kvr::kModeRows2;
+    gp.ngroups = (gp.mode == kvr::kModePerLane) ? R * gp.nblk : cdiv(R * P, kvr::kWave);
+    const int64_t base_waves = gp.ngroups * gp.ntiles;
+    const int64_t target = choose_splits(base_waves, m, R * gp.ntiles * (gp.LT + 1) * P);
+    const int64_t split_len = cdiv(cdiv(m, target), kvr::kChunk) * kvr::kChunk;
+    const int64_t nsplit = cdiv(m, split_len);
     gp.nsplit = (int)nsplit;
     gp.split_len = split_len;
     bp.fused = (nsplit == 1);
@@ -136,9 +151,12 @@ BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bo
     bp.off_a2 = take(sizeof(double) * bp.Lpad);
     bp.off_X = take(sizeof(double) * R * K1);
     bp.off_G = take(sizeof(double) * R * K1);
+    int64_t part_len = 0;
+    const int parts = kvr::xg_parts(R, K1, m, &part_len);
+    bp.off_xgp = take(sizeof(double) * 2 * parts * R * K1);
     bp.off_cand = bp.off_part = bp.off_cost = 0;
     if (bp.fused) {
-        if (bootstrap) bp.off_cand = take(sizeof(kvr::ArgminCand) * R * gp.nblk * L);
+        if (bootstrap) bp.off_cand = take(sizeof(kvr::ArgminCand) * gp.ngroups * 2 * L);
     } else {
         bp.off_part = take(sizeof(double) * nsplit * R * gp.ntiles * (gp.LT + 1) * P);
         if (bootstrap && !want_cost) bp.off_cost = take(sizeof(double) * R * L * P);
@@ -263,7 +281,7 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
             return rc;
         SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
         double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
-        KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, status, s));
+        KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, at<double>(d_ws, bp.off_xgp), status, s));
         double *part = bp.fused ? nullptr : at<double>(d_ws, bp.off_part);
         KVR_MARK(g_prof_begin, s);
         KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, bp.fused ? d_cost : nullptr, nullptr,
@@ -324,15 +342,14 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
         return rc;
     SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
     double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
-    KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, status, s));
+    KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, at<double>(d_ws, bp.off_xgp), status, s));
     const int64_t P = (int64_t)g->n_t1 * g->n_t2;
     if (bp.fused) {
         kvr::ArgminCand *cand = at<kvr::ArgminCand>(d_ws, bp.off_cand);
         KVR_MARK(g_prof_begin, s);
         KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, d_cost, cand, nullptr, status, s));
         KVR_MARK(g_prof_end, s);
-        KVR_TRY(kvr::launch_reduce_cands(cand, n_resamples, bp.gp.nblk, g->n_lam, d_best,
-                                         d_best_cost, s));
+        KVR_TRY(kvr::launch_reduce_cands(cand, bp.gp, P, g->n_lam, d_best, d_best_cost, s));
         return KVR_OK;
     }
     double *part = at<double>(d_ws, bp.off_part);

@@ -49,15 +49,20 @@ hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hip
 // ------------------------------------------------------------------- X, G --
 // X[r][a] = sum_j T*min(w, t1_a), G[r][a] = sum_j T*[w > t1_a] over the
 // samples of resample r.  One 256-thread block per (resample, tile of kAT
-// timers); threads stride over samples, then a fixed-order reduction.
+// timers, sample part); threads stride over the part's samples, then a
+// fixed-order reduction.  With several parts the block writes a partial pair
+// to xgp[part][r][a][2] and xg_reduce_kernel adds the parts in part order.
 constexpr int kAT = 8;
 
-__global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, double *X, double *G,
-                                                 int *status)
+__global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, int parts,
+                                                 int64_t part_len, double *X, double *G,
+                                                 double *xgp, int *status)
 {
     const int natiles = (tb.K1 + kAT - 1) / kAT;
-    const int64_t r = blockIdx.x / natiles;
-    const int a0 = (int)(blockIdx.x % natiles) * kAT;
+    const int part = (int)(blockIdx.x % parts);
+    const int64_t rest = blockIdx.x / parts;
+    const int64_t r = rest / natiles;
+    const int a0 = (int)(rest % natiles) * kAT;
     double t1v[kAT], xs[kAT], gs[kAT];
 #pragma unroll
     for (int q = 0; q < kAT; ++q) {
@@ -66,7 +71,9 @@ __global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, doubl
         gs[q] = 0.0;
     }
     const int64_t row_off = r * src.m;
-    for (int64_t j = threadIdx.x; j < src.m; j += blockDim.x) {
+    const int64_t j0 = (int64_t)part * part_len;
+    const int64_t j1 = (j0 + part_len < src.m) ? j0 + part_len : src.m;
+    for (int64_t j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
         Sample s = fetch_sample(src, row_off, j, status);
 #pragma unroll
         for (int q = 0; q < kAT; ++q) {
@@ -90,17 +97,62 @@ __global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, doubl
         const int q = threadIdx.x;
         double x = ((red[0][q] + red[1][q]) + red[2][q]) + red[3][q];
         double g = ((red[0][kAT + q] + red[1][kAT + q]) + red[2][kAT + q]) + red[3][kAT + q];
-        X[r * tb.K1 + a0 + q] = x;
-        G[r * tb.K1 + a0 + q] = g;
+        const int64_t ra = r * tb.K1 + a0 + q;
+        if (parts == 1) {
+            X[ra] = x;
+            G[ra] = g;
+        } else {
+            const int64_t R = (int64_t)gridDim.x / parts / natiles;
+            xgp[2 * ((int64_t)part * R * tb.K1 + ra)] = x;
+            xgp[2 * ((int64_t)part * R * tb.K1 + ra) + 1] = g;
+        }
     }
 }
 
+// One thread per (resample, timer): adds the parts in part order.
+__global__ void __launch_bounds__(256) xg_reduce_kernel(int parts, int64_t RK1,
+                                                        const double *__restrict__ xgp,
+                                                        double *__restrict__ X,
+                                                        double *__restrict__ G)
+{
+    const int64_t ra = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (ra >= RK1) return;
+    double x = 0.0, g = 0.0;
+    for (int p = 0; p < parts; ++p) {
+        x += xgp[2 * ((int64_t)p * RK1 + ra)];
+        g += xgp[2 * ((int64_t)p * RK1 + ra) + 1];
+    }
+    X[ra] = x;
+    G[ra] = g;
+}
+
+int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len)
+{
+    const int64_t natiles = (K1 + kAT - 1) / kAT;
+    int64_t parts = 1;
+    if (R * natiles < 1024) {
+        parts = (1024 + R * natiles - 1) / (R * natiles);
+        const int64_t most = (m + 4095) / 4096;  // at least 4,096 samples per part
+        if (parts > most) parts = most;
+        if (parts < 1) parts = 1;
+    }
+    *part_len = (m + parts - 1) / parts;
+    return (int)((m + *part_len - 1) / *part_len);
+}
+
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     int *status, hipStream_t stream)
+                     double *xgp, int *status, hipStream_t stream)
 {
     const int natiles = (tb.K1 + kAT - 1) / kAT;
-    hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * natiles)), dim3(256), 0, stream, src, tb, X,
-                       G, status);
+    int64_t part_len = 0;
+    const int parts = xg_parts(R, tb.K1, src.m, &part_len);
+    hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * natiles * parts)), dim3(256), 0, stream, src,
+                       tb, parts, part_len, X, G, xgp, status);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess || parts == 1) return err;
+    const int64_t RK1 = R * tb.K1;
+    hipLaunchKernelGGL(xg_reduce_kernel, dim3((unsigned)((RK1 + 255) / 256)), dim3(256), 0, stream,
+                       parts, RK1, xgp, X, G);
     return hipGetLastError();
 }
 
@@ -169,8 +221,13 @@ hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const 
 
 // ------------------------------------------------------- selection kernels --
 // Per (resample, load): best of the per-wave candidates.  One wave per row.
+// The groups holding resample r's policies are r*nblk .. (r+1)*nblk-1 (one
+// resample per group), or, for groups over the flattened (resample, policy)
+// space, those covering flat indices r*P .. r*P + P - 1, where r sits in slot
+// 0 if it is the group's first resample and in slot 1 otherwise.
 __global__ void __launch_bounds__(256) reduce_cands_kernel(const ArgminCand *__restrict__ cand,
-                                                           int64_t rows, int nblk, int L,
+                                                           int64_t rows, int per_lane, int nblk,
+                                                           int64_t P, int L,
                                                            int32_t *__restrict__ best,
                                                            double *__restrict__ best_cost)
 {
@@ -179,10 +236,19 @@ __global__ void __launch_bounds__(256) reduce_cands_kernel(const ArgminCand *__r
     if (row >= rows) return;
     const int64_t r = row / L;
     const int l = (int)(row % L);
+    int64_t g0, g1;
+    if (per_lane) {
+        g0 = r * nblk;
+        g1 = g0 + nblk - 1;
+    } else {
+        g0 = (r * P) / kWave;
+        g1 = (r * P + P - 1) / kWave;
+    }
     double bc = INFINITY;
     int32_t bf = -1;
-    for (int b = lane; b < nblk; b += kWave) {
-        const ArgminCand c = cand[(r * nblk + b) * L + l];
+    for (int64_t g = g0 + lane; g <= g1; g += kWave) {
+        const int slot = (per_lane || (g * kWave) / P == r) ? 0 : 1;
+        const ArgminCand c = cand[(g * 2 + slot) * L + l];
         argmin_merge(bc, bf, c.cost, c.f);
     }
     wave_argmin(bc, bf);
@@ -192,12 +258,13 @@ __global__ void __launch_bounds__(256) reduce_cands_kernel(const ArgminCand *__r
     }
 }
 
-hipError_t launch_reduce_cands(const ArgminCand *cand, int64_t R, int nblk, int L, int32_t *best,
-                               double *best_cost, hipStream_t stream)
+hipError_t launch_reduce_cands(const ArgminCand *cand, const GridPlan &plan, int64_t P, int L,
+                               int32_t *best, double *best_cost, hipStream_t stream)
 {
-    const int64_t rows = R * L;
+    const int64_t rows = plan.R * L;
     hipLaunchKernelGGL(reduce_cands_kernel, dim3((unsigned)((rows + 3) / 4)), dim3(256), 0, stream,
-                       cand, rows, nblk, L, best, best_cost);
+                       cand, rows, plan.mode == kModePerLane ? 1 : 0, plan.nblk, P, L, best,
+                       best_cost);
     return hipGetLastError();
 }
 

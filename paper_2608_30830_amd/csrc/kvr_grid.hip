@@ -12,13 +12,13 @@
 // computed once per (sample, policy); terms that depend only on t1 (X, G) once
 // per (sample, t1) by xg_kernel.
 //
-// Layout: one wave owns 64 consecutive policies (lane = flat policy index
-// f = a*K2 + k) of one resample and one tile of up to 32 loads.  The samples
-// are streamed through LDS in chunks of kChunk and read back as wave-uniform
-// broadcasts, so each lane accumulates its own policy over the whole sample
-// in a fixed order; no cross-lane reduction of costs is needed, and every
-// policy of a call is summed in exactly the same order, which keeps policies
-// with identical per-sample terms bit-identical (structural ties stay exact).
+// Layout: one wave owns 64 consecutive policies (lane = one policy of one
+// resample) and one tile of up to 32 loads.  The samples are streamed through
+// LDS in chunks and read back as wave-uniform broadcasts, so each lane
+// accumulates its own policy over the whole sample in a fixed order; no
+// cross-lane reduction of costs is needed, and every policy of a call is
+// summed in exactly the same order, which keeps policies with identical
+// per-sample terms bit-identical (structural ties stay exact).
 // No MFMA: nothing here is a dense contraction.
 #include "kvr_device.h"
 
@@ -27,13 +27,20 @@
 namespace kvr {
 
 // ------------------------------------------------------------- grid kernel --
-// ROWPAIR: K2 >= 64, so the 64 consecutive policies of a wave lie in at most
-// two timer rows a0, a0+1.  The t1-dependent part of h, d = max(w,t1) - t1,
-// is computed once per staged sample for both rows and each lane reads its
-// row's copy from LDS.  Otherwise (K2 < 64) every lane computes d itself.
+// Modes (chosen on the host, see GridPlan::mode):
+//  kModePerLane  K2 < 64.  Groups of 64 policies of one resample; every lane
+//                computes d = max(w,t1) - t1 itself.
+//  kModeRows1    K2 >= 64, groups over the flattened (resample, policy) space
+//                that never straddle a resample.  A group's 64 policies lie
+//                in at most two (resample, t1-row) combinations; d is
+//                computed once per staged sample for both and each lane reads
+//                its combination's copy from LDS.
+//  kModeRows2    As kModeRows1, but a group may straddle two resamples (the
+//                policy count is not a multiple of 64): two sample streams are
+//                staged, one per resample, with half-size chunks.
 // Rounding note: min(fl(max(w,t1) - t1), fl(e - t1)) equals
 // fl(min(max(w,t1), e) - t1) because rounding is monotone.
-template <int LT, bool ROWPAIR>
+template <int LT, int MODE>
 __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, PriceDev pr,
                                                      GridPlan plan, const double *__restrict__ X,
                                                      const double *__restrict__ G,
@@ -42,32 +49,52 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
                                                      double *__restrict__ partials, int *status,
                                                      int64_t nlogical)
 {
-    __shared__ double2 wt[2][kChunk];     // (w, T) per staged sample
-    __shared__ double2 dd[2][kChunk];     // (d for row a0, d for row a0+1)
+    constexpr bool kStaged = MODE != kModePerLane;
+    constexpr bool kTwo = MODE == kModeRows2;
+    constexpr int kCh = kTwo ? kChunk / 2 : kChunk;   // samples per staged chunk
+    constexpr int kPer = kCh / kWave;                  // samples each lane stages per stream
+    __shared__ double2 wt[2][kTwo ? 2 : 1][kCh];        // (w, T) per stream
+    __shared__ double2 dd[2][kStaged ? kCh : 1];        // (d for combination A, for B)
 
     const int64_t logical = xcd_logical_block(blockIdx.x, nlogical);
-    const int blk = (int)(logical % plan.nblk);
-    int64_t rest = logical / plan.nblk;
-    const int tile = (int)(rest % plan.ntiles);
-    rest /= plan.ntiles;
+    const int tile = (int)(logical % plan.ntiles);
+    int64_t rest = logical / plan.ntiles;
     const int split = (int)(rest % plan.nsplit);
-    const int64_t r = rest / plan.nsplit;
+    const int64_t grp = rest / plan.nsplit;
 
     const int lane = threadIdx.x;
     const int64_t P = (int64_t)tb.K1 * tb.K2;
-    const int64_t f0 = (int64_t)blk * kWave;
-    const int64_t f = f0 + lane;
-    const bool valid = f < P;
-    const int a = valid ? (int)(f / tb.K2) : (int)(f0 / tb.K2);
-    const int k = valid ? (int)(f % tb.K2) : 0;
+    const int64_t RP = plan.R * P;
+    int64_t r, f;
+    bool valid;
+    int64_t FA = 0, FB = 0;
+    if (MODE == kModePerLane) {
+        r = grp / plan.nblk;
+        const int64_t f0 = (grp % plan.nblk) * kWave;
+        f = f0 + lane;
+        valid = f < P;
+        if (!valid) f = f0;
+    } else {
+        FA = grp * kWave;
+        FB = (FA + kWave - 1 < RP) ? FA + kWave - 1 : RP - 1;
+        int64_t F = FA + lane;
+        valid = F < RP;
+        if (!valid) F = FB;
+        r = F / P;
+        f = F % P;
+    }
+    const int a = (int)(f / tb.K2);
+    const int k = (int)(f % tb.K2);
     const double t1 = tb.t1[a];
-    const double e = valid ? t1 + tb.t2[k] : t1;   // deadline from suspension
-    const double ep = e - t1;                       // host time before discard
-    // rows staged for this wave
-    const int a0 = (int)(f0 / tb.K2);
-    const int a1r = (a0 + 1 < tb.K1) ? a0 + 1 : a0;
-    const double t1A = tb.t1[a0], t1B = tb.t1[a1r];
-    const int sel = (a != a0) ? 1 : 0;
+    const double e = t1 + tb.t2[k];   // deadline from suspension
+    const double ep = e - t1;         // host time before discard
+    // the (resample, t1-row) combinations of this group
+    const int64_t rA = FA / P, rB = FB / P;
+    const int aA = (int)((FA % P) / tb.K2), aB = (int)((FB % P) / tb.K2);
+    const double t1A = tb.t1[aA], t1B = tb.t1[aB];
+    const int sel = (r == rA && a == aA) ? 0 : 1;      // which staged d
+    const int stream = (kTwo && r != rA) ? 1 : 0;      // which staged (w, T)
+    const bool twoStreams = kTwo && rB != rA;
 
     double a2[LT], acc[LT];
 #pragma unroll
@@ -80,20 +107,23 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
     const int64_t j0 = (int64_t)split * plan.split_len;
     int64_t j1 = j0 + plan.split_len;
     if (j1 > src.m) j1 = src.m;
-    const int64_t nch = (j1 - j0 + kChunk - 1) / kChunk;
-    const int64_t row_off = r * src.m;
+    const int64_t nch = (j1 - j0 + kCh - 1) / kCh;
+    const int64_t offA = (kStaged ? rA : r) * src.m;   // index-row offsets of the streams
+    const int64_t offB = rB * src.m;
 
-    constexpr int kPer = kChunk / kWave;
-    Sample pre[kPer];
+    Sample preA[kPer], preB[kPer];
     auto load_chunk = [&](int64_t c) {
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
-            int64_t j = j0 + c * kChunk + q * kWave + lane;
+            const int64_t j = j0 + c * kCh + q * kWave + lane;
             if (j < j1) {
-                pre[q] = fetch_sample(src, row_off, j, status);
+                preA[q] = fetch_sample(src, offA, j, status);
+                if (twoStreams) preB[q] = fetch_sample(src, offB, j, status);
+                else preB[q] = preA[q];
             } else {  // padding: contributes exact zeros
-                pre[q].w = 0.0;
-                pre[q].T = 0.0;
+                preA[q].w = 0.0;
+                preA[q].T = 0.0;
+                preB[q] = preA[q];
             }
         }
     };
@@ -101,9 +131,10 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             const int s = q * kWave + lane;
-            wt[b][s] = make_double2(pre[q].w, pre[q].T);
-            if (ROWPAIR)
-                dd[b][s] = make_double2(fmax(pre[q].w, t1A) - t1A, fmax(pre[q].w, t1B) - t1B);
+            wt[b][0][s] = make_double2(preA[q].w, preA[q].T);
+            if (kTwo) wt[b][kTwo ? 1 : 0][s] = make_double2(preB[q].w, preB[q].T);
+            if (kStaged)
+                dd[b][s] = make_double2(fmax(preA[q].w, t1A) - t1A, fmax(preB[q].w, t1B) - t1B);
         }
     };
 
@@ -115,12 +146,13 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
     for (int64_t c = 0; c < nch; ++c) {
         const int cur = (int)(c & 1);
         if (c + 1 < nch) load_chunk(c + 1);
+        const double2 *wrow = &wt[cur][stream][0];   // uniform unless two streams
         const double *drow = reinterpret_cast<const double *>(&dd[cur][0]) + sel;
-#pragma unroll 4
-        for (int j = 0; j < kChunk; ++j) {
-            const double2 s = wt[cur][j];            // wave-uniform broadcast
+#pragma unroll 8
+        for (int j = 0; j < kCh; ++j) {
+            const double2 s = wrow[j];
             double d;
-            if (ROWPAIR) d = drow[2 * j];             // this lane's timer row
+            if (kStaged) d = drow[2 * j];             // this lane's combination
             else d = fmax(s.x, t1) - t1;              // 0 when w <= t1
             const double h = s.y * fmin(d, ep);       // T * host seconds held
             const double gone = (s.x > e) ? 1.0 : 0.0;   // discarded before resume
@@ -144,15 +176,20 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
             const double c = (base + acc[l]) / md;
             if (cost_out != nullptr && valid) cost_out[(r * tb.L + lg) * P + f] = c;
             if (cand != nullptr) {
-                double bc = valid ? c : INFINITY;
-                int32_t bf = valid ? (int32_t)f : -1;
-                wave_argmin(bc, bf);
-                if (lane == 0) {
-                    ArgminCand out;
-                    out.cost = bc;
-                    out.f = bf;
-                    out.pad = 0;
-                    cand[(r * plan.nblk + blk) * tb.L + lg] = out;
+                // one candidate per (group, resample slot, load): slot 0 holds
+                // the group's first resample, slot 1 the second one if any
+                for (int slot = 0; slot < (twoStreams ? 2 : 1); ++slot) {
+                    const bool mine = valid && (slot == 0 ? r == rA || !kStaged : r == rB);
+                    double bc = mine ? c : INFINITY;
+                    int32_t bf = mine ? (int32_t)f : -1;
+                    wave_argmin(bc, bf);
+                    if (lane == 0) {
+                        ArgminCand out;
+                        out.cost = bc;
+                        out.f = bf;
+                        out.pad = 0;
+                        cand[(grp * 2 + slot) * tb.L + lg] = out;
+                    }
                 }
             }
         }
@@ -164,22 +201,33 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
     }
 }
 
+template <int LT, int MODE>
+static hipError_t launch_grid_m(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
+                                const GridPlan &plan, const double *X, const double *G,
+                                double *cost_out, ArgminCand *cand, double *partials,
+                                int *status, hipStream_t stream)
+{
+    const int64_t nlogical = plan.ngroups * plan.nsplit * plan.ntiles;
+    hipLaunchKernelGGL((grid_kernel<LT, MODE>), dim3((unsigned)nlogical), dim3(kWave), 0, stream,
+                       src, tb, pr, plan, X, G, cost_out, cand, partials, status, nlogical);
+    return hipGetLastError();
+}
+
 template <int LT>
 static hipError_t launch_grid_t(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                                 const GridPlan &plan, const double *X, const double *G,
                                 double *cost_out, ArgminCand *cand, double *partials,
                                 int *status, hipStream_t stream)
 {
-    const int64_t nlogical = plan.R * plan.nsplit * plan.ntiles * plan.nblk;
-    if (tb.K2 >= kWave)
-        hipLaunchKernelGGL((grid_kernel<LT, true>), dim3((unsigned)nlogical), dim3(kWave), 0,
-                           stream, src, tb, pr, plan, X, G, cost_out, cand, partials, status,
-                           nlogical);
-    else
-        hipLaunchKernelGGL((grid_kernel<LT, false>), dim3((unsigned)nlogical), dim3(kWave), 0,
-                           stream, src, tb, pr, plan, X, G, cost_out, cand, partials, status,
-                           nlogical);
-    return hipGetLastError();
+    switch (plan.mode) {
+    case kModePerLane:
+        return launch_grid_m<LT, kModePerLane>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+    case kModeRows1:
+        return launch_grid_m<LT, kModeRows1>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+    case kModeRows2:
+        return launch_grid_m<LT, kModeRows2>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+    default: return hipErrorInvalidValue;
+    }
 }
 
 hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,

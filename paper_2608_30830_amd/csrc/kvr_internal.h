@@ -33,17 +33,24 @@ struct Tables {
     int32_t K1, K2, L, Lpad;
 };
 
+// Grid-kernel modes (how 64-lane groups map onto policies and resamples).
+enum { kModePerLane = 0, kModeRows1 = 1, kModeRows2 = 2 };
+
 // Brute-force launch plan.
 struct GridPlan {
     int LT;              // loads per tile (4, 8, 16 or 32)
     int ntiles;          // ceil(L / LT)
-    int nblk;            // policy blocks of one wave: ceil(K1*K2 / 64)
+    int nblk;            // groups per resample, kModePerLane: ceil(K1*K2 / 64)
     int nsplit;          // sample splits per resample
+    int mode;            // kModePerLane, kModeRows1 or kModeRows2
+    int64_t ngroups;     // 64-lane groups: R*nblk (per lane) or ceil(R*K1*K2 / 64)
     int64_t split_len;   // samples per split (multiple of kChunk)
     int64_t R;           // resamples
 };
 
-struct ArgminCand {     // one wave's best policy for one (resample, load)
+// One wave's best policy for one (group, resample slot, load); laid out
+// [ngroups][2][L], slot 1 used only by groups that straddle two resamples.
+struct ArgminCand {
     double cost;
     int32_t f;
     int32_t pad;
@@ -53,8 +60,11 @@ struct ArgminCand {     // one wave's best policy for one (resample, load)
 hipError_t launch_clear_status(int *status, hipStream_t stream);
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
 
+// X and G per (resample, t1); with few resamples the samples are cut into
+// parts (partials in xgp[parts][R][K1][2], summed in part order).
+int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len);
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     int *status, hipStream_t stream);
+                     double *xgp, int *status, hipStream_t stream);
 
 hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                        const GridPlan &plan, const double *X, const double *G,
@@ -66,7 +76,7 @@ hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const 
                                   int64_t m, const double *X, const double *G,
                                   double *partials, double *cost_out, hipStream_t stream);
 
-hipError_t launch_reduce_cands(const ArgminCand *cand, int64_t R, int nblk, int L,
+hipError_t launch_reduce_cands(const ArgminCand *cand, const GridPlan &plan, int64_t P, int L,
                                int32_t *best, double *best_cost, hipStream_t stream);
 
 hipError_t launch_select(const double *cost, int64_t batch, int L, int64_t P, int K2,
@@ -78,7 +88,7 @@ struct SortWs {
     uint64_t *keys[2];
     int32_t *vals[2];
     uint32_t *hist;       // [256][nblocks]
-    uint32_t *counts;     // [8][256] global digit counts per pass
+    uint32_t *counts;     // [256] digit totals of the current pass
     int64_t *Nsum;        // [n] inclusive prefix of T (sorted order)
     double *Ssum;         // [n] inclusive prefix of T*w (sorted order)
     int64_t *blkN;        // [nblocks_scan]

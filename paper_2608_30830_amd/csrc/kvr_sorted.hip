@@ -38,7 +38,7 @@ size_t sort_ws_bytes(int64_t n)
     b += 2 * align256(sizeof(uint64_t) * n);
     b += 2 * align256(sizeof(int32_t) * n);
     b += align256(sizeof(uint32_t) * 256 * nb);
-    b += align256(sizeof(uint32_t) * 8 * 256);
+    b += align256(sizeof(uint32_t) * 256);
     b += align256(sizeof(int64_t) * n);
     b += align256(sizeof(double) * n);
     b += align256(sizeof(int64_t) * ns);
@@ -61,7 +61,7 @@ void sort_ws_carve(void *base, int64_t n, SortWs &ws)
     ws.vals[0] = (int32_t *)take(sizeof(int32_t) * n);
     ws.vals[1] = (int32_t *)take(sizeof(int32_t) * n);
     ws.hist = (uint32_t *)take(sizeof(uint32_t) * 256 * ws.nblocks);
-    ws.counts = (uint32_t *)take(sizeof(uint32_t) * 8 * 256);
+    ws.counts = (uint32_t *)take(sizeof(uint32_t) * 256);
     ws.Nsum = (int64_t *)take(sizeof(int64_t) * n);
     ws.Ssum = (double *)take(sizeof(double) * n);
     ws.blkN = (int64_t *)take(sizeof(int64_t) * ws.nblocks_scan);
@@ -105,35 +105,42 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t 
     hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
 }
 
-// Exclusive scan of a uint32 array in place, one block of 1024 threads.
-__global__ void __launch_bounds__(1024) scan_u32_kernel(uint32_t *a, int64_t len)
+// Exclusive scan, within one block of 256 threads, of one value per thread;
+// returns the prefix and writes the block total to *total (all threads).
+__device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *total)
 {
-    __shared__ uint32_t wsum[16];
-    __shared__ uint32_t carry_s;
-    if (threadIdx.x == 0) carry_s = 0;
-    __syncthreads();
+    __shared__ uint32_t wsum[4];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    for (int64_t base = 0; base < len; base += 1024) {
-        const int64_t i = base + threadIdx.x;
-        uint32_t v = (i < len) ? a[i] : 0u;
-        uint32_t x = v;  // inclusive wave scan
-        for (int off = 1; off < kWave; off <<= 1) {
-            uint32_t y = __shfl_up(x, off, kWave);
-            if (lane >= off) x += y;
-        }
-        if (lane == kWave - 1) wsum[wave] = x;
-        __syncthreads();
-        uint32_t before = carry_s;
-        for (int q = 0; q < wave; ++q) before += wsum[q];
-        if (i < len) a[i] = before + x - v;
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            uint32_t t = carry_s;
-            for (int q = 0; q < 16; ++q) t += wsum[q];
-            carry_s = t;
-        }
-        __syncthreads();
+    uint32_t x = v;
+    for (int off = 1; off < kWave; off <<= 1) {
+        uint32_t y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
     }
+    if (lane == kWave - 1) wsum[wave] = x;
+    __syncthreads();
+    uint32_t before = 0;
+    for (int q = 0; q < wave; ++q) before += wsum[q];
+    *total = wsum[0] + wsum[1] + wsum[2] + wsum[3];
+    __syncthreads();
+    return before + x - v;
+}
+
+// One block per digit: exclusive scan of that digit's per-tile counts over the
+// tiles (in place) and the digit's total count.
+__global__ void __launch_bounds__(256) digit_scan_kernel(uint32_t *__restrict__ hist, int nblocks,
+                                                         uint32_t *__restrict__ totals)
+{
+    uint32_t *row = hist + (int64_t)blockIdx.x * nblocks;
+    uint32_t carry = 0;
+    for (int base = 0; base < nblocks; base += 256) {
+        const int i = base + threadIdx.x;
+        const uint32_t v = (i < nblocks) ? row[i] : 0u;
+        uint32_t tot;
+        const uint32_t pre = block_exclusive_scan(v, &tot);
+        if (i < nblocks) row[i] = carry + pre;
+        carry += tot;
+    }
+    if (threadIdx.x == 0) totals[blockIdx.x] = carry;
 }
 
 __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
@@ -142,17 +149,24 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
                                      __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
 }
 
-// Stable ranking scatter of one digit pass.
+// Stable ranking scatter of one digit pass.  The destination of a key is
+// (keys with a smaller digit) + (keys with its digit in earlier tiles, from
+// digit_scan_kernel) + (keys with its digit earlier in this tile).
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int64_t n, int shift,
-    const uint32_t *__restrict__ offs, int nblocks, uint64_t *__restrict__ keys_out,
-    int32_t *__restrict__ vals_out)
+    const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
+    uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
 {
     __shared__ uint32_t wcnt[4][256];
     __shared__ uint32_t wofs[4][256];
+    __shared__ uint32_t dbase[256];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
 #pragma unroll
     for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
+    {
+        uint32_t all;
+        dbase[threadIdx.x] = block_exclusive_scan(totals[threadIdx.x], &all);
+    }
     __syncthreads();
 
     const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * kWaveKeys;
@@ -196,7 +210,8 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
         const int64_t i = base + j * kWave + lane;
         if (i < n) {
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
-            const int64_t dest = (int64_t)offs[(int64_t)d * nblocks + blockIdx.x] + wofs[wave][d] + local[j];
+            const int64_t dest = (int64_t)dbase[d] + offs[(int64_t)d * nblocks + blockIdx.x] +
+                                 wofs[wave][d] + local[j];
             if (dest < n) {  // always true when the histograms agree; never write outside
                 keys_out[dest] = key[j];
                 vals_out[dest] = val[j];
@@ -378,10 +393,10 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
         const int shift = 8 * pass;
         hipLaunchKernelGGL(sort_hist_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
                            ws.keys[cur], n, shift, ws.hist, ws.nblocks);
-        hipLaunchKernelGGL(scan_u32_kernel, dim3(1), dim3(1024), 0, stream, ws.hist,
-                           (int64_t)256 * ws.nblocks);
+        hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(256), 0, stream, ws.hist, ws.nblocks,
+                           ws.counts);
         hipLaunchKernelGGL(sort_scatter_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                           ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.nblocks,
+                           ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts, ws.nblocks,
                            ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
         if ((err = hipGetLastError()) != hipSuccess) return err;
         cur ^= 1;

@@ -311,3 +311,35 @@ def test_domain_errors_are_reported(kvr):
     # a clean call afterwards on a fresh workspace reports OK
     kvr.kvr_cost_grid(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()), pr, g)
     torch.cuda.synchronize()
+
+
+def test_profile_events_bracket_the_grid_kernel(kvr):
+    """kvr_set_profile_events: the library records the caller's events around
+    its main kernel on the call's stream."""
+    import ctypes
+    import torch
+    hip = ctypes.CDLL("libamdhip64.so")
+    hip.hipEventCreate.argtypes = [ctypes.POINTER(ctypes.c_void_p)]
+    hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                        ctypes.c_void_p]
+    hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+    evs = [ctypes.c_void_p(), ctypes.c_void_p()]
+    for e in evs:
+        assert hip.hipEventCreate(ctypes.byref(e)) == 0
+    wl = workloads.random_case(304, 20000, 2, 80, 8, resamples=8)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    args = (_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()), _dev(wl.idx, _i32()),
+            _lib_prices(kvr, wl), g)
+    kvr.kvr_set_profile_events(evs[0].value, evs[1].value)
+    try:
+        kvr.kvr_bootstrap(*args)
+    finally:
+        kvr.kvr_set_profile_events(None, None)
+    torch.cuda.synchronize()
+    ms = ctypes.c_float()
+    assert hip.hipEventElapsedTime(ctypes.byref(ms), evs[0], evs[1]) == 0
+    assert ms.value > 0.0
+    for e in evs:
+        hip.hipEventDestroy(e)
+    with pytest.raises(kvr.KvrError):
+        kvr.kvr_set_profile_events(evs[0].value, None)
