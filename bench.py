@@ -200,7 +200,7 @@ def main() -> int:
         "roofline": {"bound": "alu", "achieved": achieved, "peak": FP64_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFLOPS,
                      "traffic": counter_traffic(args.workload, wl.n_resamples),
-                     "kernel": "grid_kernel<32,true>", "kernel_ms": kernel_ms,
+                     "kernel": "grid_kernel<32,1>", "kernel_ms": kernel_ms,
                      "flops_per_launch": 2.0 * evals},
     }
 
