@@ -54,6 +54,9 @@ def _configure(lib):
                                                  D, D, P, I32, P, I32, P, I32,
                                                  P, P]
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_capacity_replay.argtypes = [P, P, P, I64, I64, D, D, D, P, P]
+    lib.oracle_capacity_replay.restype = D
+    lib.oracle_capacity_replay_batch.argtypes = [P, P, P, I64, I64, I64, P, I32, D, D, P, P]
     return lib
 
 
@@ -197,3 +200,28 @@ def closed_form_bootstrap(wait_s, ctx, idx, prices: Prices, t1, t2, lam):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def capacity_replay(arrival_s, wait_s, c2, t2, b2, b3, ctx=None):
+    """Finite-capacity admission replay of one request sequence under one
+    host timer: (mean cost per request, restored tokens, admitted requests)."""
+    a, w = _f64(arrival_s), _f64(wait_s)
+    T = None if ctx is None else _i32(ctx)
+    rest, adm = ctypes.c_int64(), ctypes.c_int64()
+    cost = _load().oracle_capacity_replay(_p(a), _p(w), _p(T), a.size, int(c2), float(t2),
+                                          float(b2), float(b3), ctypes.byref(rest),
+                                          ctypes.byref(adm))
+    return cost, rest.value, adm.value
+
+
+def capacity_replay_batch(arrival_s, wait_s, c2, t2, b2, b3, ctx=None):
+    """Rows [reps, n] of arrivals and waits x timers t2[K] -> (cost, restored) [reps, K]."""
+    a, w = _f64(arrival_s), _f64(wait_s)
+    T = None if ctx is None else _i32(ctx)
+    t2 = _f64(t2)
+    reps, n = a.shape
+    cost = np.empty((reps, t2.size), dtype=np.float64)
+    rest = np.empty((reps, t2.size), dtype=np.int64)
+    _load().oracle_capacity_replay_batch(_p(a), _p(w), _p(T), reps, n, int(c2), _p(t2), t2.size,
+                                         float(b2), float(b3), _p(cost), _p(rest))
+    return cost, rest

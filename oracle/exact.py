@@ -96,3 +96,27 @@ def select(cost) -> List[int]:
                 bi = f
         best.append(bi)
     return best
+
+
+def capacity_replay(arrival_s, wait_s, c2, t2, b2, b3, ctx=None):
+    """The admission replay of Appendix D written out with an explicit list of
+    resident departure times (quadratic, for tiny inputs): departures at or
+    before an arrival free their slots first; admit if fewer than c2 remain;
+    an admitted request is restored if its wait is within the host timer.
+    Returns (exact mean cost as a Fraction, restored tokens, admitted)."""
+    residents = []
+    restored = admitted = total = 0
+    for i, (a, w) in enumerate(zip(arrival_s, wait_s)):
+        T = 1 if ctx is None else int(ctx[i])
+        total += T
+        residents = [d for d in residents if not d <= a]
+        if len(residents) < c2:
+            admitted += 1
+            if w <= t2:
+                restored += T
+                residents.append(float(a) + float(w))
+            else:
+                residents.append(float(a) + float(t2))
+    n = len(arrival_s)
+    cost = (_fr(b2) * restored + _fr(b3) * (total - restored)) / n
+    return cost, restored, admitted

@@ -311,3 +311,97 @@ int oracle_num_threads(void)
     return 1;
 #endif
 }
+
+/*
+ * Finite-capacity admission replay (Appendix D; the evaluation behind
+ * Table 6).  Requests suspend at their arrival times (ascending) and resume
+ * after their waits; every request is offloaded to host DRAM at suspension.
+ * The host tier has C2 slots: a request that arrives when a slot is free is
+ * admitted, one that finds the tier full is not admitted and recomputes at
+ * resume; residents are never displaced.  Under a host timer t2 an admitted
+ * request whose wait exceeds t2 is discarded at arrival + t2 (its slot frees
+ * then) and recomputes at resume; otherwise it is restored from host at
+ * arrival + wait.  t2 = +inf is host-retain.  Departures at or before an
+ * arrival free their slots before that arrival is admitted; a resume at the
+ * instant its timer fires counts as a restore.  No holding price is charged:
+ * capacity is enforced directly.
+ *
+ *   arrival_s[n] ascending, wait_s[n], ctx[n] (NULL: every context 1 token).
+ *   restored_tokens_out: sum of T over restored requests (exact integer).
+ *   Returns the mean cost per request, (b2*R + b3*(Ttot - R)) / n with
+ *   R = restored_tokens_out, which is also how the GPU path reports it.
+ */
+typedef struct { double *v; int64_t size; } minheap;
+
+static void heap_push(minheap *h, double x)
+{
+    int64_t i = h->size++;
+    h->v[i] = x;
+    while (i > 0) {
+        int64_t p = (i - 1) / 2;
+        if (!(h->v[i] < h->v[p])) break;
+        double t = h->v[i]; h->v[i] = h->v[p]; h->v[p] = t;
+        i = p;
+    }
+}
+
+static void heap_pop(minheap *h)
+{
+    h->v[0] = h->v[--h->size];
+    int64_t i = 0;
+    for (;;) {
+        int64_t l = 2 * i + 1, r = l + 1, s = i;
+        if (l < h->size && h->v[l] < h->v[s]) s = l;
+        if (r < h->size && h->v[r] < h->v[s]) s = r;
+        if (s == i) break;
+        double t = h->v[i]; h->v[i] = h->v[s]; h->v[s] = t;
+        i = s;
+    }
+}
+
+double oracle_capacity_replay(const double *arrival_s, const double *wait_s, const int32_t *ctx,
+                              int64_t n, int64_t c2, double t2, double b2, double b3,
+                              int64_t *restored_tokens_out, int64_t *admitted_out)
+{
+    minheap h;
+    h.v = (double *)malloc(sizeof(double) * (size_t)(c2 > 0 ? c2 : 1));
+    h.size = 0;
+    int64_t restored = 0, total = 0, admitted = 0;
+    for (int64_t i = 0; i < n; ++i) {
+        const double a = arrival_s[i], w = wait_s[i];
+        const int64_t T = ctx ? (int64_t)ctx[i] : 1;
+        total += T;
+        while (h.size > 0 && h.v[0] <= a) heap_pop(&h);     /* resumed or expired by now */
+        if (h.size < c2) {
+            admitted += 1;
+            if (w <= t2) {                                   /* resumes before the timer */
+                restored += T;
+                heap_push(&h, a + w);
+            } else {                                         /* discarded at the timer   */
+                heap_push(&h, a + t2);
+            }
+        }                                                    /* else: tier full, recompute */
+    }
+    free(h.v);
+    if (restored_tokens_out) *restored_tokens_out = restored;
+    if (admitted_out) *admitted_out = admitted;
+    return (b2 * (double)restored + b3 * (double)(total - restored)) / (double)n;
+}
+
+/* Many replays: rows of arrivals/waits [reps][n] x host timers [n_t2];
+ * outputs [reps][n_t2]. */
+void oracle_capacity_replay_batch(const double *arrival_s, const double *wait_s,
+                                  const int32_t *ctx, int64_t reps, int64_t n, int64_t c2,
+                                  const double *t2, int32_t n_t2, double b2, double b3,
+                                  double *cost_out, int64_t *restored_out)
+{
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t q = 0; q < reps * n_t2; ++q) {
+        int64_t r = q / n_t2, k = q % n_t2;
+        int64_t rest = 0;
+        cost_out[q] = oracle_capacity_replay(arrival_s + r * n, wait_s + r * n,
+                                             ctx ? ctx + r * n : NULL, n, c2, t2[k], b2, b3,
+                                             &rest, NULL);
+        if (restored_out) restored_out[q] = rest;
+    }
+}

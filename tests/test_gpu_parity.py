@@ -343,3 +343,62 @@ def test_profile_events_bracket_the_grid_kernel(kvr):
         hip.hipEventDestroy(e)
     with pytest.raises(kvr.KvrError):
         kvr.kvr_set_profile_events(evs[0].value, None)
+
+
+DEGENERATE = {
+    # every wait zero: every policy costs 0 (ties everywhere, largest index wins)
+    "all-zero": (np.zeros(300), np.full(300, 7, np.int32), np.array([0.0, 5.0]),
+                 np.array([1.0, 2.0, np.inf]), np.array([0.1, 0.9])),
+    # every wait sits exactly on a deadline t1 + t2
+    "on-deadline": (np.full(200, 30.0 + 45.0), np.arange(1, 201, dtype=np.int32),
+                    np.array([0.0, 30.0]), np.array([10.0, 45.0, 80.0, np.inf]),
+                    np.array([0.2, 0.5, 3.0])),
+    # host-retain only
+    "retain-only": (np.linspace(0.0, 5000.0, 777), np.full(777, 4096, np.int32),
+                    np.array([0.0]), np.array([np.inf]), np.array([0.05, 0.3, 1.0])),
+    # every load at or below lambda_crit: no congestion price
+    "uncongested": (np.geomspace(1.0, 20000.0, 1500), np.full(1500, 1000, np.int32),
+                    np.array([0.0, 2.0, 9.0]), np.concatenate([np.geomspace(3, 9000, 70), [np.inf]]),
+                    np.array([0.0, 0.1, 425.0 / 1800.0])),
+    # one sample, one timer pair, one load
+    "single": (np.array([123.0]), np.array([5], np.int32), np.array([0.0]), np.array([100.0]),
+               np.array([0.7])),
+    # many t1 rows, one host timer (group straddles rows every lane)
+    "k2-one": (np.geomspace(0.5, 9000.0, 640), np.full(640, 33, np.int32),
+               np.geomspace(0.1, 3000.0, 150), np.array([60.0]), np.array([0.4, 0.8])),
+}
+
+
+@pytest.mark.parametrize("name", sorted(DEGENERATE))
+@pytest.mark.parametrize("method", ["brute", "sorted"])
+def test_degenerate_inputs(kvr, oracle_mod, name, method):
+    w, T, t1, t2, lam = DEGENERATE[name]
+    wl = workloads.Workload(name, w.astype(np.float64), T, t1, t2, lam, float(workloads.KV_128K))
+    cost, perm, g = run_grid(kvr, wl, method)
+    pr = oracle_mod.workload_prices(wl)
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    if np.all(ref == 0):
+        assert np.all(cost == 0)
+    else:
+        assert_costs(cost, ref)
+    if perm is not None:
+        assert np.array_equal(perm, oracle_mod.stable_order(wl.wait_s))
+    import torch
+    best, _, br = kvr.kvr_select_policy(torch.as_tensor(cost).cuda(), g.last_inf)
+    rb, _, rbr = oracle_mod.select(ref, wl.t2)
+    assert np.array_equal(_np(best), rb)
+    assert np.array_equal(_np(br), rbr)
+
+
+def test_batched_select_matches_fused_selection(kvr):
+    """kvr_select_policy over a [R, L, K1, K2] cost tensor picks what the
+    bootstrap's fused per-wave selection picked."""
+    wl = workloads.random_case(305, 6000, 3, 90, 12, resamples=6, ties=True)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    best, bc, cost = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                       _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g,
+                                       want_cost=True)
+    b2, bc2, br2 = kvr.kvr_select_policy(cost, g.last_inf)
+    assert np.array_equal(_np(best), _np(b2))
+    assert np.array_equal(_np(bc), _np(bc2))
+    assert tuple(b2.shape) == (6, wl.lam.size)

@@ -72,3 +72,43 @@ def test_mutant_is_caught(oracle_mod, tmp_path, name):
         assert not _pins_pass(oracle), f"mutant {name} survived the pins"
     finally:
         oracle._lib = saved
+
+
+REPLAY_MUTANTS = {
+    "expiry_never_frees": ("heap_push(&h, a + t2);", "heap_push(&h, a + w);"),
+    "admit_one_short": ("if (h.size < c2) {", "if (h.size + 1 < c2 || h.size == 0) {"),
+    "departure_strict": ("while (h.size > 0 && h.v[0] <= a) heap_pop(&h);",
+                         "while (h.size > 0 && h.v[0] < a) heap_pop(&h);"),
+    "timer_strict": ("if (w <= t2) {                                   /* resumes before the timer */",
+                     "if (w < t2) {"),
+}
+
+
+def _replay_pins_pass(mod):
+    from tests.test_replay_pins import _tiny
+    for seed in range(16):
+        arr, w, T = _tiny(seed)
+        for c2 in (1, 2, 3):
+            for t2 in (7.5, 30.0, float("inf")):
+                got = mod.capacity_replay(arr, w, c2, t2, 0.02, 1.91, ctx=T)
+                ref = exact.capacity_replay(arr, w, c2, t2, 0.02, 1.91, ctx=T)
+                if got[1:] != ref[1:]:
+                    return False
+    return True
+
+
+@pytest.mark.parametrize("name", sorted(REPLAY_MUTANTS))
+def test_replay_mutant_is_caught(oracle_mod, tmp_path, name):
+    old, new = REPLAY_MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    mpath = tmp_path / "mutant.c"
+    mpath.write_text(src.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    oracle.compile_library(str(mpath), str(lib))
+    saved = oracle._lib
+    try:
+        oracle._lib = oracle._configure(ctypes.CDLL(str(lib)))
+        assert _replay_pins_pass(oracle) is False, f"mutant {name} survived"
+    finally:
+        oracle._lib = saved

@@ -168,6 +168,52 @@ def make(name: str, resamples: Optional[int] = None) -> Workload:
     raise KeyError(f"unknown workload {name!r}; known: {NAMES}")
 
 
+FAMILIES = ("lognormal", "exponential", "mixture")
+
+
+def family_waits(rng: np.random.Generator, family: str, n: int) -> np.ndarray:
+    """The approval-wait families of Section 4.1, each with mean 1,800 s:
+    LogNormal(sigma 1); Exponential; 0.5 Exp(mean 60 s) + 0.5 LogNormal(sigma
+    0.7, mean 3,540 s)."""
+    if family == "lognormal":
+        return rng.lognormal(math.log(1800.0) - 0.5, 1.0, n)
+    if family == "exponential":
+        return rng.exponential(1800.0, n)
+    if family == "mixture":
+        short = rng.random(n) < 0.5
+        return np.where(short, rng.exponential(60.0, n),
+                        rng.lognormal(math.log(3540.0) - 0.5 * 0.7 * 0.7, 0.7, n))
+    raise KeyError(family)
+
+
+@dataclasses.dataclass
+class ReplayCase:
+    family: str
+    rate_per_s: float
+    arrival_s: np.ndarray    # float64 [reps, n], ascending per row (Poisson arrivals)
+    wait_s: np.ndarray       # float64 [reps, n]
+
+    @property
+    def reps(self) -> int:
+        return int(self.arrival_s.shape[0])
+
+    @property
+    def n(self) -> int:
+        return int(self.arrival_s.shape[1])
+
+
+def replay_case(family: str, rate_per_s: float, reps: int, n: int = 4000,
+                seed: int = 2000) -> ReplayCase:
+    """``reps`` independent request sequences of ``n`` suspensions: Poisson
+    arrivals at ``rate_per_s`` starting at time 0, waits from ``family``."""
+    fam = FAMILIES.index(family)
+    ss = np.random.SeedSequence([seed, fam, int(round(rate_per_s * 1e9))])
+    ra, rw = [np.random.Generator(np.random.PCG64(s)) for s in ss.spawn(2)]
+    arr = np.cumsum(ra.exponential(1.0 / rate_per_s, (reps, n)), axis=1)
+    w = np.stack([family_waits(rw, family, n) for _ in range(reps)])
+    return ReplayCase(family, rate_per_s, arr, w)
+
+
 def bootstrap_rows(rng: np.random.Generator, rows: int, m: int, n: int) -> np.ndarray:
     """``rows`` x ``m`` with-replacement index rows into ``n`` samples, drawn
     row by row so that any prefix of rows is reproducible on its own."""
