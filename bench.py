@@ -257,6 +257,39 @@ def time_paths(kvr, workloads, torch):
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
+    res.update(time_replay(kvr, workloads, torch))
+    return res
+
+
+def time_replay(kvr, workloads, torch, reps: int = 8192):
+    """The finite-capacity admission replay at 2 lambda_crit (the Table 6
+    setting): ``reps`` sequences of 4,000 requests per wait family under the
+    Eq. 3 timer, host-retain and the 10/30/60-minute timers."""
+    res = {}
+    lc = 425.0 / 1800.0
+    pr = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, 425.0, 1800.0)
+    pr.b2_per_token, pr.b3_per_token = 0.02, 1.91
+    for family in workloads.FAMILIES:
+        rc = workloads.replay_case(family, 2 * lc, reps=reps)
+        t2 = [kvr.kvr_eq3_timer(pr, 2 * lc), float("inf"), 600.0, 1800.0, 3600.0]
+        arr = torch.as_tensor(rc.arrival_s).cuda()
+        w = torch.as_tensor(rc.wait_s).cuda()
+        kvr.kvr_capacity_replay(arr, w, pr, t2)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            kvr.kvr_capacity_replay(arr, w, pr, t2, check=False)
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        ms = sorted(times)[len(times) // 2]
+        events = reps * len(t2) * rc.n
+        key = f"replay-{family}-2x/{reps}x{rc.n}"
+        res[key] = {"ms": ms, "replayed_requests": events,
+                    "replayed_requests_per_s": events / (ms * 1e-3)}
+        log(f"[bench] path {key}: {ms:.3f} ms")
     return res
 
 

@@ -178,6 +178,47 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
 int kvr_workspace_status(const void *d_ws, void *hip_stream);
 
 /*
+ * Eq. 3 timer (host only): t2(lambda) = +inf if lambda <= lambda_crit =
+ * C2/W_ref, else (beta_3 - beta_2) / alpha_2(lambda) with alpha_2(lambda) =
+ * (lambda - lambda_crit) * beta_3 / C2.  With per-token prices both terms scale
+ * with T, so the timer is the same for every context size.  Writes *t2_out;
+ * KVR_E_PRICE for an invalid price vector, KVR_E_GRID for a load that is not
+ * finite and >= 0, KVR_E_NULL for NULL pointers.
+ */
+int kvr_eq3_timer(const kvr_prices *p, double lambda, double *t2_out);
+
+/*
+ * Finite-capacity admission replay (Appendix D; the replay behind Table 6 and
+ * the replay columns of Table 3).  Each row is one sequence of suspensions:
+ * every request is offloaded to host DRAM at suspension; the host tier holds
+ * C2 contexts (p->host_slots_c2, an integer >= 1); a request that arrives
+ * while a slot is free is admitted, one that finds the tier full recomputes
+ * at resume (beta_3), and residents are never displaced.  Under host timer t2
+ * an admitted request whose wait exceeds t2 is discarded at arrival + t2
+ * (recompute at resume); otherwise it is restored from host (beta_2) and
+ * leaves at arrival + wait.  Departures at or before an arrival free their
+ * slots first.  No holding price is charged: capacity is enforced directly.
+ *   d_arrival_s     device, float64 [n_reps][n]: suspension times, seconds,
+ *                   finite, >= 0, non-decreasing within a row.
+ *   d_wait_s        device, float64 [n_reps][n]: waits, finite, >= 0.
+ *   d_ctx_tokens    device, int32 [n_reps][n] or NULL (every context 1 token).
+ *   p               host: b2, b3 and host_slots_c2 are used (all fields must be
+ *                   valid; C2 not an integer >= 1 is KVR_E_PRICE).
+ *   t2[n_t2]        host: host timers, > 0 (+INFINITY = host-retain), any order.
+ *   d_cost          device, float64 [n_reps][n_t2]: mean GPU-s per request,
+ *                   (b2*R + b3*(Ttot - R)) / n with R the restored tokens.
+ *   d_restored_tokens, d_admitted  device, int64 [n_reps][n_t2] or NULL:
+ *                   tokens restored from host, requests admitted (exact).
+ *   Sizes: 1 <= n <= 8192, 1 <= n_t2 <= 4096, n_reps * n_t2 <= 2^31 - 1.
+ *   Workspace: two-phase sizing as above.
+ */
+int kvr_capacity_replay(const double *d_arrival_s, const double *d_wait_s,
+                        const int32_t *d_ctx_tokens, int64_t n_reps, int64_t n,
+                        const kvr_prices *p, const double *t2, int32_t n_t2,
+                        double *d_cost, int64_t *d_restored_tokens, int64_t *d_admitted,
+                        void *d_ws, size_t *ws_bytes, void *hip_stream);
+
+/*
  * Instrumentation for benchmarks.  After this call, every kvr_cost_grid and
  * kvr_bootstrap call made from the same host thread records ev_begin (a
  * hipEvent_t) on its stream right before its main kernel -- the brute-force

@@ -30,8 +30,8 @@ KVR_RETAIN = 0
 KVR_EXPIRE = 1
 
 EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy",
-           "kvr_bootstrap", "kvr_workspace_status", "kvr_set_profile_events",
-           "kvr_status_string")
+           "kvr_bootstrap", "kvr_eq3_timer", "kvr_capacity_replay", "kvr_workspace_status",
+           "kvr_set_profile_events", "kvr_status_string")
 
 
 class kvr_prices(ctypes.Structure):
@@ -77,6 +77,11 @@ def load_library(path: str = LIB_PATH):
     lib.kvr_bootstrap.restype = ctypes.c_int
     lib.kvr_workspace_status.argtypes = [P, P]
     lib.kvr_workspace_status.restype = ctypes.c_int
+    lib.kvr_eq3_timer.argtypes = [ctypes.POINTER(kvr_prices), D, ctypes.POINTER(ctypes.c_double)]
+    lib.kvr_eq3_timer.restype = ctypes.c_int
+    lib.kvr_capacity_replay.argtypes = [P, P, P, I64, I64, ctypes.POINTER(kvr_prices), P, I32,
+                                        P, P, P, P, SZ, P]
+    lib.kvr_capacity_replay.restype = ctypes.c_int
     lib.kvr_set_profile_events.argtypes = [P, P]
     lib.kvr_set_profile_events.restype = ctypes.c_int
     lib.kvr_status_string.argtypes = [ctypes.c_int]
@@ -245,6 +250,48 @@ def kvr_bootstrap(wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
     if want_cost:
         return call.best, call.best_cost, call.cost
     return call.best, call.best_cost
+
+
+def kvr_eq3_timer(prices: kvr_prices, lam: float) -> float:
+    """Eq. 3 host timer t2(lambda) (inf at or below lambda_crit)."""
+    out = ctypes.c_double()
+    _check(load_library().kvr_eq3_timer(ctypes.byref(prices), float(lam), ctypes.byref(out)),
+           "kvr_eq3_timer")
+    return out.value
+
+
+def kvr_capacity_replay(arrival_s, wait_s, prices: kvr_prices, t2: Sequence[float],
+                        ctx_tokens=None, stream=None, check: bool = True):
+    """Finite-capacity admission replay of rows [n_reps, n] under each timer:
+    (cost, restored_tokens, admitted), each [n_reps, n_t2]."""
+    torch = _torch()
+    lib = load_library()
+    _need(arrival_s, torch.float64, "arrival_s")
+    _need(wait_s, torch.float64, "wait_s")
+    if ctx_tokens is not None:
+        _need(ctx_tokens, torch.int32, "ctx_tokens")
+    if arrival_s.dim() != 2 or tuple(wait_s.shape) != tuple(arrival_s.shape):
+        raise ValueError("arrival_s and wait_s must both be [n_reps, n]")
+    reps, n = arrival_s.shape
+    K = len(t2)
+    t2c = (ctypes.c_double * K)(*[float(x) for x in t2])
+    need = ctypes.c_size_t(0)
+    _check(lib.kvr_capacity_replay(None, None, None, reps, n, ctypes.byref(prices), t2c, K, None,
+                                   None, None, None, ctypes.byref(need), None),
+           "kvr_capacity_replay(size)")
+    ws = _workspace(need.value)
+    cost = torch.empty((reps, K), dtype=torch.float64, device="cuda")
+    rest = torch.empty((reps, K), dtype=torch.int64, device="cuda")
+    adm = torch.empty((reps, K), dtype=torch.int64, device="cuda")
+    have = ctypes.c_size_t(ws.numel())
+    st = _stream_ptr(stream)
+    _check(lib.kvr_capacity_replay(_ptr(arrival_s), _ptr(wait_s), _ptr(ctx_tokens), reps, n,
+                                   ctypes.byref(prices), t2c, K, _ptr(cost), _ptr(rest),
+                                   _ptr(adm), _ptr(ws), ctypes.byref(have), st),
+           "kvr_capacity_replay")
+    if check:
+        _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_capacity_replay(device)")
+    return cost, rest, adm
 
 
 def kvr_set_profile_events(ev_begin, ev_end) -> None:

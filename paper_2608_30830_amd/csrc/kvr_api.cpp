@@ -363,6 +363,55 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     return KVR_OK;
 }
 
+int kvr_eq3_timer(const kvr_prices *p, double lambda, double *t2_out)
+{
+    if (!t2_out) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if (!std::isfinite(lambda) || lambda < 0.0) return KVR_E_GRID;
+    const double lc = p->host_slots_c2 / p->w_ref_s;
+    double d = lambda - lc;
+    if (!(d > 0.0)) d = 0.0;
+    const double a2 = (d * p->b3_per_token) / p->host_slots_c2;
+    *t2_out = (a2 > 0.0) ? (p->b3_per_token - p->b2_per_token) / a2
+                         : std::numeric_limits<double>::infinity();
+    return KVR_OK;
+}
+
+int kvr_capacity_replay(const double *d_arrival_s, const double *d_wait_s,
+                        const int32_t *d_ctx_tokens, int64_t n_reps, int64_t n,
+                        const kvr_prices *p, const double *t2, int32_t n_t2, double *d_cost,
+                        int64_t *d_restored_tokens, int64_t *d_admitted, void *d_ws,
+                        size_t *ws_bytes, void *hip_stream)
+{
+    if (!ws_bytes || !t2) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    const double c2d = p->host_slots_c2;
+    if (!(c2d >= 1.0) || c2d != std::floor(c2d) || c2d > 9.0e15) return KVR_E_PRICE;
+    if (n_reps < 1 || n < 1 || n > 8192 || n_t2 < 1 || n_t2 > kMaxLoads) return KVR_E_SIZE;
+    if (n_reps > INT32_MAX / n_t2) return KVR_E_SIZE;
+    for (int32_t k = 0; k < n_t2; ++k)
+        if (std::isnan(t2[k]) || !(t2[k] > 0.0)) return KVR_E_GRID;
+    const size_t need = kStatusBytes + kvr::replay_ws_bytes(n_reps, n, n_t2);
+    if (d_ws == nullptr) {
+        *ws_bytes = need;
+        return KVR_OK;
+    }
+    if (!d_arrival_s || !d_wait_s || !d_cost) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, need)) != KVR_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    KVR_TRY(kvr::launch_clear_status(status, s));
+    KVR_MARK(g_prof_begin, s);
+    KVR_TRY(kvr::launch_replay(d_arrival_s, d_wait_s, d_ctx_tokens, n_reps, n, t2, n_t2,
+                               (int64_t)c2d, p->b2_per_token, p->b3_per_token,
+                               at<char>(d_ws, kStatusBytes), d_cost, d_restored_tokens,
+                               d_admitted, status, s));
+    KVR_MARK(g_prof_end, s);
+    return KVR_OK;
+}
+
 int kvr_set_profile_events(void *ev_begin, void *ev_end)
 {
     if ((ev_begin == nullptr) != (ev_end == nullptr)) return KVR_E_NULL;

@@ -83,6 +83,13 @@ hipError_t launch_select(const double *cost, int64_t batch, int L, int64_t P, in
                          int last_inf, int32_t *best, double *best_cost, int32_t *branch,
                          hipStream_t stream);
 
+// Finite-capacity admission replay (n <= kReplayMaxN requests per sequence).
+size_t replay_ws_bytes(int64_t reps, int64_t n, int K);
+hipError_t launch_replay(const double *arrival, const double *wait, const int32_t *ctx,
+                         int64_t reps, int64_t n, const double *h_t2, int K, int64_t c2, double b2,
+                         double b3, void *ws, double *cost, int64_t *restored,
+                         int64_t *admitted, int *status, hipStream_t stream);
+
 // Sorted path.
 struct SortWs {
     uint64_t *keys[2];

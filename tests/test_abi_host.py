@@ -28,7 +28,7 @@ def lib():
 def _declared():
     text = open(HEADER).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
-    return sorted(set(re.findall(r"\b(kvr_[a-z_]+)\s*\(", text)))
+    return sorted(set(re.findall(r"\b(kvr_[a-z0-9_]+)\s*\(", text)))
 
 
 def test_exports_match_header(lib):
@@ -36,7 +36,7 @@ def test_exports_match_header(lib):
     assert declared == sorted(kvr.EXPORTS)
     out = subprocess.run(["nm", "-D", "--defined-only", kvr.LIB_PATH], check=True,
                          capture_output=True, text=True).stdout
-    exported = sorted(set(re.findall(r"\bT (kvr_[a-z_]+)\b", out)))
+    exported = sorted(set(re.findall(r"\bT (kvr_[a-z0-9_]+)\b", out)))
     assert exported == declared
 
 
@@ -199,6 +199,47 @@ def test_bootstrap_and_select_errors(lib):
     assert sel(FAKE, 1, 0, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
     assert sel(FAKE, 1, 1, 1, 2, 2, FAKE, FAKE, None, None) == kvr.KVR_E_GRID
     assert lib.kvr_workspace_status(None, None) == kvr.KVR_E_NULL
+
+
+def test_eq3_timer_matches_oracle(lib, oracle_mod):
+    """The library's Eq. 3 timer and the oracle's agree bit for bit."""
+    p = kvr.kvr_prices_from_platform(327680, 250e9, 50e9, 20000.0)
+    for mult in (0.0, 0.5, 1.0, 1.0000001, 2.0, 3.0, 17.0):
+        lam = mult * 425.0 / 1800.0
+        got = kvr.kvr_eq3_timer(p, lam)
+        want = oracle_mod.eq3_timer(lam, p.b2_per_token, p.b3_per_token, 425.0, 1800.0)
+        assert got == want or (math.isinf(got) and math.isinf(want))
+    with pytest.raises(kvr.KvrError) as ei:
+        kvr.kvr_eq3_timer(p, math.nan)
+    assert ei.value.code == kvr.KVR_E_GRID
+    assert lib.kvr_eq3_timer(ctypes.byref(p), 0.5, None) == kvr.KVR_E_NULL
+
+
+def test_capacity_replay_host_errors(lib):
+    p = _prices()
+    t2 = (ctypes.c_double * 2)(600.0, math.inf)
+    sz = ctypes.c_size_t(0)
+
+    def call(reps=4, n=100, prices=p, timers=t2, k=2, ws=None):
+        return lib.kvr_capacity_replay(FAKE, FAKE, None, reps, n, ctypes.byref(prices), timers, k,
+                                       FAKE, None, None, ws, ctypes.byref(sz), None)
+
+    assert call() == kvr.KVR_OK and sz.value > 0
+    assert call(n=8193) == kvr.KVR_E_SIZE
+    assert call(n=0) == kvr.KVR_E_SIZE
+    assert call(reps=0) == kvr.KVR_E_SIZE
+    assert call(k=0) == kvr.KVR_E_SIZE
+    bad = (ctypes.c_double * 2)(600.0, math.nan)
+    assert call(timers=bad) == kvr.KVR_E_GRID
+    neg = (ctypes.c_double * 2)(0.0, 1.0)
+    assert call(timers=neg) == kvr.KVR_E_GRID
+    frac = _prices()
+    frac.host_slots_c2 = 425.5
+    assert call(prices=frac) == kvr.KVR_E_PRICE
+    sz.value = 1                                   # far below the size needed
+    assert call(ws=FAKE) == kvr.KVR_E_WORKSPACE
+    assert lib.kvr_capacity_replay(FAKE, FAKE, None, 4, 100, ctypes.byref(p), None, 2, FAKE,
+                                   None, None, None, ctypes.byref(sz), None) == kvr.KVR_E_NULL
 
 
 def test_product_path_has_no_cpu_fallback():
