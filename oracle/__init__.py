@@ -57,6 +57,9 @@ def _configure(lib):
     lib.oracle_capacity_replay.argtypes = [P, P, P, I64, I64, D, D, D, P, P]
     lib.oracle_capacity_replay.restype = D
     lib.oracle_capacity_replay_batch.argtypes = [P, P, P, I64, I64, I64, P, I32, D, D, P, P]
+    lib.oracle_controller_select.argtypes = [P, P, P, I64, I64, I64, D, D, D, D, D, P, P]
+    lib.oracle_crossover_count.argtypes = [P, I64, D, D]
+    lib.oracle_crossover_count.restype = I64
     return lib
 
 
@@ -225,3 +228,40 @@ def capacity_replay_batch(arrival_s, wait_s, c2, t2, b2, b3, ctx=None):
     _load().oracle_capacity_replay_batch(_p(a), _p(w), _p(T), reps, n, int(c2), _p(t2), t2.size,
                                          float(b2), float(b3), _p(cost), _p(rest))
     return cost, rest
+
+
+class Controller:
+    """The frozen host branch and the figures it was chosen from; index 0 of
+    each pair is the Eq. 3 timer branch, index 1 host-retain."""
+    I64 = ("branch", "restored_timer", "restored_retain", "admitted_timer",
+           "admitted_retain", "total_tokens", "n_short", "n_requests")
+    F64 = ("t2_s", "total_cost_timer", "total_cost_retain", "cost_per_request_timer",
+           "cost_per_request_retain", "t_star_s", "p_short")
+
+    def __init__(self, i64, f64):
+        for k, v in zip(self.I64, i64):
+            setattr(self, k, int(v))
+        for k, v in zip(self.F64, f64):
+            setattr(self, k, float(v))
+
+    def as_tuple(self):
+        return tuple(getattr(self, k) for k in self.I64 + self.F64)
+
+
+def controller_select(arrival_s, wait_s, c2, lam, a1, b2, b3, w_ref=1800.0, ctx=None):
+    """Section 3.4 controller on a calibration sample of rows [reps, n]."""
+    a, w = np.atleast_2d(_f64(arrival_s)), np.atleast_2d(_f64(wait_s))
+    T = None if ctx is None else _i32(ctx)
+    reps, n = a.shape
+    i64 = np.zeros(8, dtype=np.int64)
+    f64 = np.zeros(7, dtype=np.float64)
+    _load().oracle_controller_select(_p(a), _p(w), _p(T), reps, n, int(c2), float(lam),
+                                     float(a1), float(b2), float(b3), float(w_ref),
+                                     _p(i64), _p(f64))
+    return Controller(i64, f64)
+
+
+def crossover_count(wait_s, a1, b3) -> int:
+    """Number of waits w <= t* = b3 / a1 (Section 4.3)."""
+    w = _f64(wait_s).ravel()
+    return int(_load().oracle_crossover_count(_p(w), w.size, float(a1), float(b3)))

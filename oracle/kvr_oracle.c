@@ -405,3 +405,75 @@ void oracle_capacity_replay_batch(const double *arrival_s, const double *wait_s,
         if (restored_out) restored_out[q] = rest;
     }
 }
+
+/*
+ * Regime-aware controller (Section 3.4; frozen across loads as in Appendix F).
+ * The same calibration sample -- n_reps sequences of n suspensions -- is
+ * replayed with finite capacity under the two host branches: the Eq. 3 timer
+ * t2(lambda) and host-retain (t2 = +inf).  Each branch's GPU opportunity cost
+ * is totalled over every request of the sample, b2*R + b3*(Ttot - R) with R
+ * the tokens restored from host, and the cheaper branch is frozen; equal
+ * totals keep host-retain (the timer only adds churn then, and below
+ * lambda_crit the two branches are the same policy).  The sample's summary
+ * statistic of Section 4.3 / Figure 4(d) is the fraction of its waits at or
+ * below the break-even time t* = beta_3 / alpha_1.
+ *
+ *   i64_out[8]: branch (0 retain, 1 expire), R[timer], R[retain],
+ *               admitted[timer], admitted[retain], Ttot, #(w <= t*), n_reps*n.
+ *   f64_out[7]: t2(lambda), total cost[timer], total cost[retain],
+ *               cost per request[timer], cost per request[retain], t*, P(W <= t*).
+ */
+void oracle_controller_select(const double *arrival_s, const double *wait_s, const int32_t *ctx,
+                              int64_t n_reps, int64_t n, int64_t c2, double lam, double a1,
+                              double b2, double b3, double w_ref, int64_t *i64_out,
+                              double *f64_out)
+{
+    const double t2 = oracle_eq3_timer(lam, b2, b3, (double)c2, w_ref);
+    const double tstar = b3 / a1;
+    const double timers[2] = {t2, INFINITY};
+    int64_t restored[2] = {0, 0}, admitted[2] = {0, 0}, total = 0, n_short = 0;
+    for (int64_t r = 0; r < n_reps; ++r) {
+        const double *A = arrival_s + r * n, *W = wait_s + r * n;
+        const int32_t *C = ctx ? ctx + r * n : NULL;
+        for (int k = 0; k < 2; ++k) {
+            int64_t rest = 0, adm = 0;
+            oracle_capacity_replay(A, W, C, n, c2, timers[k], b2, b3, &rest, &adm);
+            restored[k] += rest;
+            admitted[k] += adm;
+        }
+        for (int64_t i = 0; i < n; ++i) {
+            total += C ? (int64_t)C[i] : 1;
+            if (W[i] <= tstar) n_short += 1;
+        }
+    }
+    const int64_t requests = n_reps * n;
+    double cost[2];
+    for (int k = 0; k < 2; ++k)
+        cost[k] = b2 * (double)restored[k] + b3 * (double)(total - restored[k]);
+    i64_out[0] = (cost[0] < cost[1]) ? 1 : 0;
+    i64_out[1] = restored[0];
+    i64_out[2] = restored[1];
+    i64_out[3] = admitted[0];
+    i64_out[4] = admitted[1];
+    i64_out[5] = total;
+    i64_out[6] = n_short;
+    i64_out[7] = requests;
+    f64_out[0] = t2;
+    f64_out[1] = cost[0];
+    f64_out[2] = cost[1];
+    f64_out[3] = cost[0] / (double)requests;
+    f64_out[4] = cost[1] / (double)requests;
+    f64_out[5] = tstar;
+    f64_out[6] = (double)n_short / (double)requests;
+}
+
+/* The crossover statistic of Section 4.3 / Figure 4(d) on a bare wait sample:
+ * the number of waits at or below t* = beta_3 / alpha_1. */
+int64_t oracle_crossover_count(const double *wait_s, int64_t n, double a1, double b3)
+{
+    const double t_star = b3 / a1;
+    int64_t c = 0;
+    for (int64_t i = 0; i < n; ++i)
+        if (wait_s[i] <= t_star) c += 1;
+    return c;
+}

@@ -112,3 +112,52 @@ def test_replay_mutant_is_caught(oracle_mod, tmp_path, name):
         assert _replay_pins_pass(oracle) is False, f"mutant {name} survived"
     finally:
         oracle._lib = saved
+
+
+CONTROLLER_MUTANTS = {
+    "ties_expire": ("i64_out[0] = (cost[0] < cost[1]) ? 1 : 0;",
+                    "i64_out[0] = (cost[0] <= cost[1]) ? 1 : 0;"),
+    "branches_swapped": ("const double timers[2] = {t2, INFINITY};",
+                         "const double timers[2] = {INFINITY, t2};"),
+    "short_strict": ("if (W[i] <= tstar) n_short += 1;", "if (W[i] < tstar) n_short += 1;"),
+    "count_strict": ("if (wait_s[i] <= t_star) c += 1;", "if (wait_s[i] < t_star) c += 1;"),
+    "t_star_inverted": ("const double tstar = b3 / a1;", "const double tstar = a1 / b3;"),
+    "no_restore_price": ("cost[k] = b2 * (double)restored[k] + b3 * (double)(total - restored[k]);",
+                         "cost[k] = b3 * (double)(total - restored[k]);"),
+}
+
+
+def _controller_pins_pass(mod):
+    from tests import test_controller_pins as C
+    try:
+        for seed in range(8):
+            for c2 in (1, 2, 3):
+                C.test_controller_is_the_exact_two_branch_replay(mod, seed, c2)
+        C.test_controller_at_or_below_lambda_crit_keeps_retain(mod, 0.5)
+        C.test_crossover_counts_the_break_even_wait(mod)
+        for family in ("lognormal", "mixture"):
+            C.test_controller_freezes_table6_branch(mod, family)
+    except AssertionError:
+        return False
+    return True
+
+
+def test_unmutated_controller_passes(oracle_mod):
+    assert _controller_pins_pass(oracle_mod)
+
+
+@pytest.mark.parametrize("name", sorted(CONTROLLER_MUTANTS))
+def test_controller_mutant_is_caught(oracle_mod, tmp_path, name):
+    old, new = CONTROLLER_MUTANTS[name]
+    src = open(SRC).read()
+    assert src.count(old) == 1, f"mutation site for {name} not unique"
+    mpath = tmp_path / "mutant.c"
+    mpath.write_text(src.replace(old, new))
+    lib = tmp_path / "libmutant.so"
+    oracle.compile_library(str(mpath), str(lib))
+    saved = oracle._lib
+    try:
+        oracle._lib = oracle._configure(ctypes.CDLL(str(lib)))
+        assert _controller_pins_pass(oracle) is False, f"mutant {name} survived"
+    finally:
+        oracle._lib = saved

@@ -171,18 +171,24 @@ def make(name: str, resamples: Optional[int] = None) -> Workload:
 FAMILIES = ("lognormal", "exponential", "mixture")
 
 
-def family_waits(rng: np.random.Generator, family: str, n: int) -> np.ndarray:
+def family_waits(rng: np.random.Generator, family: str, n: int,
+                 short_weight: float = 0.5) -> np.ndarray:
     """The approval-wait families of Section 4.1, each with mean 1,800 s:
     LogNormal(sigma 1); Exponential; 0.5 Exp(mean 60 s) + 0.5 LogNormal(sigma
-    0.7, mean 3,540 s)."""
+    0.7, mean 3,540 s).  ``short_weight`` changes the mixture's share of short
+    approvals; the long component's mean then keeps the overall mean at
+    1,800 s (3,540 s at the default 0.5)."""
     if family == "lognormal":
         return rng.lognormal(math.log(1800.0) - 0.5, 1.0, n)
     if family == "exponential":
         return rng.exponential(1800.0, n)
     if family == "mixture":
-        short = rng.random(n) < 0.5
+        if not 0.0 <= short_weight < 1.0:
+            raise ValueError("short_weight must be in [0, 1)")
+        long_mean = (1800.0 - 60.0 * short_weight) / (1.0 - short_weight)
+        short = rng.random(n) < short_weight
         return np.where(short, rng.exponential(60.0, n),
-                        rng.lognormal(math.log(3540.0) - 0.5 * 0.7 * 0.7, 0.7, n))
+                        rng.lognormal(math.log(long_mean) - 0.5 * 0.7 * 0.7, 0.7, n))
     raise KeyError(family)
 
 
@@ -203,14 +209,19 @@ class ReplayCase:
 
 
 def replay_case(family: str, rate_per_s: float, reps: int, n: int = 4000,
-                seed: int = 2000) -> ReplayCase:
+                seed: int = 2000, short_weight: float = 0.5) -> ReplayCase:
     """``reps`` independent request sequences of ``n`` suspensions: Poisson
-    arrivals at ``rate_per_s`` starting at time 0, waits from ``family``."""
+    arrivals at ``rate_per_s`` starting at time 0, waits from ``family``
+    (``short_weight`` as in family_waits; it also seeds the mixture's draws
+    when it is not the default)."""
     fam = FAMILIES.index(family)
-    ss = np.random.SeedSequence([seed, fam, int(round(rate_per_s * 1e9))])
+    key = [seed, fam, int(round(rate_per_s * 1e9))]
+    if short_weight != 0.5:
+        key.append(int(round(short_weight * 1e6)))
+    ss = np.random.SeedSequence(key)
     ra, rw = [np.random.Generator(np.random.PCG64(s)) for s in ss.spawn(2)]
     arr = np.cumsum(ra.exponential(1.0 / rate_per_s, (reps, n)), axis=1)
-    w = np.stack([family_waits(rw, family, n) for _ in range(reps)])
+    w = np.stack([family_waits(rw, family, n, short_weight) for _ in range(reps)])
     return ReplayCase(family, rate_per_s, arr, w)
 
 
