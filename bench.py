@@ -290,6 +290,41 @@ def time_replay(kvr, workloads, torch, reps: int = 8192):
         res[key] = {"ms": ms, "replayed_requests": events,
                     "replayed_requests_per_s": events / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
+    res.update(time_controller(kvr, workloads, torch, pr, reps))
+    return res
+
+
+def time_controller(kvr, workloads, torch, pr, reps: int):
+    """The Section 3.4 controller calibrated at 2 lambda_crit on ``reps``
+    sequences of 4,000 requests per wait family: both branches replayed,
+    totals, frozen branch and P(W <= t*), all on the device."""
+    res = {}
+    lc = 425.0 / 1800.0
+    pr.a1_per_token = 0.0176
+    for family in workloads.FAMILIES:
+        rc = workloads.replay_case(family, 2 * lc, reps=reps, seed=77)
+        arr = torch.as_tensor(rc.arrival_s).cuda()
+        w = torch.as_tensor(rc.wait_s).cuda()
+        call = kvr.ControllerCall(arr, w, pr, 2 * lc)
+        call.launch()
+        out = call.result()
+        times = []
+        for _ in range(5):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            call.launch()
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        ms = sorted(times)[len(times) // 2]
+        events = reps * 2 * rc.n
+        key = f"controller-{family}-2x/{reps}x{rc.n}"
+        res[key] = {"ms": ms, "replayed_requests": events,
+                    "replayed_requests_per_s": events / (ms * 1e-3),
+                    "branch": "expire" if out.branch == kvr.KVR_EXPIRE else "retain",
+                    "p_short": out.p_short}
+        log(f"[bench] path {key}: {ms:.3f} ms, branch {res[key]['branch']}, "
+            f"P(W<=t*) {out.p_short:.4f}")
     return res
 
 

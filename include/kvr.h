@@ -218,6 +218,65 @@ int kvr_capacity_replay(const double *d_arrival_s, const double *d_wait_s,
                         double *d_cost, int64_t *d_restored_tokens, int64_t *d_admitted,
                         void *d_ws, size_t *ws_bytes, void *hip_stream);
 
+/* Result of kvr_controller_select, written to device memory by the library.
+ * Every field is 8 bytes wide (120 bytes, no padding).  In each pair, index 0
+ * is the Eq. 3 timer branch and index 1 is host-retain. */
+typedef struct {
+    int64_t branch;              /* KVR_RETAIN (also on equal totals) or KVR_EXPIRE */
+    int64_t restored_tokens[2];  /* tokens restored from host over the whole sample */
+    int64_t admitted[2];         /* requests admitted to the host tier */
+    int64_t total_tokens;        /* context tokens over the whole sample */
+    int64_t n_short;             /* waits w <= t* */
+    int64_t n_requests;          /* n_reps * n */
+    double t2_s;                 /* Eq. 3 timer at lambda; +inf at or below lambda_crit */
+    double total_cost[2];        /* b2*R + b3*(Ttot - R), GPU-s, summed over the sample */
+    double cost_per_request[2];  /* total_cost / n_requests */
+    double t_star_s;             /* break-even time t* = beta_3 / alpha_1 */
+    double p_short;              /* n_short / n_requests, i.e. P(W <= t*) */
+} kvr_controller_out;
+
+/*
+ * Regime-aware controller (Section 3.4; calibrated once and frozen across
+ * loads, Appendix F).  Replays the calibration sample with finite host
+ * capacity exactly as kvr_capacity_replay does, under the Eq. 3 timer
+ * t2(lambda) and under host-retain; totals each branch's GPU opportunity cost
+ * over the whole sample, b2*R + b3*(Ttot - R); freezes the cheaper branch.
+ * Equal totals keep host-retain (at or below lambda_crit the two branches are
+ * one policy).  At run time a frozen KVR_EXPIRE branch needs only the offered
+ * load: kvr_eq3_timer gives its timer.  The same call reports the summary
+ * statistic of Section 4.3 / Figure 4(d): the share of calibration waits at
+ * or below the break-even time t* = beta_3 / alpha_1.
+ *   d_arrival_s, d_wait_s, d_ctx_tokens, n_reps, n: the calibration sample,
+ *                   laid out and validated as in kvr_capacity_replay (its
+ *                   arrivals are expected to be drawn at the load lambda).
+ *   p               host: every field is used (alpha_1 for t*); C2 must be an
+ *                   integer >= 1 (else KVR_E_PRICE).
+ *   lambda          host: calibration load, suspended requests per second,
+ *                   finite and >= 0 (else KVR_E_GRID).
+ *   d_out           device: one kvr_controller_out, written by the call.
+ *   Sizes: 1 <= n <= 8192, n_reps * 2 <= 2^31 - 1.  Workspace: two-phase
+ *   sizing as above.
+ */
+int kvr_controller_select(const double *d_arrival_s, const double *d_wait_s,
+                          const int32_t *d_ctx_tokens, int64_t n_reps, int64_t n,
+                          const kvr_prices *p, double lambda, kvr_controller_out *d_out,
+                          void *d_ws, size_t *ws_bytes, void *hip_stream);
+
+/*
+ * The crossover statistic of Section 4.3 / Figure 4(d) on any wait sample:
+ * the share of waits at or below t* = beta_3 / alpha_1 (a rank query; the
+ * library counts rather than sorts).
+ *   d_wait_s        device, float64 [n]: waits, finite and >= 0 (else
+ *                   KVR_E_DOMAIN through the workspace status word).
+ *   p               host: a1 and b3 give t*; every field must be valid.
+ *   d_count         device, int64 [1]: the number of waits w <= t* (exact).
+ *   d_fraction      device, float64 [1] or NULL: d_count / n.
+ *   Sizes: 1 <= n <= 2^40.  Workspace: two-phase sizing as above.
+ */
+int kvr_crossover_statistic(const double *d_wait_s, int64_t n, const kvr_prices *p,
+                            int64_t *d_count, double *d_fraction, void *d_ws, size_t *ws_bytes,
+                            void *hip_stream);
+
 /*
  * Instrumentation for benchmarks.  After this call, every kvr_cost_grid and
  * kvr_bootstrap call made from the same host thread records ev_begin (a

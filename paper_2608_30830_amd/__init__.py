@@ -30,8 +30,9 @@ KVR_RETAIN = 0
 KVR_EXPIRE = 1
 
 EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy",
-           "kvr_bootstrap", "kvr_eq3_timer", "kvr_capacity_replay", "kvr_workspace_status",
-           "kvr_set_profile_events", "kvr_status_string")
+           "kvr_bootstrap", "kvr_eq3_timer", "kvr_capacity_replay", "kvr_controller_select",
+           "kvr_crossover_statistic", "kvr_workspace_status", "kvr_set_profile_events",
+           "kvr_status_string")
 
 
 class kvr_prices(ctypes.Structure):
@@ -44,6 +45,17 @@ class kvr_policy_grid(ctypes.Structure):
     _fields_ = [("t1", ctypes.POINTER(ctypes.c_double)), ("n_t1", ctypes.c_int32),
                 ("t2", ctypes.POINTER(ctypes.c_double)), ("n_t2", ctypes.c_int32),
                 ("lam", ctypes.POINTER(ctypes.c_double)), ("n_lam", ctypes.c_int32)]
+
+
+class kvr_controller_out(ctypes.Structure):
+    """Device-written result of kvr_controller_select; in each pair index 0 is
+    the Eq. 3 timer branch, index 1 host-retain."""
+    _fields_ = [("branch", ctypes.c_int64), ("restored_tokens", ctypes.c_int64 * 2),
+                ("admitted", ctypes.c_int64 * 2), ("total_tokens", ctypes.c_int64),
+                ("n_short", ctypes.c_int64), ("n_requests", ctypes.c_int64),
+                ("t2_s", ctypes.c_double), ("total_cost", ctypes.c_double * 2),
+                ("cost_per_request", ctypes.c_double * 2), ("t_star_s", ctypes.c_double),
+                ("p_short", ctypes.c_double)]
 
 
 class KvrError(RuntimeError):
@@ -82,6 +94,11 @@ def load_library(path: str = LIB_PATH):
     lib.kvr_capacity_replay.argtypes = [P, P, P, I64, I64, ctypes.POINTER(kvr_prices), P, I32,
                                         P, P, P, P, SZ, P]
     lib.kvr_capacity_replay.restype = ctypes.c_int
+    lib.kvr_controller_select.argtypes = [P, P, P, I64, I64, ctypes.POINTER(kvr_prices), D, P,
+                                          P, SZ, P]
+    lib.kvr_controller_select.restype = ctypes.c_int
+    lib.kvr_crossover_statistic.argtypes = [P, I64, ctypes.POINTER(kvr_prices), P, P, P, SZ, P]
+    lib.kvr_crossover_statistic.restype = ctypes.c_int
     lib.kvr_set_profile_events.argtypes = [P, P]
     lib.kvr_set_profile_events.restype = ctypes.c_int
     lib.kvr_status_string.argtypes = [ctypes.c_int]
@@ -292,6 +309,83 @@ def kvr_capacity_replay(arrival_s, wait_s, prices: kvr_prices, t2: Sequence[floa
     if check:
         _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_capacity_replay(device)")
     return cost, rest, adm
+
+
+class ControllerCall:
+    """kvr_controller_select with its buffers allocated once: launch() only
+    enqueues the library's kernels; result() copies the device struct back."""
+
+    def __init__(self, arrival_s, wait_s, prices: kvr_prices, lam: float, ctx_tokens=None,
+                 stream=None):
+        torch = _torch()
+        self.lib = load_library()
+        _need(arrival_s, torch.float64, "arrival_s")
+        _need(wait_s, torch.float64, "wait_s")
+        if ctx_tokens is not None:
+            _need(ctx_tokens, torch.int32, "ctx_tokens")
+        if arrival_s.dim() != 2 or tuple(wait_s.shape) != tuple(arrival_s.shape):
+            raise ValueError("arrival_s and wait_s must both be [n_reps, n]")
+        if ctx_tokens is not None and tuple(ctx_tokens.shape) != tuple(arrival_s.shape):
+            raise ValueError("ctx_tokens must be [n_reps, n]")
+        self.args = (arrival_s, wait_s, ctx_tokens)
+        self.reps, self.n = arrival_s.shape
+        self.prices, self.lam = prices, float(lam)
+        need = ctypes.c_size_t(0)
+        _check(self.lib.kvr_controller_select(None, None, None, self.reps, self.n,
+                                              ctypes.byref(prices), self.lam, None, None,
+                                              ctypes.byref(need), None),
+               "kvr_controller_select(size)")
+        self.ws = _workspace(need.value)
+        self.out = torch.empty(ctypes.sizeof(kvr_controller_out), dtype=torch.uint8,
+                               device="cuda")
+        self.stream = _stream_ptr(stream)
+
+    def launch(self) -> None:
+        a, w, T = self.args
+        have = ctypes.c_size_t(self.ws.numel())
+        _check(self.lib.kvr_controller_select(_ptr(a), _ptr(w), _ptr(T), self.reps, self.n,
+                                              ctypes.byref(self.prices), self.lam,
+                                              _ptr(self.out), _ptr(self.ws), ctypes.byref(have),
+                                              self.stream),
+               "kvr_controller_select")
+
+    def result(self) -> kvr_controller_out:
+        _check(self.lib.kvr_workspace_status(_ptr(self.ws), self.stream),
+               "kvr_controller_select(device)")
+        host = self.out.cpu()
+        res = kvr_controller_out()
+        ctypes.memmove(ctypes.byref(res), host.data_ptr(), ctypes.sizeof(res))
+        return res
+
+
+def kvr_controller_select(arrival_s, wait_s, prices: kvr_prices, lam: float, ctx_tokens=None,
+                          stream=None) -> kvr_controller_out:
+    """Section 3.4 controller on a calibration sample [n_reps, n]."""
+    call = ControllerCall(arrival_s, wait_s, prices, lam, ctx_tokens, stream)
+    call.launch()
+    return call.result()
+
+
+def kvr_crossover_statistic(wait_s, prices: kvr_prices, stream=None, check: bool = True):
+    """P(W <= t*) of a wait sample: (count, fraction), device tensors of one element."""
+    torch = _torch()
+    lib = load_library()
+    _need(wait_s, torch.float64, "wait_s")
+    n = wait_s.numel()
+    need = ctypes.c_size_t(0)
+    _check(lib.kvr_crossover_statistic(None, n, ctypes.byref(prices), None, None, None,
+                                       ctypes.byref(need), None), "kvr_crossover_statistic(size)")
+    ws = _workspace(need.value)
+    count = torch.empty(1, dtype=torch.int64, device="cuda")
+    frac = torch.empty(1, dtype=torch.float64, device="cuda")
+    have = ctypes.c_size_t(ws.numel())
+    st = _stream_ptr(stream)
+    _check(lib.kvr_crossover_statistic(_ptr(wait_s), n, ctypes.byref(prices), _ptr(count),
+                                       _ptr(frac), _ptr(ws), ctypes.byref(have), st),
+           "kvr_crossover_statistic")
+    if check:
+        _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_crossover_statistic(device)")
+    return count, frac
 
 
 def kvr_set_profile_events(ev_begin, ev_end) -> None:

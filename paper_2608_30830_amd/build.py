@@ -13,7 +13,8 @@ OUT_DIR = os.path.join(PKG, "_build")
 LIB = os.path.join(OUT_DIR, "libkvr.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
-SOURCES = ["kvr_api.cpp", "kvr_grid.hip", "kvr_aux.hip", "kvr_sorted.hip", "kvr_replay.hip"]
+SOURCES = ["kvr_api.cpp", "kvr_grid.hip", "kvr_aux.hip", "kvr_sorted.hip", "kvr_replay.hip",
+           "kvr_controller.hip"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
           # no packed-fp32 instruction selection anywhere
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

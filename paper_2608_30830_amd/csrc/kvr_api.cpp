@@ -412,6 +412,75 @@ int kvr_capacity_replay(const double *d_arrival_s, const double *d_wait_s,
     return KVR_OK;
 }
 
+int kvr_controller_select(const double *d_arrival_s, const double *d_wait_s,
+                          const int32_t *d_ctx_tokens, int64_t n_reps, int64_t n,
+                          const kvr_prices *p, double lambda, kvr_controller_out *d_out,
+                          void *d_ws, size_t *ws_bytes, void *hip_stream)
+{
+    if (!ws_bytes) return KVR_E_NULL;
+    int rc;
+    double t2 = 0.0;
+    if ((rc = kvr_eq3_timer(p, lambda, &t2)) != KVR_OK) return rc;
+    const double c2d = p->host_slots_c2;
+    if (!(c2d >= 1.0) || c2d != std::floor(c2d) || c2d > 9.0e15) return KVR_E_PRICE;
+    if (n_reps < 1 || n < 1 || n > 8192 || n_reps > INT32_MAX / 2) return KVR_E_SIZE;
+    const double t_star = p->b3_per_token / p->a1_per_token;
+    const int64_t reps = n_reps;
+    const size_t off_replay = kStatusBytes;
+    const size_t off_cost = off_replay + align256(kvr::replay_ws_bytes(reps, n, 2));
+    const size_t off_rest = off_cost + align256(sizeof(double) * 2 * (size_t)reps);
+    const size_t off_adm = off_rest + align256(sizeof(int64_t) * 2 * (size_t)reps);
+    const size_t off_cnt = off_adm + align256(sizeof(int64_t) * 2 * (size_t)reps);
+    const size_t need = off_cnt + align256(kvr::count_ws_bytes());
+    if (d_ws == nullptr) {
+        *ws_bytes = need;
+        return KVR_OK;
+    }
+    if (!d_arrival_s || !d_wait_s || !d_out) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, need)) != KVR_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    int64_t *rest = at<int64_t>(d_ws, off_rest), *adm = at<int64_t>(d_ws, off_adm);
+    const double timers[2] = {t2, std::numeric_limits<double>::infinity()};
+    KVR_TRY(kvr::launch_clear_status(status, s));
+    KVR_MARK(g_prof_begin, s);
+    KVR_TRY(kvr::launch_replay(d_arrival_s, d_wait_s, d_ctx_tokens, reps, n, timers, 2,
+                               (int64_t)c2d, p->b2_per_token, p->b3_per_token,
+                               at<char>(d_ws, off_replay), at<double>(d_ws, off_cost), rest, adm,
+                               status, s));
+    KVR_TRY(kvr::launch_short_count(d_wait_s, d_ctx_tokens, reps * n, t_star,
+                                    at<char>(d_ws, off_cnt), status, s));
+    KVR_TRY(kvr::launch_controller_final(rest, adm, reps, reps * n, at<char>(d_ws, off_cnt), t2,
+                                         t_star, p->b2_per_token, p->b3_per_token, d_out, s));
+    KVR_MARK(g_prof_end, s);
+    return KVR_OK;
+}
+
+int kvr_crossover_statistic(const double *d_wait_s, int64_t n, const kvr_prices *p,
+                            int64_t *d_count, double *d_fraction, void *d_ws, size_t *ws_bytes,
+                            void *hip_stream)
+{
+    if (!ws_bytes) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if (n < 1 || n > kMaxBatch) return KVR_E_SIZE;
+    const size_t need = kStatusBytes + align256(kvr::count_ws_bytes());
+    if (d_ws == nullptr) {
+        *ws_bytes = need;
+        return KVR_OK;
+    }
+    if (!d_wait_s || !d_count) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, need)) != KVR_OK) return rc;
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    void *cnt = at<char>(d_ws, kStatusBytes);
+    KVR_TRY(kvr::launch_clear_status(status, s));
+    KVR_TRY(kvr::launch_short_count(d_wait_s, nullptr, n, p->b3_per_token / p->a1_per_token, cnt,
+                                    status, s));
+    KVR_TRY(kvr::launch_fraction(cnt, n, d_count, d_fraction, s));
+    return KVR_OK;
+}
+
 int kvr_set_profile_events(void *ev_begin, void *ev_end)
 {
     if ((ev_begin == nullptr) != (ev_end == nullptr)) return KVR_E_NULL;

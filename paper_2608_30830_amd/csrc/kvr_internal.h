@@ -4,6 +4,8 @@
 #include <hip/hip_runtime.h>
 #include <stdint.h>
 
+#include "kvr.h"
+
 namespace kvr {
 
 constexpr int kWave = 64;          // CDNA wavefront width
@@ -89,6 +91,18 @@ hipError_t launch_replay(const double *arrival, const double *wait, const int32_
                          int64_t reps, int64_t n, const double *h_t2, int K, int64_t c2, double b2,
                          double b3, void *ws, double *cost, int64_t *restored,
                          int64_t *admitted, int *status, hipStream_t stream);
+
+// Controller tail: share of waits <= t_star and token total over N waits,
+// then the branch totals from the replay's per-row counts [reps][2].
+size_t count_ws_bytes();
+hipError_t launch_short_count(const double *wait, const int32_t *ctx, int64_t N, double t_star,
+                              void *count_ws, int *status, hipStream_t stream);
+hipError_t launch_fraction(const void *count_ws, int64_t N, int64_t *count, double *fraction,
+                           hipStream_t stream);
+hipError_t launch_controller_final(const int64_t *restored, const int64_t *admitted,
+                                   int64_t reps, int64_t n_requests, const void *count_ws,
+                                   double t2, double t_star, double b2, double b3,
+                                   kvr_controller_out *out, hipStream_t stream);
 
 // Sorted path.
 struct SortWs {

@@ -242,6 +242,73 @@ def test_capacity_replay_host_errors(lib):
                                    None, None, None, ctypes.byref(sz), None) == kvr.KVR_E_NULL
 
 
+def test_controller_out_layout():
+    """The device-written result struct is 15 eight-byte fields, no padding,
+    in the order the header declares."""
+    assert ctypes.sizeof(kvr.kvr_controller_out) == 120
+    assert kvr.kvr_controller_out.t2_s.offset == 64
+    assert kvr.kvr_controller_out.p_short.offset == 112
+    text = open(HEADER).read()
+    body = text[text.index("typedef struct {\n    int64_t branch;"):]
+    body = body[:body.index("} kvr_controller_out;")]
+    names = re.findall(r"(?:int64_t|double) ([a-z0-9_]+)", body)
+    assert names == [f[0] for f in kvr.kvr_controller_out._fields_]
+
+
+def test_controller_host_errors(lib):
+    p = _prices()
+    sz = ctypes.c_size_t(0)
+
+    def call(reps=4, n=100, prices=p, lam=0.5, ws=None, out=FAKE):
+        return lib.kvr_controller_select(FAKE, FAKE, None, reps, n, ctypes.byref(prices), lam,
+                                         out, ws, ctypes.byref(sz), None)
+
+    assert call() == kvr.KVR_OK and sz.value > 0
+    small = sz.value
+    assert call(reps=64) == kvr.KVR_OK and sz.value > small
+    assert call(n=8193) == kvr.KVR_E_SIZE
+    assert call(n=0) == kvr.KVR_E_SIZE
+    assert call(reps=0) == kvr.KVR_E_SIZE
+    assert call(reps=2 ** 30) == kvr.KVR_E_SIZE
+    for lam in (math.nan, -1.0, math.inf):
+        assert call(lam=lam) == kvr.KVR_E_GRID
+    frac = _prices()
+    frac.host_slots_c2 = 425.5
+    assert call(prices=frac) == kvr.KVR_E_PRICE
+    zero = _prices()
+    zero.a1_per_token = 0.0
+    assert call(prices=zero) == kvr.KVR_E_PRICE
+    assert lib.kvr_controller_select(FAKE, FAKE, None, 4, 100, None, 0.5, FAKE, None,
+                                     ctypes.byref(sz), None) == kvr.KVR_E_NULL
+    assert lib.kvr_controller_select(FAKE, FAKE, None, 4, 100, ctypes.byref(p), 0.5, FAKE, None,
+                                     None, None) == kvr.KVR_E_NULL
+    sz.value = 1                                   # far below the size needed
+    assert call(ws=FAKE) == kvr.KVR_E_WORKSPACE
+    call()
+    assert call(ws=FAKE, out=None) == kvr.KVR_E_NULL
+
+
+def test_crossover_statistic_host_errors(lib):
+    p = _prices()
+    sz = ctypes.c_size_t(0)
+
+    def call(n=100, prices=p, ws=None, count=FAKE):
+        return lib.kvr_crossover_statistic(FAKE, n, ctypes.byref(prices), count, None, ws,
+                                           ctypes.byref(sz), None)
+
+    assert call() == kvr.KVR_OK and sz.value > 0
+    assert call(n=0) == kvr.KVR_E_SIZE
+    assert call(n=2 ** 41) == kvr.KVR_E_SIZE
+    bad = _prices()
+    bad.b3_per_token = math.nan
+    assert call(prices=bad) == kvr.KVR_E_PRICE
+    need = sz.value
+    sz.value = need - 1
+    assert call(ws=FAKE) == kvr.KVR_E_WORKSPACE
+    sz.value = need
+    assert call(ws=FAKE, count=None) == kvr.KVR_E_NULL
+
+
 def test_product_path_has_no_cpu_fallback():
     """The binding never imports the oracle and has no CPU arithmetic path."""
     src = open(os.path.join(ROOT, "paper_2608_30830_amd", "__init__.py")).read()

@@ -1,0 +1,149 @@
+"""GPU parity of the regime-aware controller (kvr_controller_select) and the
+crossover statistic (kvr_crossover_statistic) against the oracle.  Every
+field of the controller's result is compared exactly: the counts are
+integers, and both sides form the totals b2*R + b3*(Ttot - R) from them with
+the same three roundings and divide once, correctly rounded."""
+import math
+
+import numpy as np
+import pytest
+
+import workloads
+from tests.test_controller_pins import A1, B2, B3, LC, TABLE3, _lam_for_timer, crossing
+from tests.test_replay_pins import _tiny
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kvr():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2608_30830_amd as k
+    k.load_library()
+    return k
+
+
+def _dev(x, dtype):
+    import torch
+    return torch.as_tensor(np.ascontiguousarray(x)).to(device="cuda", dtype=dtype)
+
+
+def _prices(kvr, a1=A1, b2=B2, b3=B3, c2=425.0):
+    p = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, c2, 1800.0)
+    p.a1_per_token, p.b2_per_token, p.b3_per_token = a1, b2, b3
+    return p
+
+
+def _gpu(kvr, arr, w, lam, c2, T=None, a1=A1, b3=B3):
+    import torch
+    arr, w = np.atleast_2d(arr), np.atleast_2d(w)
+    Td = None if T is None else _dev(np.atleast_2d(T), torch.int32)
+    return kvr.kvr_controller_select(_dev(arr, torch.float64), _dev(w, torch.float64),
+                                     _prices(kvr, a1=a1, b3=b3, c2=float(c2)), lam, ctx_tokens=Td)
+
+
+def _same(g, o):
+    assert g.branch == o.branch
+    assert (g.restored_tokens[0], g.restored_tokens[1]) == (o.restored_timer, o.restored_retain)
+    assert (g.admitted[0], g.admitted[1]) == (o.admitted_timer, o.admitted_retain)
+    assert (g.total_tokens, g.n_short, g.n_requests) == (o.total_tokens, o.n_short, o.n_requests)
+    pairs = [(g.t2_s, o.t2_s), (g.total_cost[0], o.total_cost_timer),
+             (g.total_cost[1], o.total_cost_retain), (g.cost_per_request[0], o.cost_per_request_timer),
+             (g.cost_per_request[1], o.cost_per_request_retain), (g.t_star_s, o.t_star_s),
+             (g.p_short, o.p_short)]
+    for a, b in pairs:
+        assert a == b or (math.isinf(a) and math.isinf(b)), pairs
+
+
+def _check(kvr, oracle_mod, arr, w, lam, c2, T=None, a1=A1, b3=B3):
+    g = _gpu(kvr, arr, w, lam, c2, T, a1, b3)
+    o = oracle_mod.controller_select(arr, w, c2, lam, a1, B2, b3, ctx=T)
+    _same(g, o)
+    return g, o
+
+
+@pytest.mark.parametrize("seed", range(16))
+def test_controller_tiny_crafted(kvr, oracle_mod, seed):
+    arr, w, T = _tiny(seed)
+    for c2 in (1, 2, 3):
+        for t2 in (5.0, 12.0, 40.0):
+            _check(kvr, oracle_mod, arr, w, _lam_for_timer(c2, t2), c2, T)
+
+
+@pytest.mark.parametrize("n", [1, 33, 4000, 8192])
+def test_controller_ragged_with_contexts(kvr, oracle_mod, n):
+    rc = workloads.replay_case("lognormal", 2 * LC, reps=5, n=n, seed=9)
+    T = np.random.Generator(np.random.PCG64(n)).integers(1, 32768, rc.arrival_s.shape)
+    _check(kvr, oracle_mod, rc.arrival_s, rc.wait_s, 2 * LC, 425, T.astype(np.int32))
+
+
+@pytest.mark.parametrize("family", workloads.FAMILIES)
+def test_controller_table6_calibrations(kvr, oracle_mod, family):
+    """The calibration the Table 6 controller runs, at every load of the
+    sweep; the branch at 2 lambda_crit is the printed one (retain, retain,
+    timer)."""
+    for mult in (0.5, 1.0, 2.0, 3.0):
+        rc = workloads.replay_case(family, mult * LC, reps=64, seed=77)
+        g, _ = _check(kvr, oracle_mod, rc.arrival_s, rc.wait_s, mult * LC, 425)
+        if mult <= 1.0:
+            assert g.branch == kvr.KVR_RETAIN and math.isinf(g.t2_s)
+        if mult == 2.0:
+            assert g.branch == (kvr.KVR_EXPIRE if family == "mixture" else kvr.KVR_RETAIN)
+
+
+@pytest.mark.parametrize("platform,a1,b3,t_star,printed", TABLE3)
+def test_controller_crossover_sweep(kvr, oracle_mod, platform, a1, b3, t_star, printed):
+    """Figure 4(d)'s sweep of the mixture's short-approval share: every point
+    identical to the oracle's, so the crossing is too, and it sits at the
+    printed P(W <= t*) within 0.03."""
+    pts = []
+    for q in np.linspace(0.2, 0.7, 11):
+        rc = workloads.replay_case("mixture", 2 * LC, reps=60, seed=404, short_weight=q)
+        g, _ = _check(kvr, oracle_mod, rc.arrival_s, rc.wait_s, 2 * LC, 425, a1=a1, b3=b3)
+        pts.append((g.p_short, g.total_cost[1] / g.total_cost[0] - 1.0, g.branch))
+    x = crossing(pts)
+    assert x is not None and abs(x - printed) <= 0.03, (platform, x)
+
+
+@pytest.mark.parametrize("name", ["tiny-exp-1k", "mix-64k", "weibull-1m"])
+def test_crossover_statistic_on_workloads(kvr, oracle_mod, name):
+    import torch
+    wl = workloads.make(name)
+    pr = oracle_mod.workload_prices(wl)
+    p = _prices(kvr, a1=pr.a1, b2=pr.b2, b3=pr.b3)
+    count, frac = kvr.kvr_crossover_statistic(_dev(wl.wait_s, torch.float64), p)
+    want = oracle_mod.crossover_count(wl.wait_s, pr.a1, pr.b3)
+    assert int(count.item()) == want
+    assert float(frac.item()) == want / wl.n
+
+
+def test_crossover_statistic_boundary_and_sizes(kvr, oracle_mod):
+    import torch
+    a1, b3 = 0.0232, 2.61
+    t_star = b3 / a1
+    p = _prices(kvr, a1=a1, b3=b3)
+    w = np.array([0.0, t_star, np.nextafter(t_star, np.inf), 1e6, t_star / 2])
+    count, frac = kvr.kvr_crossover_statistic(_dev(w, torch.float64), p)
+    assert int(count.item()) == 3 and float(frac.item()) == 0.6
+    rng = np.random.Generator(np.random.PCG64(5))
+    for n in (1, 63, 64, 65, 2047, 2049, 1 << 22):
+        w = rng.exponential(100.0, n)
+        count, _ = kvr.kvr_crossover_statistic(_dev(w, torch.float64), p)
+        assert int(count.item()) == oracle_mod.crossover_count(w, a1, b3), n
+
+
+def test_controller_and_statistic_domain_errors(kvr):
+    import torch
+    rc = workloads.replay_case("exponential", 2 * LC, reps=2, n=500, seed=4)
+    w = rc.wait_s.copy()
+    w[1, 9] = np.nan
+    with pytest.raises(kvr.KvrError) as ei:
+        kvr.kvr_controller_select(_dev(rc.arrival_s, torch.float64), _dev(w, torch.float64),
+                                  _prices(kvr), 2 * LC)
+    assert ei.value.code == kvr.KVR_E_DOMAIN
+    for bad in (np.nan, -1.0, np.inf):
+        w = np.array([1.0, 2.0, bad, 4.0])
+        with pytest.raises(kvr.KvrError) as ei:
+            kvr.kvr_crossover_statistic(_dev(w, torch.float64), _prices(kvr))
+        assert ei.value.code == kvr.KVR_E_DOMAIN
