@@ -120,6 +120,9 @@ def main() -> int:
                     help="bootstrap rows the CPU oracle evaluates for cpu_baseline")
     ap.add_argument("--paths", action="store_true",
                     help="also time the other entry points on their workloads")
+    ap.add_argument("--replay-only", action="store_true",
+                    help="time only the admission replay and the controller, then exit")
+    ap.add_argument("--replay-reps", type=int, default=8192)
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
@@ -135,6 +138,11 @@ def main() -> int:
 
     import paper_2608_30830_amd as kvr
     import workloads
+
+    if args.replay_only:
+        print(json.dumps({"paths": time_replay(kvr, workloads, torch, args.replay_reps)}),
+              flush=True)
+        return 0
 
     log(f"[bench] workload {args.workload}: generating inputs")
     wl = workloads.make(args.workload, resamples=args.resamples)
