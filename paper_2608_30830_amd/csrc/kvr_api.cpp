@@ -97,6 +97,10 @@ struct BrutePlan {
     bool fused;              // nsplit == 1: costs finalised inside the grid kernel
     // workspace offsets
     size_t off_t1, off_t2, off_a2, off_X, off_G, off_xgp, off_cand, off_part, off_cost, total;
+    size_t off_binT, off_lb, off_S;
+    int64_t r3_bins;         // finite grid deadlines (bins kept per resample)
+    int r3_nsplit;
+    int64_t r3_split_len;
 };
 
 int choose_tile(int32_t L)
@@ -105,7 +109,8 @@ int choose_tile(int32_t L)
     int best = 32;
     int64_t best_cost = std::numeric_limits<int64_t>::max();
     for (int c : cands) {
-        // issue slots per sample: ~5 load-free ops per tile plus one FMA per load
+        // issue slots per sample: ~5 per tile (forming h, the staged reads, the
+        // loop) plus one FMA per load
         const int64_t cost = cdiv(L, c) * (c + 5);
         if (cost < best_cost) {
             best_cost = cost;
@@ -115,9 +120,10 @@ int choose_tile(int32_t L)
     return best;
 }
 
-BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bool bootstrap,
+BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, bool bootstrap,
                      bool want_cost)
 {
+    const int32_t K1 = g.n_t1, K2 = g.n_t2, L = g.n_lam;
     BrutePlan bp{};
     GridPlan &gp = bp.gp;
     const int64_t P = (int64_t)K1 * K2;
@@ -133,7 +139,7 @@ BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bo
     else gp.mode = kvr::kModeRows2;
     gp.ngroups = (gp.mode == kvr::kModePerLane) ? R * gp.nblk : cdiv(R * P, kvr::kWave);
     const int64_t base_waves = gp.ngroups * gp.ntiles;
-    const int64_t target = choose_splits(base_waves, m, R * gp.ntiles * (gp.LT + 1) * P);
+    const int64_t target = choose_splits(base_waves, m, R * gp.ntiles * gp.LT * P);
     const int64_t split_len = cdiv(cdiv(m, target), kvr::kChunk) * kvr::kChunk;
     const int64_t nsplit = cdiv(m, split_len);
     gp.nsplit = (int)nsplit;
@@ -154,11 +160,20 @@ BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bo
     int64_t part_len = 0;
     const int parts = kvr::xg_parts(R, K1, m, &part_len);
     bp.off_xgp = take(sizeof(double) * 2 * parts * R * K1);
+    // recompute-share bins: same IEEE sums as the device's deadlines
+    bp.r3_bins = 0;
+    for (int32_t a = 0; a < K1; ++a)
+        for (int32_t k = 0; k < K2; ++k)
+            if (std::isfinite((g.t1[a] + 0.0) + g.t2[k])) ++bp.r3_bins;
+    bp.r3_nsplit = kvr::r3_splits(R, m, &bp.r3_split_len);
+    bp.off_binT = take(sizeof(int32_t) * 2 * n);
+    bp.off_lb = take(sizeof(int32_t) * P);
+    bp.off_S = take(sizeof(uint64_t) * R * bp.r3_bins);
     bp.off_cand = bp.off_part = bp.off_cost = 0;
     if (bp.fused) {
         if (bootstrap) bp.off_cand = take(sizeof(kvr::ArgminCand) * gp.ngroups * 2 * L);
     } else {
-        bp.off_part = take(sizeof(double) * nsplit * R * gp.ntiles * (gp.LT + 1) * P);
+        bp.off_part = take(sizeof(double) * nsplit * R * gp.ntiles * gp.LT * P);
         if (bootstrap && !want_cost) bp.off_cost = take(sizeof(double) * R * L * P);
     }
     bp.total = off;
@@ -166,6 +181,18 @@ BrutePlan plan_brute(int64_t R, int64_t m, int32_t K1, int32_t K2, int32_t L, bo
 }
 
 template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>(static_cast<char *>(ws) + off); }
+
+kvr::R3Ws r3_view(void *ws, const BrutePlan &bp)
+{
+    kvr::R3Ws v{};
+    v.binT = at<int2>(ws, bp.off_binT);
+    v.lb = at<int32_t>(ws, bp.off_lb);
+    v.S = at<unsigned long long>(ws, bp.off_S);
+    v.nbins = bp.r3_bins;
+    v.nsplit = bp.r3_nsplit;
+    v.split_len = bp.r3_split_len;
+    return v;
+}
 
 int hip_ok(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_E_HIP; }
 
@@ -257,7 +284,7 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     size_t off_t1 = kStatusBytes, off_t2 = 0, off_a2 = 0, off_sort = 0;
     int32_t Lpad = g->n_lam;
     if (method == KVR_BRUTE) {
-        bp = plan_brute(1, n, g->n_t1, g->n_t2, g->n_lam, false, true);
+        bp = plan_brute(1, n, n, *g, false, true);
         need = bp.total;
     } else {
         off_t2 = off_t1 + align256(sizeof(double) * g->n_t1);
@@ -282,12 +309,15 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
         SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
         double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
         KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, at<double>(d_ws, bp.off_xgp), status, s));
+        const kvr::R3Ws r3 = r3_view(d_ws, bp);
+        KVR_TRY(kvr::launch_r3(src, 1, tb, r3, status, s));
         double *part = bp.fused ? nullptr : at<double>(d_ws, bp.off_part);
         KVR_MARK(g_prof_begin, s);
-        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, bp.fused ? d_cost : nullptr, nullptr,
-                                 part, status, s));
+        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, r3, bp.fused ? d_cost : nullptr,
+                                 nullptr, part, status, s));
         KVR_MARK(g_prof_end, s);
-        if (!bp.fused) KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, n, X, G, part, d_cost, s));
+        if (!bp.fused)
+            KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, n, X, G, r3, part, d_cost, s));
         return KVR_OK;
     }
     if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
@@ -326,7 +356,7 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     if (n_resamples > kMaxBatch / m) return KVR_E_SIZE;
     if (n_resamples * g->n_lam > INT32_MAX) return KVR_E_SIZE;
     const bool want_cost = d_cost != nullptr;
-    BrutePlan bp = plan_brute(n_resamples, m, g->n_t1, g->n_t2, g->n_lam, true, want_cost);
+    BrutePlan bp = plan_brute(n_resamples, n, m, *g, true, want_cost);
     if (d_ws == nullptr) {
         *ws_bytes = bp.total;
         return KVR_OK;
@@ -343,11 +373,13 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
     double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
     KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, at<double>(d_ws, bp.off_xgp), status, s));
+    const kvr::R3Ws r3 = r3_view(d_ws, bp);
+    KVR_TRY(kvr::launch_r3(src, n_resamples, tb, r3, status, s));
     const int64_t P = (int64_t)g->n_t1 * g->n_t2;
     if (bp.fused) {
         kvr::ArgminCand *cand = at<kvr::ArgminCand>(d_ws, bp.off_cand);
         KVR_MARK(g_prof_begin, s);
-        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, d_cost, cand, nullptr, status, s));
+        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, r3, d_cost, cand, nullptr, status, s));
         KVR_MARK(g_prof_end, s);
         KVR_TRY(kvr::launch_reduce_cands(cand, bp.gp, P, g->n_lam, d_best, d_best_cost, s));
         return KVR_OK;
@@ -355,9 +387,9 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     double *part = at<double>(d_ws, bp.off_part);
     double *cost = want_cost ? d_cost : at<double>(d_ws, bp.off_cost);
     KVR_MARK(g_prof_begin, s);
-    KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, nullptr, nullptr, part, status, s));
+    KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, r3, nullptr, nullptr, part, status, s));
     KVR_MARK(g_prof_end, s);
-    KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, m, X, G, part, cost, s));
+    KVR_TRY(kvr::launch_reduce_partials(bp.gp, tb, pr, m, X, G, r3, part, cost, s));
     KVR_TRY(kvr::launch_select(cost, n_resamples, g->n_lam, P, g->n_t2, 0, d_best, d_best_cost,
                                nullptr, s));
     return KVR_OK;

@@ -175,7 +175,7 @@ __global__ void __launch_bounds__(256) reduce_splits_kernel(int64_t nsplit, int6
 template <int LT>
 __global__ void __launch_bounds__(256) finalize_kernel(GridPlan plan, Tables tb, PriceDev pr,
                                                        double md, const double *__restrict__ X,
-                                                       const double *__restrict__ G,
+                                                       const double *__restrict__ G, R3Ws r3s,
                                                        const double *__restrict__ sums,
                                                        double *__restrict__ cost_out)
 {
@@ -186,8 +186,9 @@ __global__ void __launch_bounds__(256) finalize_kernel(GridPlan plan, Tables tb,
     const int tile = (int)((gid / P) % plan.ntiles);
     const int64_t r = gid / (P * plan.ntiles);
     const int a = (int)(f / tb.K2);
-    const int64_t base_row = (r * plan.ntiles + tile) * (LT + 1);
-    const double r3 = sums[(base_row + LT) * P + f];
+    const int64_t base_row = (r * plan.ntiles + tile) * LT;
+    const int32_t xb = r3s.lb[f];
+    const double r3 = (xb < r3s.nbins) ? (double)r3s.S[r * r3s.nbins + xb] : 0.0;
     const double base = pr.a1 * X[r * tb.K1 + a] + (pr.b2 * (G[r * tb.K1 + a] - r3) + pr.b3 * r3);
 #pragma unroll
     for (int l = 0; l < LT; ++l) {
@@ -197,11 +198,11 @@ __global__ void __launch_bounds__(256) finalize_kernel(GridPlan plan, Tables tb,
 }
 
 hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
-                                  int64_t m, const double *X, const double *G,
+                                  int64_t m, const double *X, const double *G, const R3Ws &r3,
                                   double *partials, double *cost_out, hipStream_t stream)
 {
     const int64_t P = (int64_t)tb.K1 * tb.K2;
-    const int64_t slice = plan.R * plan.ntiles * (int64_t)(plan.LT + 1) * P;
+    const int64_t slice = plan.R * plan.ntiles * (int64_t)plan.LT * P;
     hipLaunchKernelGGL(reduce_splits_kernel, dim3((unsigned)((slice + 255) / 256)), dim3(256), 0,
                        stream, (int64_t)plan.nsplit, slice, partials);
     hipError_t err = hipGetLastError();
@@ -210,10 +211,10 @@ hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const 
     const unsigned blocks = (unsigned)((threads + 255) / 256);
     const double md = (double)m;
     switch (plan.LT) {
-    case 4: hipLaunchKernelGGL(finalize_kernel<4>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
-    case 8: hipLaunchKernelGGL(finalize_kernel<8>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
-    case 16: hipLaunchKernelGGL(finalize_kernel<16>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
-    case 32: hipLaunchKernelGGL(finalize_kernel<32>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, partials, cost_out); break;
+    case 4: hipLaunchKernelGGL(finalize_kernel<4>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, r3, partials, cost_out); break;
+    case 8: hipLaunchKernelGGL(finalize_kernel<8>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, r3, partials, cost_out); break;
+    case 16: hipLaunchKernelGGL(finalize_kernel<16>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, r3, partials, cost_out); break;
+    case 32: hipLaunchKernelGGL(finalize_kernel<32>, dim3(blocks), dim3(256), 0, stream, plan, tb, pr, md, X, G, r3, partials, cost_out); break;
     default: return hipErrorInvalidValue;
     }
     return hipGetLastError();

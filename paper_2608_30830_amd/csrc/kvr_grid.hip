@@ -8,9 +8,10 @@
 // with X(t1) = sum T*min(w,t1), G(t1) = sum T*[w > t1], R3(e) = sum T*[w > e]
 // and h_i = T*(min(max(w,t1),e) - t1) >= 0 (zero when w <= t1).  The load
 // axis is evaluated in full: every (sample, policy, load) gets one fp64 FMA
-// acc[lambda] += a2(lambda) * h.  Terms that do not depend on the load are
-// computed once per (sample, policy); terms that depend only on t1 (X, G) once
-// per (sample, t1) by xg_kernel.
+// acc[lambda] += a2(lambda) * h, after h is formed once per (sample, policy).
+// The load-independent integer sums come from other kernels: X and G per
+// (sample, t1) from xg_kernel, R3 per (resample, deadline) from the deadline
+// bins of kvr_r3.hip; the epilogue combines them with the accumulators.
 //
 // Layout: one wave owns 64 consecutive policies (lane = one policy of one
 // resample) and one tile of up to 32 loads.  The samples are streamed through
@@ -40,10 +41,12 @@ namespace kvr {
 //                staged, one per resample, with half-size chunks.
 // Rounding note: min(fl(max(w,t1) - t1), fl(e - t1)) equals
 // fl(min(max(w,t1), e) - t1) because rounding is monotone.
+// Four resident waves per SIMD: the register budget is capped at 128 VGPRs
+// (the accumulators and loads of LT = 32 fit without spilling).
 template <int LT, int MODE>
-__global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, PriceDev pr,
+__global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4))) grid_kernel(SampleSrc src, Tables tb, PriceDev pr,
                                                      GridPlan plan, const double *__restrict__ X,
-                                                     const double *__restrict__ G,
+                                                     const double *__restrict__ G, R3Ws r3s,
                                                      double *__restrict__ cost_out,
                                                      ArgminCand *__restrict__ cand,
                                                      double *__restrict__ partials, int *status,
@@ -102,7 +105,6 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
         a2[l] = tb.a2[tile * LT + l];
         acc[l] = 0.0;
     }
-    double r3 = 0.0;
 
     const int64_t j0 = (int64_t)split * plan.split_len;
     int64_t j1 = j0 + plan.split_len;
@@ -155,8 +157,6 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
             if (kStaged) d = drow[2 * j];             // this lane's combination
             else d = fmax(s.x, t1) - t1;              // 0 when w <= t1
             const double h = s.y * fmin(d, ep);       // T * host seconds held
-            const double gone = (s.x > e) ? 1.0 : 0.0;   // discarded before resume
-            r3 = fma(gone, s.y, r3);
 #pragma unroll
             for (int l = 0; l < LT; ++l) acc[l] = fma(a2[l], h, acc[l]);
         }
@@ -168,6 +168,8 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
         const double md = (double)src.m;
         const double x = valid ? X[r * tb.K1 + a] : 0.0;
         const double g = valid ? G[r * tb.K1 + a] : 0.0;
+        const int32_t xb = r3s.lb[f];                 // recompute share of this deadline
+        const double r3 = (valid && xb < r3s.nbins) ? (double)r3s.S[r * r3s.nbins + xb] : 0.0;
         const double base = pr.a1 * x + (pr.b2 * (g - r3) + pr.b3 * r3);
 #pragma unroll
         for (int l = 0; l < LT; ++l) {
@@ -194,51 +196,51 @@ __global__ void __launch_bounds__(kWave) grid_kernel(SampleSrc src, Tables tb, P
             }
         }
     } else if (valid) {
-        const int64_t base_row = (((int64_t)split * plan.R + r) * plan.ntiles + tile) * (LT + 1);
+        const int64_t base_row = (((int64_t)split * plan.R + r) * plan.ntiles + tile) * LT;
 #pragma unroll
         for (int l = 0; l < LT; ++l) partials[(base_row + l) * P + f] = acc[l];
-        partials[(base_row + LT) * P + f] = r3;
     }
 }
 
 template <int LT, int MODE>
 static hipError_t launch_grid_m(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                                 const GridPlan &plan, const double *X, const double *G,
-                                double *cost_out, ArgminCand *cand, double *partials,
-                                int *status, hipStream_t stream)
+                                const R3Ws &r3, double *cost_out, ArgminCand *cand,
+                                double *partials, int *status, hipStream_t stream)
 {
     const int64_t nlogical = plan.ngroups * plan.nsplit * plan.ntiles;
     hipLaunchKernelGGL((grid_kernel<LT, MODE>), dim3((unsigned)nlogical), dim3(kWave), 0, stream,
-                       src, tb, pr, plan, X, G, cost_out, cand, partials, status, nlogical);
+                       src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, nlogical);
     return hipGetLastError();
 }
 
 template <int LT>
 static hipError_t launch_grid_t(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                                 const GridPlan &plan, const double *X, const double *G,
-                                double *cost_out, ArgminCand *cand, double *partials,
-                                int *status, hipStream_t stream)
+                                const R3Ws &r3, double *cost_out, ArgminCand *cand,
+                                double *partials, int *status, hipStream_t stream)
 {
     switch (plan.mode) {
     case kModePerLane:
-        return launch_grid_m<LT, kModePerLane>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModePerLane>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     case kModeRows1:
-        return launch_grid_m<LT, kModeRows1>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModeRows1>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     case kModeRows2:
-        return launch_grid_m<LT, kModeRows2>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModeRows2>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     default: return hipErrorInvalidValue;
     }
 }
 
 hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
-                       const GridPlan &plan, const double *X, const double *G, double *cost_out,
-                       ArgminCand *cand, double *partials, int *status, hipStream_t stream)
+                       const GridPlan &plan, const double *X, const double *G, const R3Ws &r3,
+                       double *cost_out, ArgminCand *cand, double *partials, int *status,
+                       hipStream_t stream)
 {
     switch (plan.LT) {
-    case 4: return launch_grid_t<4>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
-    case 8: return launch_grid_t<8>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
-    case 16: return launch_grid_t<16>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
-    case 32: return launch_grid_t<32>(src, tb, pr, plan, X, G, cost_out, cand, partials, status, stream);
+    case 4: return launch_grid_t<4>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+    case 8: return launch_grid_t<8>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+    case 16: return launch_grid_t<16>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+    case 32: return launch_grid_t<32>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -58,6 +58,18 @@ struct ArgminCand {
     int32_t pad;
 };
 
+// Recompute share R3 per (resample, deadline), counted through deadline bins
+// (kvr_r3.hip).  S[r][x] is R3 of every policy f with lb[f] == x; policies
+// with lb[f] >= nbins (infinite deadlines) have R3 = 0.
+struct R3Ws {
+    int2 *binT;               // [n] (deadline bin of the wait, clamped context size)
+    int32_t *lb;              // [K1*K2] grid deadlines strictly below each policy's
+    unsigned long long *S;    // [R][nbins] suffix sums of T over bins 1..nbins
+    int64_t nbins;            // F, the number of finite grid deadlines
+    int nsplit;               // draw splits per resample
+    int64_t split_len;
+};
+
 // ---- launches (all asynchronous on `stream`) --------------------------------
 hipError_t launch_clear_status(int *status, hipStream_t stream);
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
@@ -68,14 +80,18 @@ int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len);
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
                      double *xgp, int *status, hipStream_t stream);
 
+int r3_splits(int64_t R, int64_t m, int64_t *split_len);
+hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3Ws &ws,
+                     int *status, hipStream_t stream);
+
 hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
-                       const GridPlan &plan, const double *X, const double *G,
+                       const GridPlan &plan, const double *X, const double *G, const R3Ws &r3,
                        double *cost_out, ArgminCand *cand, double *partials, int *status,
                        hipStream_t stream);
 
 // Sums the split partials in place (split order) and writes mean costs.
 hipError_t launch_reduce_partials(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
-                                  int64_t m, const double *X, const double *G,
+                                  int64_t m, const double *X, const double *G, const R3Ws &r3,
                                   double *partials, double *cost_out, hipStream_t stream);
 
 hipError_t launch_reduce_cands(const ArgminCand *cand, const GridPlan &plan, int64_t P, int L,

@@ -1,0 +1,195 @@
+// Recompute share of the grid: R3(r, e) = sum over resample r of T * [w > e]
+// for every deadline e = fl(t1 + t2) of the policy grid (the b3 branch of
+// Eq. 1 under a one-shot host timer).  R3 does not depend on the load, and
+// it is an integer, so it is counted here once per (resample, deadline)
+// instead of being tested inside the grid kernel for every (sample, policy).
+//
+// Counting through deadline bins: let c(x) be the number of grid deadlines
+// strictly below x.  For a policy with deadline e_p and lb_p = c(e_p),
+// w > e_p holds exactly when c(w) > lb_p (every deadline below e_p is below
+// w, and so is e_p; conversely w <= e_p leaves no deadline below w that is
+// not below e_p).  So with hist[b] = sum of T over draws whose wait has
+// c(w) = b, R3(e_p) = sum_{b > lb_p} hist[b], a suffix sum.  Each t1 row of
+// deadlines is non-decreasing in t2 (t2 ascending, rounding monotone), so
+// c(x) is a sum of one binary search per row; no sort is needed.  A finite
+// wait has c(w) <= F, the number of finite deadlines, and bin 0 never enters
+// a suffix that is read (lb_p + 1 >= 1), so only bins 1..F are kept, stored
+// at b - 1: S[r][x] = R3 of any policy with lb_p = x, and R3 = 0 when
+// lb_p >= F (an infinite deadline).
+//
+// The sums are exact unsigned 64-bit integers: neither the atomics' order nor
+// the reduction tree can change them, and they equal the grid kernel's former
+// fp64 accumulation of the same integers bit for bit.
+#include "kvr_device.h"
+
+namespace kvr {
+
+constexpr int kR3Threads = 1024;
+constexpr int kR3BinsPerPass = 16384;  // 128 KiB of LDS counters per pass
+
+// Number of grid deadlines fl(t1[a] + t2[k]) strictly below x.
+__device__ int32_t deadlines_below(const Tables &tb, double x)
+{
+    int32_t c = 0;
+    for (int a = 0; a < tb.K1; ++a) {
+        const double t1 = tb.t1[a];
+        int lo = 0, hi = tb.K2;   // first k with t1 + t2[k] >= x
+        while (lo < hi) {
+            const int mid = (lo + hi) >> 1;
+            if (t1 + tb.t2[mid] < x) lo = mid + 1;
+            else hi = mid;
+        }
+        c += lo;
+    }
+    return c;
+}
+
+// Items 0..n-1: per base sample, its wait's bin and its (clamped) context
+// size, read as fetch_sample reads them (bad waits count as 0, contexts below
+// 1 as 1; the grid kernel flags both).  Items n..n+P-1: per policy f =
+// a*K2 + k, the number of grid deadlines strictly below its own.
+__global__ void __launch_bounds__(256) r3_bins_kernel(const double *__restrict__ w,
+                                                      const int32_t *__restrict__ T, int64_t n,
+                                                      Tables tb, int2 *__restrict__ binT,
+                                                      int32_t *__restrict__ lb)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    if (i < n) {
+        double x = w[i];
+        const uint64_t bits = (uint64_t)__double_as_longlong(x);
+        if (!(bits < 0x7ff0000000000000ull || bits == 0x8000000000000000ull)) x = 0.0;
+        int32_t t = T[i];
+        if (t < 1) t = 1;
+        binT[i] = make_int2(deadlines_below(tb, x + 0.0), t);
+    } else if (i - n < P) {
+        const int64_t f = i - n;
+        const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
+        lb[f] = deadlines_below(tb, tb.t1[a] + tb.t2[k]);
+    }
+}
+
+__global__ void __launch_bounds__(256) r3_zero_kernel(unsigned long long *__restrict__ p,
+                                                      int64_t count)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < count) p[i] = 0ull;
+}
+
+// One block per (resample, split of its draws): histogram of T over the
+// stored bins 1..nbins (index b - 1) in LDS, one pass per range of
+// kR3BinsPerPass bins.  A resample with one split owns its row of hist and
+// stores it; several splits add into a zeroed row.
+__global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
+    const int32_t *__restrict__ idx, int64_t n, int64_t m, const int2 *__restrict__ binT,
+    int64_t nbins, int nsplit, int64_t split_len, unsigned long long *__restrict__ hist,
+    int *status)
+{
+    __shared__ unsigned long long lh[kR3BinsPerPass];
+    const int64_t r = blockIdx.x / nsplit;
+    const int s = (int)(blockIdx.x % nsplit);
+    const int64_t j0 = (int64_t)s * split_len;
+    const int64_t j1 = (j0 + split_len < m) ? j0 + split_len : m;
+    unsigned long long *row = hist + r * nbins;
+    for (int64_t b0 = 0; b0 < nbins; b0 += kR3BinsPerPass) {
+        const int64_t nb = (nbins - b0 < kR3BinsPerPass) ? nbins - b0 : kR3BinsPerPass;
+        for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) lh[x] = 0ull;
+        __syncthreads();
+        for (int64_t j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
+            int64_t i = j;
+            if (idx != nullptr) {
+                int32_t ii = idx[r * m + j];
+                if (ii < 0 || (int64_t)ii >= n) {
+                    flag_domain(status);
+                    ii = 0;
+                }
+                i = ii;
+            }
+            const int2 bt = binT[i];
+            const int64_t b = (int64_t)bt.x - 1 - b0;   // bin 0 gives b < 0
+            if (b >= 0 && b < nb) atomicAdd(&lh[b], (unsigned long long)bt.y);
+        }
+        __syncthreads();
+        for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) {
+            const unsigned long long v = lh[x];
+            if (nsplit == 1) row[b0 + x] = v;
+            else if (v != 0ull) atomicAdd(&row[b0 + x], v);
+        }
+        __syncthreads();
+    }
+}
+
+// One block per resample: hist row -> suffix sums S[b] = sum_{b' >= b} hist[b'],
+// in place, chunk by chunk from the top bin down.
+__global__ void __launch_bounds__(kR3Threads) r3_suffix_kernel(unsigned long long *__restrict__ hist,
+                                                               int64_t nbins)
+{
+    __shared__ unsigned long long wsum[kR3Threads / kWave];
+    __shared__ unsigned long long carry_s;
+    unsigned long long *row = hist + (int64_t)blockIdx.x * nbins;
+    const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+    constexpr int nw = kR3Threads / kWave;
+    if (threadIdx.x == 0) carry_s = 0ull;
+    __syncthreads();
+    for (int64_t top = nbins; top > 0; top -= kR3Threads) {
+        // element handled by this thread: position top-1-tid (descending)
+        const int64_t pos = top - 1 - threadIdx.x;
+        unsigned long long v = (pos >= 0) ? row[pos] : 0ull;
+        // inclusive scan in descending-position order within the wave
+        for (int off = 1; off < kWave; off <<= 1) {
+            const unsigned long long o = __shfl_up(v, off, kWave);
+            if (lane >= off) v += o;
+        }
+        if (lane == kWave - 1) wsum[wv] = v;
+        __syncthreads();
+        unsigned long long before = carry_s;
+        for (int q = 0; q < wv; ++q) before += wsum[q];
+        v += before;
+        if (pos >= 0) row[pos] = v;
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            unsigned long long t = carry_s;
+            for (int q = 0; q < nw; ++q) t += wsum[q];
+            carry_s = t;
+        }
+        __syncthreads();
+    }
+}
+
+int r3_splits(int64_t R, int64_t m, int64_t *split_len)
+{
+    // enough blocks to cover the chip when there are few resamples, but never
+    // fewer than 4,096 draws per block
+    int64_t ns = (512 + R - 1) / R;
+    const int64_t cap = (m + 4095) / 4096;
+    if (ns > cap) ns = cap;
+    if (ns < 1) ns = 1;
+    *split_len = (m + ns - 1) / ns;
+    return (int)ns;
+}
+
+hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3Ws &ws,
+                     int *status, hipStream_t stream)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    hipLaunchKernelGGL(r3_bins_kernel, dim3((unsigned)((src.n + P + 255) / 256)), dim3(256), 0,
+                       stream, src.w, src.T, src.n, tb, ws.binT, ws.lb);
+    hipError_t err = hipGetLastError();
+    if (err != hipSuccess) return err;
+    if (ws.nbins == 0) return hipSuccess;   // every deadline infinite: R3 = 0
+    if (ws.nsplit > 1) {
+        const int64_t cnt = R * ws.nbins;
+        hipLaunchKernelGGL(r3_zero_kernel, dim3((unsigned)((cnt + 255) / 256)), dim3(256), 0,
+                           stream, ws.S, cnt);
+        if ((err = hipGetLastError()) != hipSuccess) return err;
+    }
+    hipLaunchKernelGGL(r3_hist_kernel, dim3((unsigned)(R * ws.nsplit)), dim3(kR3Threads), 0,
+                       stream, src.idx, src.n, src.m, ws.binT, ws.nbins, ws.nsplit,
+                       ws.split_len, ws.S, status);
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    hipLaunchKernelGGL(r3_suffix_kernel, dim3((unsigned)R), dim3(kR3Threads), 0, stream, ws.S,
+                       ws.nbins);
+    return hipGetLastError();
+}
+
+}  // namespace kvr

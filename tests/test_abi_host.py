@@ -99,9 +99,10 @@ def test_workspace_size_query(lib):
                            ctypes.byref(g4.c), None, None, None, None, ctypes.byref(sz), None)
     assert rc == kvr.KVR_OK
     # fused selection: two candidate slots per wave (257 waves per resample) x 32 loads,
-    # no cost tensor
+    # no cost tensor; recompute-share sums for the 64 x 256 finite deadlines per resample
     cands = 4096 * 257 * 2 * 32 * 16
-    assert cands <= sz.value < cands + (64 << 20)
+    r3 = 4096 * 64 * 256 * 8
+    assert cands + r3 <= sz.value < cands + r3 + (64 << 20)
     del wl
 
 
