@@ -265,7 +265,39 @@ def time_paths(kvr, workloads, torch):
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
+    res.update(time_platforms(kvr, workloads, torch))
     res.update(time_replay(kvr, workloads, torch))
+    return res
+
+
+def time_platforms(kvr, workloads, torch):
+    """The second workload: the three wait families as index rows, priced with
+    each Table 3 vector; one kvr_bootstrap call per platform."""
+    res = {}
+    wl = workloads.cross_platform_case()
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    w = torch.as_tensor(wl.wait_s).cuda()
+    T = torch.as_tensor(wl.ctx_tokens).cuda()
+    idx = torch.as_tensor(wl.idx).cuda()
+    for name, (a1, b2, b3) in workloads.PLATFORM_PRICES.items():
+        pr = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, 425.0, 1800.0)
+        pr.a1_per_token, pr.b2_per_token, pr.b3_per_token = a1, b2, b3
+        call = kvr.BootstrapCall(w, T, idx, pr, g)
+        call.launch()
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(7):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            call.launch()
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        ms = sorted(times)[len(times) // 2]
+        key = f"{wl.name}-{name}/bootstrap"
+        res[key] = {"ms": ms, "evaluations": wl.evaluations,
+                    "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
+        log(f"[bench] path {key}: {ms:.3f} ms")
     return res
 
 

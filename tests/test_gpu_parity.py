@@ -170,7 +170,10 @@ def test_weibull_1m_sorted_brute_and_sampled_oracle(kvr, oracle_mod):
 
 
 @pytest.mark.parametrize("case", [(201, 500, 2, 70, 5, 3, None), (202, 1300, 1, 65, 16, 4, 777),
-                                  (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None)])
+                                  (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None),
+                                  # few resamples, many draws: several recompute-share blocks
+                                  # per resample add into one row
+                                  (205, 5000, 2, 70, 6, 2, 20000)])
 def test_bootstrap_random(kvr, oracle_mod, case):
     seed, n, k1, k2, L, R, m = case
     wl = workloads.random_case(seed, n, k1, k2, L, resamples=R, m=m, ties=True)
@@ -363,6 +366,16 @@ DEGENERATE = {
     # one sample, one timer pair, one load
     "single": (np.array([123.0]), np.array([5], np.int32), np.array([0.0]), np.array([100.0]),
                np.array([0.7])),
+    # deadlines repeated across t1 rows (10+20 = 20+10 = ...), waits on them and one ulp above
+    "dup-deadlines": (np.concatenate([np.repeat([10.0, 20.0, 30.0, 40.0, 50.0], 40),
+                                      np.nextafter([10.0, 20.0, 30.0, 40.0, 50.0], np.inf),
+                                      np.geomspace(1.0, 90.0, 395)]),
+                      np.arange(1, 601, dtype=np.int32), np.array([0.0, 10.0, 20.0]),
+                      np.array([10.0, 20.0, 30.0, np.inf]), np.array([0.1, 0.5, 2.0])),
+    # t1 + t2 overflows to +inf for a finite t2: that deadline is never reached
+    "overflow": (np.concatenate([np.geomspace(1.0, 1e306, 300), [0.0, 1e300]]),
+                 np.full(302, 3, np.int32), np.array([0.0, 1e308]),
+                 np.array([1e300, 1e308, np.inf]), np.array([0.05, 0.2])),
     # many t1 rows, one host timer (group straddles rows every lane)
     "k2-one": (np.geomspace(0.5, 9000.0, 640), np.full(640, 33, np.int32),
                np.geomspace(0.1, 3000.0, 150), np.array([60.0]), np.array([0.4, 0.8])),

@@ -192,6 +192,31 @@ def family_waits(rng: np.random.Generator, family: str, n: int,
     raise KeyError(family)
 
 
+# Table 3 price vectors, per request of the Section 4 model (alpha_1 GPU-s/s,
+# beta_2 GPU-s, beta_3 GPU-s), with the host tier fixed at C2 = 425.
+PLATFORM_PRICES = {"h100-nvl": (0.0176, 0.02, 1.91),
+                   "a100-sxm": (0.0232, 0.02, 2.61),
+                   "l40s": (0.118, 0.02, 5.14)}
+
+
+def cross_platform_case(n: int = 65536, seed: int = 1005) -> Workload:
+    """The second workload: the three Section 4.1 wait families (mean 1,800 s)
+    side by side as one base sample of 3n waits, one context token each, with
+    one index row per family (row f selects samples f*n .. f*n + n - 1); 64
+    GPU-tier timers ({0} and 63 log-spaced 0.1 s - 1,000 s), 255 log-spaced
+    host timers 10 s - 24 h plus infinity, loads 0.5, 1, 2, 3 x lambda_crit.
+    It is priced with each PLATFORM_PRICES vector in turn."""
+    rw, _, _ = _streams(seed)
+    w = np.concatenate([family_waits(rw, f, n) for f in FAMILIES])
+    t = np.ones(3 * n, dtype=np.int32)
+    idx = np.arange(3 * n, dtype=np.int32).reshape(3, n)
+    lc = 425.0 / 1800.0
+    return Workload(f"platforms-3x{n // 1024}k", w, t,
+                    np.concatenate([[0.0], np.geomspace(0.1, 1000.0, 63)]),
+                    _with_inf(np.geomspace(10.0, 86400.0, 255)),
+                    np.array([0.5, 1.0, 2.0, 3.0]) * lc, 1.0, idx=idx)
+
+
 @dataclasses.dataclass
 class ReplayCase:
     family: str
