@@ -229,7 +229,8 @@ def time_paths(kvr, workloads, torch):
     cases = (("weibull-1m", kvr.KVR_BRUTE), ("weibull-1m", kvr.KVR_SORTED),
              ("mix-64k", kvr.KVR_BRUTE), ("mix-64k", kvr.KVR_SORTED),
              ("tiny-exp-1k", kvr.KVR_BRUTE), ("tiny-exp-1k", kvr.KVR_SORTED),
-             ("boot-1024x64k", None))
+             ("boot-1024x64k", None), ("boot-1024x64k", "factored"),
+             ("twotier-4096x64k", "factored"))
     for name, method in cases:
         wl = workloads.make(name)
         pf = wl.platform
@@ -239,10 +240,11 @@ def time_paths(kvr, workloads, torch):
         g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
-        if method is None:
-            call = kvr.BootstrapCall(w, T, torch.as_tensor(wl.idx).cuda(), pr, g)
+        if method is None or method == "factored":
+            call = kvr.BootstrapCall(w, T, torch.as_tensor(wl.idx).cuda(), pr, g,
+                                     factored=method == "factored")
             run = call.launch
-            key = f"{name}/bootstrap"
+            key = f"{name}/{'factored' if method else 'bootstrap'}"
         else:
             out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
                               device="cuda")

@@ -178,6 +178,24 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
 int kvr_workspace_status(const void *d_ws, void *hip_stream);
 
 /*
+ * Bootstrap calibration by the multiplicity-count closed form: a second
+ * method for the same result as kvr_bootstrap (Eq. 1 with Eq. 3 integrated
+ * over the sorted waits, the SORTED path's closed form, with the number of
+ * times each resample draws a base sample as its weight).  The base sample is
+ * sorted once; per resample the work is O(m + n + n_t1*n_t2*n_lam) instead of
+ * O(m*n_t1*n_t2*n_lam).  Arguments, outputs, layouts and errors are those of
+ * kvr_bootstrap, except n <= 2^31 - 2.  The prefix sums of T*w round
+ * differently from the brute force's per-sample sums, so costs agree with it
+ * within rounding (about 1e-12 relative on the bench workloads) and the
+ * selection is the same up to rounding-level near ties.
+ */
+int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                           const int32_t *d_idx, int64_t n_resamples, int64_t m,
+                           const kvr_prices *p, const kvr_policy_grid *g, int32_t *d_best,
+                           double *d_best_cost, double *d_cost, void *d_ws, size_t *ws_bytes,
+                           void *hip_stream);
+
+/*
  * Eq. 3 timer (host only): t2(lambda) = +inf if lambda <= lambda_crit =
  * C2/W_ref, else (beta_3 - beta_2) / alpha_2(lambda) with alpha_2(lambda) =
  * (lambda - lambda_crit) * beta_3 / C2.  With per-token prices both terms scale

@@ -29,10 +29,10 @@ KVR_SORTED = 1
 KVR_RETAIN = 0
 KVR_EXPIRE = 1
 
-EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy",
-           "kvr_bootstrap", "kvr_eq3_timer", "kvr_capacity_replay", "kvr_controller_select",
-           "kvr_crossover_statistic", "kvr_workspace_status", "kvr_set_profile_events",
-           "kvr_status_string")
+EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy", "kvr_bootstrap",
+           "kvr_bootstrap_factored", "kvr_eq3_timer", "kvr_capacity_replay",
+           "kvr_controller_select", "kvr_crossover_statistic", "kvr_workspace_status",
+           "kvr_set_profile_events", "kvr_status_string")
 
 
 class kvr_prices(ctypes.Structure):
@@ -87,6 +87,8 @@ def load_library(path: str = LIB_PATH):
     lib.kvr_bootstrap.argtypes = [P, P, I64, P, I64, I64, ctypes.POINTER(kvr_prices),
                                   ctypes.POINTER(kvr_policy_grid), P, P, P, P, SZ, P]
     lib.kvr_bootstrap.restype = ctypes.c_int
+    lib.kvr_bootstrap_factored.argtypes = lib.kvr_bootstrap.argtypes
+    lib.kvr_bootstrap_factored.restype = ctypes.c_int
     lib.kvr_workspace_status.argtypes = [P, P]
     lib.kvr_workspace_status.restype = ctypes.c_int
     lib.kvr_eq3_timer.argtypes = [ctypes.POINTER(kvr_prices), D, ctypes.POINTER(ctypes.c_double)]
@@ -217,11 +219,12 @@ def kvr_select_policy(cost, last_t2_is_inf: bool, stream=None) -> Tuple:
 
 
 class BootstrapCall:
-    """A prepared kvr_bootstrap call: outputs and workspace allocated once, so
-    that ``launch()`` only enqueues the library's kernels."""
+    """A prepared kvr_bootstrap call (or kvr_bootstrap_factored with
+    ``factored=True``): outputs and workspace allocated once, so that
+    ``launch()`` only enqueues the library's kernels."""
 
     def __init__(self, wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
-                 want_cost: bool = False):
+                 want_cost: bool = False, factored: bool = False):
         torch = _torch()
         _need(wait_s, torch.float64, "wait_s")
         _need(ctx_tokens, torch.int32, "ctx_tokens")
@@ -229,6 +232,8 @@ class BootstrapCall:
         if idx.dim() != 2:
             raise ValueError("idx must be [n_resamples, m]")
         self.lib = load_library()
+        self.name = "kvr_bootstrap_factored" if factored else "kvr_bootstrap"
+        self.fn = getattr(self.lib, self.name)
         self.wait_s, self.ctx, self.idx = wait_s, ctx_tokens, idx
         self.prices, self.grid = prices, grid
         self.n = wait_s.numel()
@@ -238,29 +243,28 @@ class BootstrapCall:
         self.cost = (torch.empty((self.R, grid.n_lam, grid.n_t1, grid.n_t2), dtype=torch.float64,
                                  device="cuda") if want_cost else None)
         need = ctypes.c_size_t(0)
-        _check(self.lib.kvr_bootstrap(None, None, self.n, None, self.R, self.m,
-                                      ctypes.byref(prices), ctypes.byref(grid.c), None, None,
-                                      _ptr(self.cost) if want_cost else None, None,
-                                      ctypes.byref(need), None), "kvr_bootstrap(size)")
+        _check(self.fn(None, None, self.n, None, self.R, self.m, ctypes.byref(prices),
+                       ctypes.byref(grid.c), None, None, _ptr(self.cost) if want_cost else None,
+                       None, ctypes.byref(need), None), f"{self.name}(size)")
         self.ws = _workspace(need.value)
         self.ws_bytes = ctypes.c_size_t(self.ws.numel())
 
     def launch(self, stream=None) -> None:
-        _check(self.lib.kvr_bootstrap(_ptr(self.wait_s), _ptr(self.ctx), self.n, _ptr(self.idx),
-                                      self.R, self.m, ctypes.byref(self.prices),
-                                      ctypes.byref(self.grid.c), _ptr(self.best),
-                                      _ptr(self.best_cost), _ptr(self.cost), _ptr(self.ws),
-                                      ctypes.byref(self.ws_bytes), _stream_ptr(stream)),
-               "kvr_bootstrap")
+        _check(self.fn(_ptr(self.wait_s), _ptr(self.ctx), self.n, _ptr(self.idx), self.R, self.m,
+                       ctypes.byref(self.prices), ctypes.byref(self.grid.c), _ptr(self.best),
+                       _ptr(self.best_cost), _ptr(self.cost), _ptr(self.ws),
+                       ctypes.byref(self.ws_bytes), _stream_ptr(stream)), self.name)
 
     def status(self, stream=None) -> int:
         return self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream))
 
 
 def kvr_bootstrap(wait_s, ctx_tokens, idx, prices: kvr_prices, grid: PolicyGrid,
-                  want_cost: bool = False, stream=None, check: bool = True):
-    """(best[R, n_lam], best_cost[R, n_lam]) and, with want_cost, cost[R, n_lam, n_t1, n_t2]."""
-    call = BootstrapCall(wait_s, ctx_tokens, idx, prices, grid, want_cost)
+                  want_cost: bool = False, stream=None, check: bool = True,
+                  factored: bool = False):
+    """(best[R, n_lam], best_cost[R, n_lam]) and, with want_cost, cost[R, n_lam, n_t1, n_t2];
+    ``factored=True`` calls kvr_bootstrap_factored."""
+    call = BootstrapCall(wait_s, ctx_tokens, idx, prices, grid, want_cost, factored)
     call.launch(stream)
     if check:
         _check(call.status(stream), "kvr_bootstrap(device)")

@@ -395,6 +395,68 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     return KVR_OK;
 }
 
+int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                           const int32_t *d_idx, int64_t n_resamples, int64_t m,
+                           const kvr_prices *p, const kvr_policy_grid *g, int32_t *d_best,
+                           double *d_best_cost, double *d_cost, void *d_ws, size_t *ws_bytes,
+                           void *hip_stream)
+{
+    if (!ws_bytes) return KVR_E_NULL;
+    int rc;
+    if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if ((rc = check_grid(g)) != KVR_OK) return rc;
+    if (n < 1 || n > INT32_MAX - 1 || n_resamples < 1 || m < 1 || m > INT32_MAX) return KVR_E_SIZE;
+    if (n_resamples > kMaxBatch / m) return KVR_E_SIZE;
+    if (n_resamples * g->n_lam > INT32_MAX) return KVR_E_SIZE;
+    const int64_t P = (int64_t)g->n_t1 * g->n_t2;
+    const int32_t Lpad = (int32_t)(cdiv(g->n_lam, 32) * 32);
+    const int64_t Rb = kvr::factored_batch(n, n_resamples);
+    size_t off = kStatusBytes;
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    const size_t off_t1 = take(sizeof(double) * g->n_t1);
+    const size_t off_t2 = take(sizeof(double) * g->n_t2);
+    const size_t off_a2 = take(sizeof(double) * Lpad);
+    const size_t off_sort = take(kvr::sort_ws_bytes(n));
+    const size_t off_rank = take(sizeof(int32_t) * 2 * n);
+    const size_t off_sw = take(sizeof(double) * n);
+    const size_t off_u1 = take(sizeof(int32_t) * g->n_t1);
+    const size_t off_ue = take(sizeof(int32_t) * P);
+    const size_t off_N = take(sizeof(uint64_t) * Rb * (n + 1));
+    const size_t off_S = take(sizeof(double) * Rb * (n + 1));
+    const size_t need = off;
+    if (d_ws == nullptr) {
+        *ws_bytes = need;
+        return KVR_OK;
+    }
+    if (!d_wait_s || !d_ctx_tokens || !d_idx || !d_best || !d_best_cost) return KVR_E_NULL;
+    if ((rc = check_workspace(d_ws, *ws_bytes, need)) != KVR_OK) return rc;
+
+    hipStream_t s = static_cast<hipStream_t>(hip_stream);
+    int *status = static_cast<int *>(d_ws);
+    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    Tables tb{};
+    if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
+    kvr::FactoredWs fw{};
+    kvr::sort_ws_carve(at<char>(d_ws, off_sort), n, fw.sort);
+    fw.rankT = at<int2>(d_ws, off_rank);
+    fw.sw = at<double>(d_ws, off_sw);
+    fw.u1 = at<int32_t>(d_ws, off_u1);
+    fw.ue = at<int32_t>(d_ws, off_ue);
+    fw.N = at<unsigned long long>(d_ws, off_N);
+    fw.S = at<double>(d_ws, off_S);
+    fw.Rb = Rb;
+    SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
+    KVR_MARK(g_prof_begin, s);
+    KVR_TRY(kvr::launch_factored(src, n_resamples, tb, pr, fw, d_best, d_best_cost, d_cost, status,
+                                 s));
+    KVR_MARK(g_prof_end, s);
+    return KVR_OK;
+}
+
 int kvr_eq3_timer(const kvr_prices *p, double lambda, double *t2_out)
 {
     if (!t2_out) return KVR_E_NULL;

@@ -380,9 +380,8 @@ __global__ void zero_u32_kernel(uint32_t *p, int64_t len)
     if (i < len) p[i] = 0;
 }
 
-hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, const Tables &tb,
-                              const PriceDev &pr, SortWs &ws, double *cost_out,
-                              int32_t *perm_out, int *status, hipStream_t stream)
+hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs &ws, int *cur_out,
+                            int *status, hipStream_t stream)
 {
     hipError_t err;
     hipLaunchKernelGGL(sort_prep_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, stream, w, T,
@@ -401,6 +400,17 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
         if ((err = hipGetLastError()) != hipSuccess) return err;
         cur ^= 1;
     }
+    *cur_out = cur;
+    return hipSuccess;
+}
+
+hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, const Tables &tb,
+                              const PriceDev &pr, SortWs &ws, double *cost_out,
+                              int32_t *perm_out, int *status, hipStream_t stream)
+{
+    int cur = 0;
+    hipError_t err = launch_sort_keys(w, T, n, ws, &cur, status, stream);
+    if (err != hipSuccess) return err;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
                        ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS);
     hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(64), 0, stream, ws.blkN, ws.blkS,

@@ -202,6 +202,39 @@ def test_bootstrap_and_select_errors(lib):
     assert lib.kvr_workspace_status(None, None) == kvr.KVR_E_NULL
 
 
+def test_factored_bootstrap_host_errors(lib):
+    """kvr_bootstrap_factored validates like kvr_bootstrap and sizes its own
+    workspace: sort buffers for n, bounded prefix rows per batch of resamples."""
+    g = kvr.PolicyGrid([0.0, 2.0], [5.0, math.inf], [0.1, 0.2, 0.3])
+    p = _prices()
+    sz = ctypes.c_size_t(0)
+
+    def boot(n=1000, R=2, m=1000, grid=g, prices=p, ws=None, best=FAKE):
+        return lib.kvr_bootstrap_factored(FAKE, FAKE, n, FAKE, R, m, ctypes.byref(prices),
+                                          ctypes.byref(grid.c), best, FAKE, None, ws,
+                                          ctypes.byref(sz), None)
+
+    assert boot(R=0) == kvr.KVR_E_SIZE
+    assert boot(m=0) == kvr.KVR_E_SIZE
+    assert boot(n=0) == kvr.KVR_E_SIZE
+    assert boot(n=(1 << 31) - 1) == kvr.KVR_E_SIZE
+    assert boot(R=1 << 30, m=1 << 11) == kvr.KVR_E_SIZE
+    bad = _prices()
+    bad.a1_per_token = -1.0
+    assert boot(prices=bad) == kvr.KVR_E_PRICE
+    assert boot(grid=kvr.PolicyGrid([0.0], [math.inf, 5.0], [0.1])) == kvr.KVR_E_GRID
+    assert boot() == kvr.KVR_OK
+    small = sz.value
+    assert small > 2 * 1001 * 16                      # two prefix rows of n + 1 entries
+    assert boot(R=100000, m=65536, n=65536) == kvr.KVR_OK
+    assert sz.value < (1 << 30) + (64 << 20)          # prefix rows are batched under 1 GiB
+    boot()
+    sz.value = 1
+    assert boot(ws=FAKE) == kvr.KVR_E_WORKSPACE
+    boot()
+    assert boot(ws=FAKE, best=None) == kvr.KVR_E_NULL
+
+
 def test_eq3_timer_matches_oracle(lib, oracle_mod):
     """The library's Eq. 3 timer and the oracle's agree bit for bit."""
     p = kvr.kvr_prices_from_platform(327680, 250e9, 50e9, 20000.0)

@@ -1,0 +1,115 @@
+"""GPU parity of the multiplicity-count closed form (kvr_bootstrap_factored):
+against the oracle's double loop on random bootstrap rows (costs within
+1e-9 relative), against the oracle's closed-form selection on every row of
+the bench bootstrap workloads, and against the brute-force kvr_bootstrap on
+the same rows (selection identical up to rounding-level near ties: where two
+picks differ, their best costs agree to rounding)."""
+import numpy as np
+import pytest
+
+import workloads
+from tests.test_gpu_parity import (RTOL, TIE_RTOL, _dev, _f64, _i32, _lib_prices, _np,
+                                   assert_costs, assert_selection)
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def kvr():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2608_30830_amd as k
+    k.load_library()
+    return k
+
+
+def _factored(kvr, wl, want_cost=False, prices=None):
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    return kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                             _dev(wl.idx, _i32()), prices or _lib_prices(kvr, wl), g,
+                             want_cost=want_cost, factored=True)
+
+
+@pytest.mark.parametrize("case", [(201, 500, 2, 70, 5, 3, None), (202, 1300, 1, 65, 16, 4, 777),
+                                  (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None),
+                                  (206, 40000, 1, 80, 40, 3, 30000)])
+def test_factored_random(kvr, oracle_mod, case):
+    seed, n, k1, k2, L, R, m = case
+    wl = workloads.random_case(seed, n, k1, k2, L, resamples=R, m=m, ties=True)
+    best, bc, cost = _factored(kvr, wl, want_cost=True)
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(R):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref, _np(best)[r], rb)
+        assert_costs(_np(bc)[r], rbc)
+    best2, bc2 = _factored(kvr, wl)
+    assert np.array_equal(_np(best2), _np(best))
+    assert np.array_equal(_np(bc2), _np(bc))
+
+
+def _rows_agree(got, got_cost, want, want_cost, label):
+    """Where two selections differ, the two picks' best costs must agree to
+    rounding (a near tie); returns how many selections differ."""
+    differ = np.argwhere(got != want)
+    for r, l in differ:
+        a, b = got_cost[r, l], want_cost[r, l]
+        assert abs(a - b) <= (TIE_RTOL + RTOL) * abs(b), (label, r, l, a, b)
+    print(f"[near-tie] {label}: {len(differ)} of {got.size} selections differ")
+    return len(differ)
+
+
+@pytest.mark.parametrize("name", ["boot-1024x64k", "twotier-4096x64k"])
+def test_factored_bench_workloads(kvr, oracle_mod, name):
+    wl = workloads.make(name)
+    fb, fbc = _factored(kvr, wl)
+    fb, fbc = _np(fb), _np(fbc)
+    pr = oracle_mod.workload_prices(wl)
+    cb, cbc = oracle_mod.closed_form_bootstrap(wl.wait_s, wl.ctx_tokens, wl.idx, pr, wl.t1,
+                                               wl.t2, wl.lam)
+    assert_costs(fbc, cbc)
+    _rows_agree(fb, fbc, cb, cbc, f"{name} factored vs oracle closed form")
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    bb, bbc = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                                _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g)
+    assert_costs(fbc, _np(bbc))
+    _rows_agree(fb, fbc, _np(bb), _np(bbc), f"{name} factored vs brute")
+    # sampled rows against the double loop, element by element
+    for r in (0, wl.n_resamples - 1):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref[None], fb[r][None], rb[None])
+        assert_costs(fbc[r], rbc)
+
+
+def test_factored_platforms(kvr, oracle_mod):
+    wl = workloads.cross_platform_case()
+    for name, (a1, b2, b3) in workloads.PLATFORM_PRICES.items():
+        p = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, 425.0, 1800.0)
+        p.a1_per_token, p.b2_per_token, p.b3_per_token = a1, b2, b3
+        best, bc, cost = _factored(kvr, wl, want_cost=True, prices=p)
+        pr = oracle_mod.Prices(a1, b2, b3)
+        for r in range(3):
+            ref = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                              idx_row=wl.idx[r])
+            assert_costs(_np(cost)[r], ref)
+            rb, _, _ = oracle_mod.select(ref, wl.t2)
+            assert_selection(ref, _np(best)[r], rb)
+
+
+def test_factored_domain_errors(kvr):
+    wl = workloads.random_case(207, 300, 1, 70, 4, resamples=2, m=300)
+    for what in ("idx", "nan"):
+        w, idx = wl.wait_s.copy(), wl.idx.copy()
+        if what == "idx":
+            idx[1, 5] = wl.n
+        else:
+            w[17] = np.nan
+        g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+        with pytest.raises(kvr.KvrError) as ei:
+            kvr.kvr_bootstrap(_dev(w, _f64()), _dev(wl.ctx_tokens, _i32()), _dev(idx, _i32()),
+                              _lib_prices(kvr, wl), g, factored=True)
+        assert ei.value.code == kvr.KVR_E_DOMAIN
