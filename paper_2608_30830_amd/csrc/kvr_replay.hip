@@ -11,12 +11,32 @@
 // cost per request is (b2*R + b3*(Ttot - R)) / n.
 //
 // GPU formulation (no heap): the departures of a replay come from two
-// monotone streams -- resumes, ordered by fl(arrival + wait) (one sort per
-// request sequence, shared by every timer), and expiries, which follow arrival
-// order because fl(arrival + t2) is monotone in the arrival.  One lane runs one
-// (sequence, timer) replay as a three-way merge of arrivals, resumes and
-// expiries, keeping an admitted bit per request; a departure frees a slot only
-// if its request was admitted and left by that stream.
+// monotone streams -- resumes, ordered by the key (fl(arrival + wait), index),
+// and expiries, which follow arrival order because fl(arrival + t2) is
+// monotone in the arrival.  The resume stream depends neither on the timer nor
+// on admissions, so one block per request sequence sorts it once and also
+// records, for every arrival j, the resume cursor rcur[j] = the number of
+// resume keys below (a_j, j): the resumes that have happened when request j
+// arrives (a request arriving later never resumes before j arrives, since its
+// key is at least (a_j, j)).  It also records the place of request i in the
+// resume order; the two travel packed in one 32-bit word per request.
+//
+// The expiry stream depends on the timer but not on admissions: a second
+// per-sequence pass records, for every timer and arrival j, how many earlier
+// requests have reached their timer by a_j (a binary search, the arrivals
+// being sorted) and whether j itself resumes before its timer.
+//
+// The merge runs one lane per (sequence, timer), 64 sequences with the same
+// timer per wave, and keeps two lane-private bitsets in LDS: rbits[p] for "the
+// request at resume place p was admitted and resumes before its timer", set at
+// its admission through its place, and ebits[i] for "request i was admitted
+// and is discarded at its timer".  At arrival j the departures that free slots
+// are the set bits of rbits between the previous and the current resume
+// cursor and of ebits between the previous and the current expiry cursor (two
+// popcounts).  The step loop reads only the packed per-arrival words, in
+// register buffers of eight arrivals filled one buffer ahead of use: no load
+// in it depends on another, so the walk is bound by LDS latency rather than
+// by chains of global loads.
 #include "kvr_device.h"
 
 namespace kvr {
@@ -31,15 +51,19 @@ __device__ __forceinline__ bool key_less(double ta, int ia, double tb, int ib)
     return ta < tb || (ta == tb && ia < ib);
 }
 
-// One block per request sequence: validate the row, then bitonic-sort
-// (fl(arrival + wait), index) in LDS and write the sorted times and indices.
+// One block per request sequence (n <= MAXN): validate the row, bitonic-sort
+// (fl(a + w), index) in LDS, then write pr[j] = place of request j in the
+// resume order (high 16 bits) | rcur[j] = number of keys below (a_j, j) (low
+// 16 bits).  Indices are 16-bit and the places reuse the key array once the
+// cursors are in registers: 10 bytes of LDS per request.
+template <int MAXN>
 __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
     const double *__restrict__ arrival, const double *__restrict__ wait,
-    const int32_t *__restrict__ ctx, int n, double *__restrict__ stime,
-    int32_t *__restrict__ sidx, int *status)
+    const int32_t *__restrict__ ctx, int n, uint32_t *__restrict__ pr, int *status)
 {
-    __shared__ double key[kReplayMaxN];
-    __shared__ int32_t idx[kReplayMaxN];
+    constexpr int kPer = (MAXN + kReplaySortThreads - 1) / kReplaySortThreads;
+    __shared__ double key[MAXN];
+    __shared__ uint16_t idx[MAXN];
     const int64_t row = blockIdx.x;
     const double *A = arrival + row * n;
     const double *W = wait + row * n;
@@ -57,10 +81,10 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
             if (ctx != nullptr && ctx[row * n + i] < 1) bad = true;
             if (bad) flag_domain(status);
             key[i] = a + w;
-            idx[i] = i;
-        } else {
+            idx[i] = (uint16_t)i;
+        } else {   // padding sorts last: +inf with indices above every request
             key[i] = INFINITY;
-            idx[i] = 0x7fffffff;
+            idx[i] = (uint16_t)i;
         }
     }
     __syncthreads();
@@ -75,7 +99,7 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
                         const double tk = key[i];
                         key[i] = key[j];
                         key[j] = tk;
-                        const int32_t ti = idx[i];
+                        const uint16_t ti = idx[i];
                         idx[i] = idx[j];
                         idx[j] = ti;
                     }
@@ -84,79 +108,236 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
             __syncthreads();
         }
     }
-    for (int i = threadIdx.x; i < n; i += blockDim.x) {
-        stime[row * n + i] = key[i];
-        sidx[row * n + i] = idx[i];
+    uint32_t rc[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int j = threadIdx.x + q * kReplaySortThreads;
+        rc[q] = 0u;
+        if (j < n) {
+            const double a = A[j];
+            int lo = 0, hi = n;   // first place whose key is not below (a, j)
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (key_less(key[mid], idx[mid], a, j)) lo = mid + 1;
+                else hi = mid;
+            }
+            rc[q] = (uint32_t)lo;
+        }
+    }
+    __syncthreads();
+    uint16_t *place = reinterpret_cast<uint16_t *>(key);   // keys are no longer needed
+    for (int p = threadIdx.x; p < n; p += blockDim.x) place[idx[p]] = (uint16_t)p;
+    __syncthreads();
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int j = threadIdx.x + q * kReplaySortThreads;
+        if (j < n) pr[row * n + j] = ((uint32_t)place[j] << 16) | rc[q];
     }
 }
 
-// One lane per (sequence, timer): the three-way merge.
-__global__ void __launch_bounds__(256) replay_merge_kernel(
-    const double *__restrict__ arrival, const double *__restrict__ wait,
-    const int32_t *__restrict__ ctx, int64_t reps, int n, const double *__restrict__ t2s, int K,
-    int64_t c2, const double *__restrict__ stime, const int32_t *__restrict__ sidx,
-    uint32_t *__restrict__ bits, double b2, double b3, double *__restrict__ cost,
-    int64_t *__restrict__ restored_out, int64_t *__restrict__ admitted_out)
-{
-    const int64_t sim = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (sim >= reps * K) return;
-    const int64_t row = sim / K;
-    const double t2 = t2s[sim % K];
-    const double *A = arrival + row * n;
-    const double *W = wait + row * n;
-    const int32_t *C = ctx ? ctx + row * n : nullptr;
-    const double *ST = stime + row * n;
-    const int32_t *SI = sidx + row * n;
-    const int nwords = (n + 31) / 32;
-    uint32_t *B = bits + sim * nwords;
+constexpr int kRing = 8;   // arrivals per register buffer in the merge
 
-    int64_t occ = 0, restored = 0, admitted = 0, total = 0;
-    int ir = 0, ie = 0;
-    uint32_t word = 0;   // admitted bits of requests 32*(j/32) .. j-1
-    auto was_admitted = [&](int i, int j) -> bool {
-        const uint32_t w32 = ((i >> 5) == (j >> 5)) ? word : B[i >> 5];
-        return (w32 >> (i & 31)) & 1u;
-    };
-    for (int j = 0; j < n; ++j) {
-        const double a = A[j];
-        // resumes at or before a (only requests that arrived before j)
-        while (ir < n) {
-            const int i = SI[ir];
-            if (i >= j || ST[ir] > a) break;
-            if (W[i] <= t2 && was_admitted(i, j)) --occ;
-            ++ir;
-        }
-        // expiries at or before a, in arrival order
-        while (ie < j) {
-            if (A[ie] + t2 > a) break;
-            if (W[ie] > t2 && was_admitted(ie, j)) --occ;
-            ++ie;
-        }
-        int32_t T = C ? C[j] : 1;
-        if (T < 1) T = 1;
-        total += T;
-        if (occ < c2) {
-            ++occ;
-            ++admitted;
-            word |= 1u << (j & 31);
-            if (W[j] <= t2) restored += T;
-        }
-        if ((j & 31) == 31 || j == n - 1) {
-            B[j >> 5] = word;
-            word = 0;
+// One block per request sequence (n <= MAXN): the arrivals into LDS, then for
+// every timer k and arrival j the packed word
+//   ec = min(j, #{i : fl(a_i + t2_k) <= a_j}) | [w_j <= t2_k] << 15,
+// laid out [timer][reps][n] for the kc timers t2s[0..kc): how many earlier
+// requests have reached their timer
+// when j arrives (a prefix, since fl(a_i + t2) is non-decreasing in i) and
+// whether j itself resumes before its timer.
+template <int MAXN>
+__global__ void __launch_bounds__(kReplaySortThreads) replay_expiry_kernel(
+    const double *__restrict__ arrival, const double *__restrict__ wait, int n,
+    const double *__restrict__ t2s, int kc, int64_t reps, uint16_t *__restrict__ ec)
+{
+    __shared__ double A[MAXN];
+    const int64_t row = blockIdx.x;
+    for (int i = threadIdx.x; i < n; i += blockDim.x) A[i] = arrival[row * n + i];
+    __syncthreads();
+    for (int k = 0; k < kc; ++k) {
+        const double t2 = t2s[k];
+        uint16_t *out = ec + ((int64_t)k * reps + row) * n;
+        for (int j = threadIdx.x; j < n; j += blockDim.x) {
+            const double a = A[j];
+            int lo = 0, hi = j;   // first i < j with fl(a_i + t2) > a
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (A[mid] + t2 <= a) lo = mid + 1;
+                else hi = mid;
+            }
+            const uint32_t stays = (wait[row * n + j] <= t2) ? 1u : 0u;
+            out[j] = (uint16_t)((uint32_t)lo | (stays << 15));
         }
     }
+}
+
+// Bits [lo, hi) of a word, 0 <= lo <= 32; zero when hi <= lo (lo = 32 only
+// happens then, so its masked shift never matters).
+__device__ __forceinline__ uint32_t bit_range(int lo, int hi)
+{
+    const uint32_t upto = (hi >= 32) ? 0xffffffffu : ((1u << (hi < 0 ? 0 : hi)) - 1u);
+    return (hi > lo) ? (upto & ~((1u << (lo & 31)) - 1u)) : 0u;
+}
+
+// Set bits of a lane's column in [from, to) beyond the first word (the rare
+// case of a range that crosses a word boundary).
+template <int NW>
+__device__ __forceinline__ int count_tail(const uint32_t (*bits)[kWave], int lane, int from, int to)
+{
+    int c = 0;
+    for (int b = ((from >> 5) + 1) << 5; b < to; b += 32) {
+        uint32_t x = bits[b >> 5][lane];
+        if (to - b < 32) x &= (1u << (to - b)) - 1u;
+        c += __popc(x);
+    }
+    return c;
+}
+
+// One lane per (sequence, timer k0 + k), k < kc; NW 32-bit words per bitset
+// bound n <= 32*NW.  Lanes past the last sequence walk the last one and write
+// nothing.  The step loop reads only the packed per-arrival words (and the
+// context sizes when CTX), kRing arrivals ahead, with no conditional loads.
+template <int NW, bool CTX>
+__global__ void __launch_bounds__(kWave) replay_merge_kernel(
+    const int32_t *__restrict__ ctx, int64_t reps, int n, int64_t c2,
+    const uint32_t *__restrict__ pr, const uint16_t *__restrict__ ec, double b2, double b3,
+    double *__restrict__ cost, int64_t *__restrict__ restored_out,
+    int64_t *__restrict__ admitted_out, int k0, int K)
+{
+    __shared__ uint32_t rbits[NW][kWave];
+    __shared__ uint32_t ebits[NW][kWave];
+    const int lane = threadIdx.x;
+    const int64_t groups = (reps + kWave - 1) / kWave;
+    const int k = (int)(blockIdx.x / groups);
+    const int64_t row = (blockIdx.x % groups) * kWave + lane;
+    const bool active = row < reps;
+    const int64_t rr = active ? row : reps - 1;
+    const int32_t *C = CTX ? ctx + rr * n : nullptr;
+    const uint32_t *PR = pr + rr * n;
+    const uint16_t *EC = ec + ((int64_t)k * reps + rr) * n;
+    const int nw = (n + 31) >> 5;
+    for (int q = 0; q < nw; ++q) {   // each lane clears only its own column
+        rbits[q][lane] = 0u;
+        ebits[q][lane] = 0u;
+    }
+
+    // Two buffers of kRing arrivals: one is processed while the other fills.
+    int32_t ta[kRing], tb[kRing];
+    uint32_t pa[kRing], pb[kRing], ea[kRing], eb[kRing];
+    auto fill = [&](int32_t (&t)[kRing], uint32_t (&pw)[kRing], uint32_t (&ew)[kRing], int j0) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) {
+            const int jj = (j0 + u < n) ? j0 + u : n - 1;
+            t[u] = CTX ? C[jj] : 1;
+            pw[u] = PR[jj];
+            ew[u] = EC[jj];
+        }
+    };
+
+    // occupancy is at most n, so C2 above n is the same as n + 1
+    const int cap = (c2 > (int64_t)n) ? n + 1 : (int)c2;
+    int occ = 0, admitted = 0;
+    int64_t restored = 0, total = 0;
+    int rdone = 0;   // resume places already applied
+    int edone = 0;   // requests (arrival order) whose timer has been applied
+    auto run = [&](const int32_t (&t)[kRing], const uint32_t (&pw)[kRing],
+                   const uint32_t (&ew)[kRing], int j0) {
+#pragma unroll
+        for (int u = 0; u < kRing; ++u) {
+            const int j = j0 + u;
+            if (j < n) {   // uniform across the wave
+                const int p = (int)(pw[u] >> 16), rc = (int)(pw[u] & 0xffffu);
+                const int ex = (int)(ew[u] & 0x7fffu);
+                const bool stays = (ew[u] >> 15) != 0u;
+                // departures at or before this arrival: set bits of rbits in
+                // [rdone, rc) (resumes) and of ebits in [edone, ex) (timers);
+                // the first word of each range is always read, so the common
+                // single-word case has no branch
+                const int rq = ((rdone < n) ? rdone : n - 1) >> 5;
+                const int eq = ((edone < n) ? edone : n - 1) >> 5;
+                const uint32_t rw0 = rbits[rq][lane], ew0 = ebits[eq][lane];
+                int gone = __popc(rw0 & bit_range(rdone - (rq << 5), rc - (rq << 5))) +
+                           __popc(ew0 & bit_range(edone - (eq << 5), ex - (eq << 5)));
+                if (rc > ((rq + 1) << 5) || ex > ((eq + 1) << 5))
+                    gone += count_tail<NW>(rbits, lane, rdone, rc) +
+                            count_tail<NW>(ebits, lane, edone, ex);
+                occ -= gone;
+                rdone = (rc > rdone) ? rc : rdone;
+                edone = (ex > edone) ? ex : edone;
+                const int32_t T = t[u] < 1 ? 1 : t[u];
+                total += T;
+                const bool in = occ < cap;
+                occ += in ? 1 : 0;
+                admitted += in ? 1 : 0;
+                restored += (in && stays) ? T : 0;
+                // admitted requests leave a bit: at their resume place if they
+                // resume in time, else at their arrival index (an OR of zero
+                // when not admitted)
+                uint32_t *word = stays ? &rbits[p >> 5][lane] : &ebits[j >> 5][lane];
+                const int bit = stays ? (p & 31) : (j & 31);
+                __hip_atomic_fetch_or(word, in ? (1u << bit) : 0u, __ATOMIC_RELAXED,
+                                      __HIP_MEMORY_SCOPE_WORKGROUP);
+            }
+        }
+    };
+    fill(ta, pa, ea, 0);
+    for (int jb = 0; jb < n; jb += 2 * kRing) {
+        fill(tb, pb, eb, jb + kRing);
+        run(ta, pa, ea, jb);
+        fill(ta, pa, ea, jb + 2 * kRing);
+        run(tb, pb, eb, jb + kRing);
+    }
+    if (!active) return;
+    const int64_t sim = row * K + k0 + k;
     cost[sim] = (b2 * (double)restored + b3 * (double)(total - restored)) / (double)n;
     if (restored_out) restored_out[sim] = restored;
     if (admitted_out) admitted_out[sim] = admitted;
 }
 
+// Timers per pass of the expiry and merge kernels: at most 1 GiB of packed
+// expiry words.
+static int replay_timer_chunk(int64_t reps, int64_t n, int K)
+{
+    int64_t kc = ((int64_t)1 << 30) / (2 * reps * n);
+    if (kc < 1) kc = 1;
+    return (int)(kc < K ? kc : K);
+}
+
 size_t replay_ws_bytes(int64_t reps, int64_t n, int K)
 {
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
-    const int64_t nwords = (n + 31) / 32;
-    return a256(sizeof(double) * reps * n) + a256(sizeof(int32_t) * reps * n) +
-           a256(sizeof(uint32_t) * reps * K * nwords) + a256(sizeof(double) * K);
+    const int kc = replay_timer_chunk(reps, n, K);
+    return a256(sizeof(uint32_t) * reps * n) + a256(sizeof(uint16_t) * kc * reps * n) +
+           a256(sizeof(double) * K);
+}
+
+template <int MAXN, int NW>
+static hipError_t launch_replay_n(const double *arrival, const double *wait, const int32_t *ctx,
+                                  int64_t reps, int n, const double *t2, int K, int64_t c2,
+                                  double b2, double b3, uint32_t *pr, uint16_t *ec, double *cost,
+                                  int64_t *restored, int64_t *admitted, int *status,
+                                  hipStream_t stream)
+{
+    hipLaunchKernelGGL(replay_sort_kernel<MAXN>, dim3((unsigned)reps), dim3(kReplaySortThreads), 0,
+                       stream, arrival, wait, ctx, n, pr, status);
+    const int kc = replay_timer_chunk(reps, n, K);
+    const int64_t groups = (reps + kWave - 1) / kWave;
+    for (int k0 = 0; k0 < K; k0 += kc) {
+        const int kn = (K - k0 < kc) ? K - k0 : kc;
+        hipLaunchKernelGGL(replay_expiry_kernel<MAXN>, dim3((unsigned)reps),
+                           dim3(kReplaySortThreads), 0, stream, arrival, wait, n, t2 + k0, kn, reps,
+                           ec);
+        if (ctx != nullptr)
+            hipLaunchKernelGGL((replay_merge_kernel<NW, true>), dim3((unsigned)(groups * kn)),
+                               dim3(kWave), 0, stream, ctx, reps, n, c2, pr, ec, b2, b3, cost,
+                               restored, admitted, k0, K);
+        else
+            hipLaunchKernelGGL((replay_merge_kernel<NW, false>), dim3((unsigned)(groups * kn)),
+                               dim3(kWave), 0, stream, ctx, reps, n, c2, pr, ec, b2, b3, cost,
+                               restored, admitted, k0, K);
+        hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+    }
+    return hipGetLastError();
 }
 
 hipError_t launch_replay(const double *arrival, const double *wait, const int32_t *ctx,
@@ -165,24 +346,24 @@ hipError_t launch_replay(const double *arrival, const double *wait, const int32_
                          int64_t *admitted, int *status, hipStream_t stream)
 {
     auto a256 = [](size_t x) { return (x + 255) & ~(size_t)255; };
+    const int kc = replay_timer_chunk(reps, n, K);
     char *p = static_cast<char *>(ws);
-    double *stime = reinterpret_cast<double *>(p);
-    p += a256(sizeof(double) * reps * n);
-    int32_t *sidx = reinterpret_cast<int32_t *>(p);
-    p += a256(sizeof(int32_t) * reps * n);
-    uint32_t *bits = reinterpret_cast<uint32_t *>(p);
-    p += a256(sizeof(uint32_t) * reps * K * ((n + 31) / 32));
+    uint32_t *pr = reinterpret_cast<uint32_t *>(p);
+    p += a256(sizeof(uint32_t) * reps * n);
+    uint16_t *ec = reinterpret_cast<uint16_t *>(p);
+    p += a256(sizeof(uint16_t) * kc * reps * n);
     double *t2 = reinterpret_cast<double *>(p);
     hipError_t err = launch_upload(t2, h_t2, K, stream);
     if (err != hipSuccess) return err;
-    hipLaunchKernelGGL(replay_sort_kernel, dim3((unsigned)reps), dim3(kReplaySortThreads), 0,
-                       stream, arrival, wait, ctx, (int)n, stime, sidx, status);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    const int64_t sims = reps * K;
-    hipLaunchKernelGGL(replay_merge_kernel, dim3((unsigned)((sims + 255) / 256)), dim3(256), 0,
-                       stream, arrival, wait, ctx, reps, (int)n, t2, K, c2, stime, sidx, bits, b2,
-                       b3, cost, restored, admitted);
-    return hipGetLastError();
+    const int ni = (int)n;
+    if (n <= 1024)
+        return launch_replay_n<1024, 32>(arrival, wait, ctx, reps, ni, t2, K, c2, b2, b3, pr, ec,
+                                         cost, restored, admitted, status, stream);
+    if (n <= 4096)
+        return launch_replay_n<4096, 128>(arrival, wait, ctx, reps, ni, t2, K, c2, b2, b3, pr, ec,
+                                          cost, restored, admitted, status, stream);
+    return launch_replay_n<kReplayMaxN, 256>(arrival, wait, ctx, reps, ni, t2, K, c2, b2, b3, pr,
+                                             ec, cost, restored, admitted, status, stream);
 }
 
 }  // namespace kvr
