@@ -51,86 +51,153 @@ __device__ __forceinline__ bool key_less(double ta, int ia, double tb, int ib)
     return ta < tb || (ta == tb && ia < ib);
 }
 
+// Keeps, of the pair (k, i) and (ok, oi), the smaller key under the total
+// order when keep_low, else the larger.
+__device__ __forceinline__ void keep_pair(double &k, int &i, double ok, int oi, bool keep_low)
+{
+    const bool mine_low = key_less(k, i, ok, oi);
+    if (mine_low != keep_low) {
+        k = ok;
+        i = oi;
+    }
+}
+
+// One compare-exchange stage of stride S < E among a thread's own elements
+// (global index t*E + r; ascending blocks of `size`).
+template <int E, int S>
+__device__ __forceinline__ void reg_stage(double (&k)[E], int (&id)[E], int t, int size)
+{
+    if constexpr (S < E) {
+#pragma unroll
+        for (int r = 0; r < E; ++r) {
+            const int q = r ^ S;
+            if (q > r) {
+                const bool asc = ((t * E + r) & size) == 0;
+                const double kr = k[r], kq = k[q];
+                const int ir = id[r], iq = id[q];
+                const bool swap = key_less(kq, iq, kr, ir) == asc;
+                k[r] = swap ? kq : kr;
+                id[r] = swap ? iq : ir;
+                k[q] = swap ? kr : kq;
+                id[q] = swap ? ir : iq;
+            }
+        }
+    }
+}
+
 // One block per request sequence (n <= MAXN): validate the row, bitonic-sort
-// (fl(a + w), index) in LDS, then write pr[j] = place of request j in the
-// resume order (high 16 bits) | rcur[j] = number of keys below (a_j, j) (low
-// 16 bits).  Indices are 16-bit and the places reuse the key array once the
-// cursors are in registers: 10 bytes of LDS per request.
+// (fl(a + w), index) padded to MAXN with +inf, then write pr[j] = place of
+// request j in the resume order (high 16 bits) | rcur[j] = number of keys
+// below (a_j, j) (low 16 bits).  Thread t holds elements t*E .. t*E + E - 1 in
+// registers: compare-exchange stages with stride < E stay in registers, those
+// with stride < 64*E pair lanes of one wave (shuffles), and only the wider
+// ones go through LDS with a block barrier.
 template <int MAXN>
 __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
     const double *__restrict__ arrival, const double *__restrict__ wait,
     const int32_t *__restrict__ ctx, int n, uint32_t *__restrict__ pr, int *status)
 {
+    constexpr int E = MAXN / kReplaySortThreads;
     constexpr int kPer = (MAXN + kReplaySortThreads - 1) / kReplaySortThreads;
+    static_assert(E >= 1 && E * kReplaySortThreads == MAXN, "MAXN must be a multiple of 512");
     __shared__ double key[MAXN];
     __shared__ uint16_t idx[MAXN];
     const int64_t row = blockIdx.x;
     const double *A = arrival + row * n;
     const double *W = wait + row * n;
-    int np2 = 1;
-    while (np2 < n) np2 <<= 1;
-    for (int i = threadIdx.x; i < np2; i += blockDim.x) {
-        if (i < n) {
-            const double a = A[i], w = W[i];
+    const int t = threadIdx.x;
+    double k[E];
+    int id[E];
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        const int e = t * E + r;
+        id[r] = e;
+        if (e < n) {
+            const double a = A[e], w = W[e];
             const uint64_t ba = (uint64_t)__double_as_longlong(a);
             const uint64_t bw = (uint64_t)__double_as_longlong(w);
             // finite and >= 0 (or -0.0), arrivals non-decreasing, contexts >= 1
             bool bad = !(ba < 0x7ff0000000000000ull || ba == 0x8000000000000000ull) ||
                        !(bw < 0x7ff0000000000000ull || bw == 0x8000000000000000ull);
-            if (i > 0 && !(A[i - 1] <= a)) bad = true;
-            if (ctx != nullptr && ctx[row * n + i] < 1) bad = true;
+            if (e > 0 && !(A[e - 1] <= a)) bad = true;
+            if (ctx != nullptr && ctx[row * n + e] < 1) bad = true;
             if (bad) flag_domain(status);
-            key[i] = a + w;
-            idx[i] = (uint16_t)i;
+            k[r] = a + w;
         } else {   // padding sorts last: +inf with indices above every request
-            key[i] = INFINITY;
-            idx[i] = (uint16_t)i;
+            k[r] = INFINITY;
         }
     }
-    __syncthreads();
-    for (int size = 2; size <= np2; size <<= 1) {
+    for (int size = 2; size <= MAXN; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
-            for (int i = threadIdx.x; i < np2; i += blockDim.x) {
-                const int j = i ^ stride;
-                if (j > i) {
-                    const bool up = (i & size) == 0;
-                    const bool gt = key_less(key[j], idx[j], key[i], idx[i]);
-                    if (gt == up) {
-                        const double tk = key[i];
-                        key[i] = key[j];
-                        key[j] = tk;
-                        const uint16_t ti = idx[i];
-                        idx[i] = idx[j];
-                        idx[j] = ti;
-                    }
+            if (stride < E) {
+                if (stride == 1) reg_stage<E, 1>(k, id, t, size);
+                else if (stride == 2) reg_stage<E, 2>(k, id, t, size);
+                else if (stride == 4) reg_stage<E, 4>(k, id, t, size);
+                else reg_stage<E, 8>(k, id, t, size);
+            } else if (stride < kWave * E) {
+                const int m = stride / E;   // partner lane offset
+#pragma unroll
+                for (int r = 0; r < E; ++r) {
+                    const int e = t * E + r;
+                    const double ok = __shfl_xor(k[r], m, kWave);
+                    const int oi = __shfl_xor(id[r], m, kWave);
+                    const bool lower = (e & stride) == 0, asc = (e & size) == 0;
+                    keep_pair(k[r], id[r], ok, oi, lower == asc);
                 }
+            } else {
+#pragma unroll
+                for (int r = 0; r < E; ++r) {
+                    key[t * E + r] = k[r];
+                    idx[t * E + r] = (uint16_t)id[r];
+                }
+                __syncthreads();
+#pragma unroll
+                for (int r = 0; r < E; ++r) {
+                    const int e = t * E + r;
+                    const double ok = key[e ^ stride];
+                    const int oi = idx[e ^ stride];
+                    const bool lower = (e & stride) == 0, asc = (e & size) == 0;
+                    keep_pair(k[r], id[r], ok, oi, lower == asc);
+                }
+                __syncthreads();
             }
-            __syncthreads();
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        key[t * E + r] = k[r];
+        idx[t * E + r] = (uint16_t)id[r];
+    }
+    __syncthreads();
+    // rcur: keys below (a_j, j), by a fixed-step search over all MAXN sorted
+    // keys (the +inf padding is never below a finite target); the kPer
+    // searches of a thread advance together, so their LDS reads overlap
+    double ta[kPer];
+    int pos[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int j = t + q * kReplaySortThreads;
+        ta[q] = (j < n) ? A[j] : 0.0;
+        pos[q] = 0;
+    }
+    for (int step = MAXN / 2; step > 0; step >>= 1) {
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int j = t + q * kReplaySortThreads;
+            const int m = pos[q] + step - 1;
+            if (key_less(key[m], idx[m], ta[q], j)) pos[q] += step;
         }
     }
     uint32_t rc[kPer];
 #pragma unroll
-    for (int q = 0; q < kPer; ++q) {
-        const int j = threadIdx.x + q * kReplaySortThreads;
-        rc[q] = 0u;
-        if (j < n) {
-            const double a = A[j];
-            int lo = 0, hi = n;   // first place whose key is not below (a, j)
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (key_less(key[mid], idx[mid], a, j)) lo = mid + 1;
-                else hi = mid;
-            }
-            rc[q] = (uint32_t)lo;
-        }
-    }
+    for (int q = 0; q < kPer; ++q) rc[q] = (uint32_t)pos[q];
     __syncthreads();
     uint16_t *place = reinterpret_cast<uint16_t *>(key);   // keys are no longer needed
-    for (int p = threadIdx.x; p < n; p += blockDim.x) place[idx[p]] = (uint16_t)p;
+    for (int p = t; p < n; p += blockDim.x) place[idx[p]] = (uint16_t)p;
     __syncthreads();
 #pragma unroll
     for (int q = 0; q < kPer; ++q) {
-        const int j = threadIdx.x + q * kReplaySortThreads;
+        const int j = t + q * kReplaySortThreads;
         if (j < n) pr[row * n + j] = ((uint32_t)place[j] << 16) | rc[q];
     }
 }
