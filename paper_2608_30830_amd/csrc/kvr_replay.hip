@@ -106,12 +106,8 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
     const double *A = arrival + row * n;
     const double *W = wait + row * n;
     const int t = threadIdx.x;
-    double k[E];
-    int id[E];
-#pragma unroll
-    for (int r = 0; r < E; ++r) {
-        const int e = t * E + r;
-        id[r] = e;
+    // coalesced loads and checks into LDS, then each thread takes E consecutive keys
+    for (int e = t; e < MAXN; e += blockDim.x) {
         if (e < n) {
             const double a = A[e], w = W[e];
             const uint64_t ba = (uint64_t)__double_as_longlong(a);
@@ -122,11 +118,20 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_sort_kernel(
             if (e > 0 && !(A[e - 1] <= a)) bad = true;
             if (ctx != nullptr && ctx[row * n + e] < 1) bad = true;
             if (bad) flag_domain(status);
-            k[r] = a + w;
+            key[e] = a + w;
         } else {   // padding sorts last: +inf with indices above every request
-            k[r] = INFINITY;
+            key[e] = INFINITY;
         }
     }
+    __syncthreads();
+    double k[E];
+    int id[E];
+#pragma unroll
+    for (int r = 0; r < E; ++r) {
+        id[r] = t * E + r;
+        k[r] = key[t * E + r];
+    }
+    __syncthreads();
     for (int size = 2; size <= MAXN; size <<= 1) {
         for (int stride = size >> 1; stride > 0; stride >>= 1) {
             if (stride < E) {
