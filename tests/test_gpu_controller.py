@@ -147,3 +147,30 @@ def test_controller_and_statistic_domain_errors(kvr):
         with pytest.raises(kvr.KvrError) as ei:
             kvr.kvr_crossover_statistic(_dev(w, torch.float64), _prices(kvr))
         assert ei.value.code == kvr.KVR_E_DOMAIN
+
+
+@pytest.mark.parametrize("family", workloads.FAMILIES)
+def test_table6_controller_column_end_to_end(kvr, family):
+    """Table 6's controller column on the GPU alone: the branch is frozen by
+    kvr_controller_select on a calibration sample at 2 lambda_crit; at every
+    load the held-out sequences (disjoint seed) are replayed by
+    kvr_capacity_replay under that branch (the Eq. 3 timer of the load, or
+    retain), and the mean cost lies within 3.5 standard deviations (of one
+    4,000-request sequence) + 0.03 of the printed cell."""
+    import torch
+    from tests.test_replay_pins import _table6
+    rows, _ = _table6()
+    cal = workloads.replay_case(family, 2 * LC, reps=64, seed=77)
+    out = _gpu(kvr, cal.arrival_s, cal.wait_s, 2 * LC, 425)
+    branch = "ttl" if out.branch == kvr.KVR_EXPIRE else "retain"
+    assert branch == rows[(family, 2.0)][1]
+    p = _prices(kvr)
+    for mult in (0.5, 1.0, 2.0, 3.0):
+        lam = mult * LC
+        t2 = kvr.kvr_eq3_timer(p, lam) if branch == "ttl" else math.inf
+        held = workloads.replay_case(family, lam, reps=100)
+        cost, _, _ = kvr.kvr_capacity_replay(_dev(held.arrival_s, torch.float64),
+                                             _dev(held.wait_s, torch.float64), p, [t2])
+        c = cost.cpu().numpy()[:, 0]
+        printed = rows[(family, mult)][0][0 if branch == "ttl" else 1]
+        assert abs(c.mean() - printed) <= 3.5 * c.std() + 0.03, (family, mult, c.mean(), printed)

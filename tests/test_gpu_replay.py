@@ -104,3 +104,15 @@ def test_replay_domain_errors(kvr):
             kvr.kvr_capacity_replay(_dev(arr, torch.float64), _dev(w, torch.float64),
                                     _prices(kvr), [600.0, math.inf])
         assert ei.value.code == kvr.KVR_E_DOMAIN
+
+
+def test_replay_many_timers_in_chunks(kvr, oracle_mod):
+    """40 timers on 2,048 sequences of 8,192 requests exceed what one pass of
+    the expiry words holds (1 GiB), so the timers run in two chunks; every
+    count still equals the oracle's."""
+    rc = workloads.replay_case("mixture", 3 * LC, reps=2048, n=8192, seed=91)
+    t2 = np.concatenate([np.geomspace(30.0, 86400.0, 39), [np.inf]])
+    cost, rest, adm = _run(kvr, rc.arrival_s, rc.wait_s, t2, 425)
+    oc, orr = oracle_mod.capacity_replay_batch(rc.arrival_s, rc.wait_s, 425, t2, 0.02, 1.91)
+    assert np.array_equal(rest, orr)
+    assert np.all(np.abs(cost - oc) <= 4 * np.spacing(oc))
