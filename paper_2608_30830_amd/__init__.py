@@ -319,8 +319,7 @@ class ControllerCall:
     """kvr_controller_select with its buffers allocated once: launch() only
     enqueues the library's kernels; result() copies the device struct back."""
 
-    def __init__(self, arrival_s, wait_s, prices: kvr_prices, lam: float, ctx_tokens=None,
-                 stream=None):
+    def __init__(self, arrival_s, wait_s, prices: kvr_prices, lam: float, ctx_tokens=None):
         torch = _torch()
         self.lib = load_library()
         _need(arrival_s, torch.float64, "arrival_s")
@@ -342,19 +341,19 @@ class ControllerCall:
         self.ws = _workspace(need.value)
         self.out = torch.empty(ctypes.sizeof(kvr_controller_out), dtype=torch.uint8,
                                device="cuda")
-        self.stream = _stream_ptr(stream)
 
-    def launch(self) -> None:
+    def launch(self, stream=None) -> None:
+        """Enqueue on ``stream`` (default: the current stream at this call)."""
         a, w, T = self.args
         have = ctypes.c_size_t(self.ws.numel())
         _check(self.lib.kvr_controller_select(_ptr(a), _ptr(w), _ptr(T), self.reps, self.n,
                                               ctypes.byref(self.prices), self.lam,
                                               _ptr(self.out), _ptr(self.ws), ctypes.byref(have),
-                                              self.stream),
+                                              _stream_ptr(stream)),
                "kvr_controller_select")
 
-    def result(self) -> kvr_controller_out:
-        _check(self.lib.kvr_workspace_status(_ptr(self.ws), self.stream),
+    def result(self, stream=None) -> kvr_controller_out:
+        _check(self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream)),
                "kvr_controller_select(device)")
         host = self.out.cpu()
         res = kvr_controller_out()
@@ -365,9 +364,9 @@ class ControllerCall:
 def kvr_controller_select(arrival_s, wait_s, prices: kvr_prices, lam: float, ctx_tokens=None,
                           stream=None) -> kvr_controller_out:
     """Section 3.4 controller on a calibration sample [n_reps, n]."""
-    call = ControllerCall(arrival_s, wait_s, prices, lam, ctx_tokens, stream)
-    call.launch()
-    return call.result()
+    call = ControllerCall(arrival_s, wait_s, prices, lam, ctx_tokens)
+    call.launch(stream)
+    return call.result(stream)
 
 
 def kvr_crossover_statistic(wait_s, prices: kvr_prices, stream=None, check: bool = True):
