@@ -2,6 +2,7 @@
 // of the load-dependent prices (Eq. 3), workspace planning and launches.
 // Built as a plain host translation unit (IEEE semantics for every check).
 #include "kvr.h"
+#include "kvr_factored.h"
 #include "kvr_internal.h"
 
 #include <algorithm>
@@ -421,7 +422,8 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     const size_t off_t2 = take(sizeof(double) * g->n_t2);
     const size_t off_a2 = take(sizeof(double) * Lpad);
     const size_t off_sort = take(kvr::sort_ws_bytes(n));
-    const size_t off_rank = take(sizeof(int32_t) * 2 * n);
+    const size_t off_rank = take(sizeof(int32_t) * n);
+    const size_t off_Ts = take(sizeof(int32_t) * n);
     const size_t off_sw = take(sizeof(double) * n);
     const size_t off_u1 = take(sizeof(int32_t) * g->n_t1);
     const size_t off_ue = take(sizeof(int32_t) * P);
@@ -442,7 +444,8 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
     kvr::FactoredWs fw{};
     kvr::sort_ws_carve(at<char>(d_ws, off_sort), n, fw.sort);
-    fw.rankT = at<int2>(d_ws, off_rank);
+    fw.rank = at<int32_t>(d_ws, off_rank);
+    fw.Ts = at<int32_t>(d_ws, off_Ts);
     fw.sw = at<double>(d_ws, off_sw);
     fw.u1 = at<int32_t>(d_ws, off_u1);
     fw.ue = at<int32_t>(d_ws, off_ue);

@@ -1,0 +1,25 @@
+// Internal declarations of the multiplicity-count closed form
+// (kvr_factored.hip); not part of the ABI.
+#pragma once
+
+#include "kvr_internal.h"
+
+namespace kvr {
+
+struct FactoredWs {
+    SortWs sort;              // radix sort of the base waits
+    int32_t *rank;            // [n] sorted position of each base sample
+    int32_t *Ts;              // [n] context size (clamped to >= 1) at each sorted position
+    double *sw;               // [n] sorted waits
+    int32_t *u1;              // [K1] sorted waits <= t1
+    int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2
+    unsigned long long *N;    // [Rb][n+1] multiplicities, then exclusive prefix of mult x T
+    double *S;                // [Rb][n+1] exclusive prefix of mult x T x w
+    int64_t Rb;               // resamples per batch
+};
+int64_t factored_batch(int64_t n, int64_t R);
+hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, const PriceDev &pr,
+                           FactoredWs &ws, int32_t *best, double *best_cost, double *cost_out,
+                           int *status, hipStream_t stream);
+
+}  // namespace kvr

@@ -17,34 +17,38 @@
 // agree within rounding and their selections up to rounding-level ties.
 //
 // Per batch of resamples: factored_hist_kernel (one block per resample,
-// LDS counters over ranges of sorted positions), factored_scan_kernel (one
-// block per resample, N and S in place), factored_policy_kernel (one block
-// per (resample, tile of 32 loads): every policy, fused arg-min).
+// 32-bit LDS counters of multiplicity over ranges of sorted positions),
+// factored_scan_kernel (one block per resample: weights c_i T_i and the N and
+// S prefix sums in place), factored_policy_kernel (one block per (resample,
+// tile of 32 loads): every policy, fused arg-min on the numerators m*C).
 #include "kvr_device.h"
+#include "kvr_factored.h"
 
 namespace kvr {
 
 constexpr int kFThreads = 1024;
-constexpr int kFRanksPerPass = 16384;   // 128 KiB of LDS counters per pass
+constexpr int kFRanksPerPass = 32768;   // 128 KiB of 32-bit LDS counters per pass
+constexpr int kFScanPer = 4;            // consecutive positions per thread in the scan
 constexpr int kFLoads = 32;             // loads per policy-kernel block
 constexpr int kFPolThreads = 256;
 
-// Per sorted position k: the sorted wait; per base sample: its sorted
-// position and its context size (below 1 counts as 1; sort_prep_kernel has
-// flagged it).
+// Per sorted position k: the sorted wait and the context size there (below
+// 1 counts as 1; sort_prep_kernel has flagged it); per base sample: its
+// sorted position.
 __global__ void __launch_bounds__(256) factored_rank_kernel(const uint64_t *__restrict__ skeys,
                                                             const int32_t *__restrict__ perm,
                                                             const int32_t *__restrict__ T, int64_t n,
                                                             double *__restrict__ sw,
-                                                            int2 *__restrict__ rankT)
+                                                            int32_t *__restrict__ Ts,
+                                                            int32_t *__restrict__ rank)
 {
     const int64_t k = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (k >= n) return;
     const int32_t i = perm[k];
     sw[k] = __longlong_as_double((long long)skeys[k]);
     int32_t t = T[i];
-    if (t < 1) t = 1;
-    rankT[i] = make_int2((int32_t)k, t);
+    Ts[k] = t < 1 ? 1 : t;
+    rank[i] = (int32_t)k;
 }
 
 // Number of sorted waits <= x.
@@ -76,19 +80,19 @@ __global__ void __launch_bounds__(256) factored_bounds_kernel(const double *__re
     }
 }
 
-// One block per resample of the batch: row[1 + k] = sum of T over the draws
-// whose base sample sits at sorted position k; row[0] = 0.
+// One block per resample of the batch: row[1 + k] = the number of its draws of
+// the base sample at sorted position k (exact: at most m < 2^31); row[0] = 0.
 __global__ void __launch_bounds__(kFThreads) factored_hist_kernel(
     const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
-    const int2 *__restrict__ rankT, unsigned long long *__restrict__ N, int *status)
+    const int32_t *__restrict__ rank, unsigned long long *__restrict__ N, int *status)
 {
-    __shared__ unsigned long long lh[kFRanksPerPass];
+    __shared__ uint32_t lh[kFRanksPerPass];
     const int64_t rb = blockIdx.x;
     const int64_t r = r0 + rb;
     unsigned long long *row = N + rb * (n + 1);
     for (int64_t k0 = 0; k0 < n; k0 += kFRanksPerPass) {
         const int64_t nk = (n - k0 < kFRanksPerPass) ? n - k0 : kFRanksPerPass;
-        for (int64_t x = threadIdx.x; x < nk; x += blockDim.x) lh[x] = 0ull;
+        for (int64_t x = threadIdx.x; x < nk; x += blockDim.x) lh[x] = 0u;
         __syncthreads();
         for (int64_t j = threadIdx.x; j < m; j += blockDim.x) {
             int32_t ii = idx[r * m + j];
@@ -96,9 +100,8 @@ __global__ void __launch_bounds__(kFThreads) factored_hist_kernel(
                 flag_domain(status);
                 ii = 0;
             }
-            const int2 rt = rankT[ii];
-            const int64_t kk = (int64_t)rt.x - k0;
-            if (kk >= 0 && kk < nk) atomicAdd(&lh[kk], (unsigned long long)rt.y);
+            const int64_t kk = (int64_t)rank[ii] - k0;
+            if (kk >= 0 && kk < nk) atomicAdd(&lh[kk], 1u);
         }
         __syncthreads();
         for (int64_t x = threadIdx.x; x < nk; x += blockDim.x) row[1 + k0 + x] = lh[x];
@@ -107,15 +110,19 @@ __global__ void __launch_bounds__(kFThreads) factored_hist_kernel(
     if (threadIdx.x == 0) row[0] = 0ull;
 }
 
-// One block per resample of the batch: inclusive prefix sums over positions
-// 1..n of the weights (N, exact) and of weight x sorted wait (S, fp64, a fixed
-// chunk-by-chunk order), in place.
+// One block per resample of the batch: weights c_k T_k (exact) and inclusive
+// prefix sums over positions 1..n of the weights (N) and of weight x sorted
+// wait (S, fp64), in place.  Each thread sums kFScanPer consecutive positions
+// in order, then the thread totals are scanned across the block: a fixed
+// order, so S is reproducible.
 __global__ void __launch_bounds__(kFThreads) factored_scan_kernel(unsigned long long *__restrict__ N,
                                                                   double *__restrict__ S,
                                                                   const double *__restrict__ sw,
+                                                                  const int32_t *__restrict__ Ts,
                                                                   int64_t n)
 {
     constexpr int nw = kFThreads / kWave;
+    constexpr int kTile = kFThreads * kFScanPer;
     __shared__ unsigned long long wn[nw];
     __shared__ double wsd[nw];
     __shared__ unsigned long long carry_n;
@@ -130,10 +137,24 @@ __global__ void __launch_bounds__(kFThreads) factored_scan_kernel(unsigned long 
         srow[0] = 0.0;
     }
     __syncthreads();
-    for (int64_t base = 0; base < n; base += kFThreads) {
-        const int64_t k = base + threadIdx.x;   // sorted position
-        unsigned long long c = (k < n) ? nrow[1 + k] : 0ull;
-        double s = (k < n) ? (double)c * sw[k] : 0.0;
+    for (int64_t base = 0; base < n; base += kTile) {
+        const int64_t k0 = base + (int64_t)threadIdx.x * kFScanPer;
+        unsigned long long cw[kFScanPer];
+        double sv[kFScanPer];
+        unsigned long long tn = 0ull;
+        double ts = 0.0;
+#pragma unroll
+        for (int q = 0; q < kFScanPer; ++q) {
+            const int64_t k = k0 + q;
+            const unsigned long long c = (k < n) ? nrow[1 + k] * (unsigned long long)Ts[k] : 0ull;
+            cw[q] = c;
+            sv[q] = (k < n) ? (double)c * sw[k] : 0.0;
+            tn += c;
+            ts += sv[q];
+        }
+        // inclusive scan of the thread totals within the wave, then across waves
+        unsigned long long c = tn;
+        double s = ts;
         for (int off = 1; off < kWave; off <<= 1) {
             const unsigned long long oc = __shfl_up(c, off, kWave);
             const double os = __shfl_up(s, off, kWave);
@@ -153,29 +174,39 @@ __global__ void __launch_bounds__(kFThreads) factored_scan_kernel(unsigned long 
             bn += wn[q];
             bs += wsd[q];
         }
-        if (k < n) {
-            nrow[1 + k] = bn + c;
-            srow[1 + k] = bs + s;
+        // this thread's exclusive offset, then its positions in order
+        bn += c - tn;
+        bs += s - ts;
+#pragma unroll
+        for (int q = 0; q < kFScanPer; ++q) {
+            const int64_t k = k0 + q;
+            bn += cw[q];
+            bs += sv[q];
+            if (k < n) {
+                nrow[1 + k] = bn;
+                srow[1 + k] = bs;
+            }
         }
         __syncthreads();
         if (threadIdx.x == 0) {
-            unsigned long long tn = carry_n;
-            double ts = carry_s;
+            unsigned long long t2 = carry_n;
+            double s2 = carry_s;
             for (int q = 0; q < nw; ++q) {
-                tn += wn[q];
-                ts += wsd[q];
+                t2 += wn[q];
+                s2 += wsd[q];
             }
-            carry_n = tn;
-            carry_s = ts;
+            carry_n = t2;
+            carry_s = s2;
         }
         __syncthreads();
     }
 }
 
 // One block per (resample of the batch, tile of kFLoads loads): every policy's
-// closed-form cost for the tile's loads, optional cost output, and the arg-min
-// per load under the library's total order (cost ascending, then larger flat
-// index).
+// closed-form total m*C for the tile's loads, the optional cost output, and
+// the arg-min per load under the library's total order (smaller first, then
+// larger flat index).  Dividing by m is monotone, so the arg-min compares the
+// totals and only the selected one is divided.
 __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
     const unsigned long long *__restrict__ N, const double *__restrict__ S, int64_t n, int64_t m,
     int64_t r0, int ntl, Tables tb, PriceDev pr, const int32_t *__restrict__ u1,
@@ -217,9 +248,9 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
 #pragma unroll
         for (int l = 0; l < kFLoads; ++l) {
             if (l < nl) {
-                const double c = (fixed + a2[l] * hold) / md;
-                if (cost_out != nullptr) cost_out[(r * tb.L + l0 + l) * P + f] = c;
-                argmin_merge(bc[l], bf[l], c, (int32_t)f);
+                const double tc = fixed + a2[l] * hold;
+                if (cost_out != nullptr) cost_out[(r * tb.L + l0 + l) * P + f] = tc / md;
+                argmin_merge(bc[l], bf[l], tc, (int32_t)f);
             }
         }
     }
@@ -239,7 +270,7 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
         int32_t f = rf[0][l];
         for (int q = 1; q < nw; ++q) argmin_merge(c, f, rc[q][l], rf[q][l]);
         best[r * tb.L + l0 + l] = f;
-        best_cost[r * tb.L + l0 + l] = c;
+        best_cost[r * tb.L + l0 + l] = c / md;
     }
 }
 
@@ -261,7 +292,8 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     hipError_t err = launch_sort_keys(src.w, src.T, n, ws.sort, &cur, status, stream);
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(factored_rank_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0,
-                       stream, ws.sort.keys[cur], ws.sort.vals[cur], src.T, n, ws.sw, ws.rankT);
+                       stream, ws.sort.keys[cur], ws.sort.vals[cur], src.T, n, ws.sw, ws.Ts,
+                       ws.rank);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     hipLaunchKernelGGL(factored_bounds_kernel, dim3((unsigned)((tb.K1 + P + 255) / 256)), dim3(256),
                        0, stream, ws.sw, n, tb, ws.u1, ws.ue);
@@ -270,9 +302,9 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     for (int64_t r0 = 0; r0 < R; r0 += ws.Rb) {
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
         hipLaunchKernelGGL(factored_hist_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
-                           src.idx, n, m, r0, ws.rankT, ws.N, status);
+                           src.idx, n, m, r0, ws.rank, ws.N, status);
         hipLaunchKernelGGL(factored_scan_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
-                           ws.N, ws.S, ws.sw, n);
+                           ws.N, ws.S, ws.sw, ws.Ts, n);
         hipLaunchKernelGGL(factored_policy_kernel, dim3((unsigned)(rb * ntl)), dim3(kFPolThreads), 0,
                            stream, ws.N, ws.S, n, m, r0, ntl, tb, pr, ws.u1, ws.ue, best, best_cost,
                            cost_out);

@@ -145,20 +145,4 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
                               const PriceDev &pr, SortWs &ws, double *cost_out,
                               int32_t *perm_out, int *status, hipStream_t stream);
 
-// Multiplicity-count closed form for bootstrap rows (kvr_factored.hip).
-struct FactoredWs {
-    SortWs sort;              // radix sort of the base waits
-    int2 *rankT;              // [n] (sorted position, clamped T) per base sample
-    double *sw;               // [n] sorted waits
-    int32_t *u1;              // [K1] sorted waits <= t1
-    int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2
-    unsigned long long *N;    // [Rb][n+1] exclusive prefix of multiplicity x T
-    double *S;                // [Rb][n+1] exclusive prefix of multiplicity x T x w
-    int64_t Rb;               // resamples per batch
-};
-int64_t factored_batch(int64_t n, int64_t R);
-hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, const PriceDev &pr,
-                           FactoredWs &ws, int32_t *best, double *best_cost, double *cost_out,
-                           int *status, hipStream_t stream);
-
 }  // namespace kvr
