@@ -120,6 +120,9 @@ def main() -> int:
                     help="bootstrap rows the CPU oracle evaluates for cpu_baseline")
     ap.add_argument("--paths", action="store_true",
                     help="also time the other entry points on their workloads")
+    ap.add_argument("--table", action="store_true",
+                    help="per-config table: GPU paths with their roofline fraction next to "
+                         "the CPU oracle on one thread and on all threads, then exit")
     ap.add_argument("--replay-only", action="store_true",
                     help="time only the admission replay and the controller, then exit")
     ap.add_argument("--replay-reps", type=int, default=8192)
@@ -138,6 +141,10 @@ def main() -> int:
 
     import paper_2608_30830_amd as kvr
     import workloads
+
+    if args.table:
+        print(json.dumps({"table": results_table(kvr, workloads, torch)}), flush=True)
+        return 0
 
     if args.replay_only:
         print(json.dumps({"paths": time_replay(kvr, workloads, torch, args.replay_reps)}),
@@ -385,6 +392,85 @@ def cpu_baseline(wl, rows: int):
             "kind": "oracle", "seconds": dt,
             "sample": f"{rows} of {wl.n_resamples} bootstrap rows, every policy and load "
                       f"({ev:.3e} evaluations)"}
+
+
+def _median_ms(torch, run, reps=5):
+    run()
+    torch.cuda.synchronize()
+    times = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        run()
+        b.record()
+        torch.cuda.synchronize()
+        times.append(a.elapsed_time(b))
+    return sorted(times)[len(times) // 2]
+
+
+def results_table(kvr, workloads, torch, cpu_evals=2.0e9):
+    """For each workload: whole-call GPU time of the brute-force path and of
+    the closed form (SORTED for one sample, factored for bootstrap rows), the
+    brute force's fraction of the fp64 peak (2 flop per evaluation), and the
+    CPU oracle's rate on one thread and on every thread over a bounded
+    sample (a prefix of the samples, or of one bootstrap row, holding about
+    ``cpu_evals`` evaluations)."""
+    import oracle
+    all_threads = oracle.num_threads()
+    rows = []
+    for name in workloads.NAMES:
+        wl = workloads.make(name)
+        pf = wl.platform
+        pr = kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
+                                          pf["host_link_bytes_per_s"],
+                                          pf["prefill_tokens_per_s"])
+        g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+        w = torch.as_tensor(wl.wait_s).cuda()
+        T = torch.as_tensor(wl.ctx_tokens).cuda()
+        reps = 3 if name.startswith("twotier") else 5
+        if wl.idx is None:
+            out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
+                              device="cuda")
+            brute = _median_ms(torch, lambda: kvr.kvr_cost_grid(w, T, pr, g, out=out,
+                                                                check=False), reps)
+            closed = _median_ms(torch, lambda: kvr.kvr_cost_grid(
+                w, T, pr, g, method=kvr.KVR_SORTED, out=out, check=False), reps)
+            closed_name = "sorted"
+        else:
+            idx = torch.as_tensor(wl.idx).cuda()
+            bc = kvr.BootstrapCall(w, T, idx, pr, g)
+            brute = _median_ms(torch, bc.launch, reps)
+            fc = kvr.BootstrapCall(w, T, idx, pr, g, factored=True)
+            closed = _median_ms(torch, fc.launch, reps)
+            closed_name = "factored"
+        evals = wl.evaluations
+        per_sample = wl.t1.size * wl.t2.size * wl.lam.size
+        m_cpu = int(max(1, min(wl.m, cpu_evals // per_sample)))
+        op = oracle.workload_prices(wl)
+        cpu = {}
+        for threads in (1, all_threads):
+            oracle.set_num_threads(threads)
+            t0 = time.perf_counter()
+            if wl.idx is None:
+                oracle.cost_grid(wl.wait_s[:m_cpu], wl.ctx_tokens[:m_cpu], op, wl.t1, wl.t2,
+                                 wl.lam)
+            else:
+                oracle.cost_grid(wl.wait_s, wl.ctx_tokens, op, wl.t1, wl.t2, wl.lam,
+                                 idx_row=wl.idx[0][:m_cpu])
+            cpu[threads] = m_cpu * per_sample / (time.perf_counter() - t0)
+        oracle.set_num_threads(all_threads)
+        row = {"workload": name, "evaluations": evals,
+               "gpu_brute_ms": brute, "gpu_brute_evals_per_s": evals / (brute * 1e-3),
+               "brute_fp64_frac": 2.0 * evals / (brute * 1e-3) / (FP64_PEAK_TFLOPS * 1e12),
+               f"gpu_{closed_name}_ms": closed,
+               "cpu_1_thread_evals_per_s": cpu[1],
+               "cpu_all_threads_evals_per_s": cpu[all_threads], "cpu_threads": all_threads,
+               "cpu_sample_evaluations": m_cpu * per_sample}
+        rows.append(row)
+        log(f"[bench] table {name}: brute {brute:.3f} ms ({row['brute_fp64_frac']:.3f} of fp64 "
+            f"peak), {closed_name} {closed:.3f} ms, oracle {cpu[1]:.3e} / {cpu[all_threads]:.3e} "
+            f"evaluations/s on 1 / {all_threads} threads")
+    return rows
 
 
 if __name__ == "__main__":

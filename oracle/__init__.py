@@ -54,6 +54,7 @@ def _configure(lib):
                                                  D, D, P, I32, P, I32, P, I32,
                                                  P, P]
     lib.oracle_num_threads.restype = ctypes.c_int
+    lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
     lib.oracle_capacity_replay.argtypes = [P, P, P, I64, I64, D, D, D, P, P]
     lib.oracle_capacity_replay.restype = D
     lib.oracle_capacity_replay_batch.argtypes = [P, P, P, I64, I64, I64, P, I32, D, D, P, P]
@@ -203,6 +204,11 @@ def closed_form_bootstrap(wait_s, ctx, idx, prices: Prices, t1, t2, lam):
 
 def num_threads() -> int:
     return int(_load().oracle_num_threads())
+
+
+def set_num_threads(n: int) -> None:
+    """Thread count of the oracle's later parallel loops (for timing it)."""
+    _load().oracle_set_num_threads(int(n))
 
 
 def capacity_replay(arrival_s, wait_s, c2, t2, b2, b3, ctx=None):

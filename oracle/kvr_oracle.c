@@ -312,6 +312,16 @@ int oracle_num_threads(void)
 #endif
 }
 
+/* Thread count of later parallel loops (timing of the oracle only). */
+void oracle_set_num_threads(int n)
+{
+#ifdef _OPENMP
+    if (n > 0) omp_set_num_threads(n);
+#else
+    (void)n;
+#endif
+}
+
 /*
  * Finite-capacity admission replay (Appendix D; the evaluation behind
  * Table 6).  Requests suspend at their arrival times (ascending) and resume
