@@ -163,3 +163,45 @@ def test_controller_sample_statistic_is_the_crossover_count(oracle_mod):
     out = oracle_mod.controller_select(rc.arrival_s, rc.wait_s, 425, 2 * LC, A1, B2, B3)
     assert out.n_short == oracle_mod.crossover_count(rc.wait_s, A1, B3)
     assert out.n_requests == 8000 and out.p_short == out.n_short / 8000
+
+
+def _meanfield_two_branch(oracle_mod, w, lam):
+    """The two branches of Section 3.4 priced by the mean-field cost of the
+    grid (Eq. 1 with the Eq. 3 congestion price, offload at suspension):
+    [cost of the Eq. 3 timer t2(lambda), cost of retain]."""
+    t2 = oracle_mod.eq3_timer(lam, B2, B3, 425.0, 1800.0)
+    pr = oracle_mod.Prices(A1, B2, B3)
+    T = np.ones(w.size, np.int32)
+    cost = oracle_mod.cost_grid(w, T, pr, np.array([0.0]), np.array([t2, np.inf]),
+                                np.array([lam]))
+    return cost[0, 0], t2
+
+
+def test_meanfield_two_branch_closed_form(oracle_mod):
+    """Exponential waits (mean mu): retain costs b2 + a2 mu and the timer
+    b2 + (b3 - b2) exp(-t2/mu) + a2 mu (1 - exp(-t2/mu)) with
+    a2 = (lambda - lambda_crit) b3 / C2; at 2 lambda_crit that is 1.9226
+    against 1.9300, so the mean-field comparison takes the timer."""
+    w = H.stratified_exponential(200000, 1800.0)
+    (c_ttl, c_ret), t2 = _meanfield_two_branch(oracle_mod, w, 2 * LC)
+    a2 = (2 * LC - LC) * B3 / 425.0
+    s = math.exp(-t2 / 1800.0)
+    assert abs(c_ret - (B2 + a2 * 1800.0)) < 2e-3
+    assert abs(c_ttl - (B2 + (B3 - B2) * s + a2 * 1800.0 * (1.0 - s))) < 2e-3
+    assert abs(c_ttl - 1.9226) < 2e-3 and abs(c_ret - 1.930) < 2e-3
+
+
+@pytest.mark.parametrize("family", workloads.FAMILIES)
+def test_meanfield_and_replay_controllers_disagree_above_lambda_crit(oracle_mod, family):
+    """At 2 lambda_crit the mean-field cost prefers the Eq. 3 timer for all
+    three families, while the finite-capacity replay (the paper's controller,
+    Table 6) keeps retain for lognormal and exponential waits: the congestion
+    price is a mean-field reading that the replay does not charge."""
+    (c_ttl, c_ret), _ = _meanfield_two_branch(oracle_mod, H.stratified_family(family, 100000),
+                                              2 * LC)
+    assert c_ttl < c_ret
+    rows, _ = _table6()
+    rc = workloads.replay_case(family, 2 * LC, reps=64, seed=77)
+    out = oracle_mod.controller_select(rc.arrival_s, rc.wait_s, 425, 2 * LC, A1, B2, B3)
+    assert ("ttl" if out.branch == 1 else "retain") == rows[(family, 2.0)][1]
+    assert (out.branch == 1) == (family == "mixture")

@@ -174,3 +174,28 @@ def test_table6_controller_column_end_to_end(kvr, family):
         c = cost.cpu().numpy()[:, 0]
         printed = rows[(family, mult)][0][0 if branch == "ttl" else 1]
         assert abs(c.mean() - printed) <= 3.5 * c.std() + 0.03, (family, mult, c.mean(), printed)
+
+
+@pytest.mark.parametrize("family", workloads.FAMILIES)
+def test_meanfield_two_branch_on_gpu(kvr, oracle_mod, family):
+    """Section 3.4's two branches priced by the mean-field grid on the GPU:
+    kvr_eq3_timer gives the load's timer, kvr_cost_grid prices [t2(lambda),
+    inf] at that load, kvr_select_policy picks the branch.  Costs equal the
+    oracle's within 1e-9; at 2 lambda_crit the timer wins for every family
+    (the replay controller keeps retain for two of them)."""
+    import torch
+    from tests import helpers as H
+    w = H.stratified_family(family, 100000)
+    T = np.ones(w.size, np.int32)
+    p = _prices(kvr)
+    lam = 2 * LC
+    t2 = kvr.kvr_eq3_timer(p, lam)
+    g = kvr.PolicyGrid([0.0], [t2, math.inf], [lam])
+    for method in (kvr.KVR_BRUTE, kvr.KVR_SORTED):
+        cost = kvr.kvr_cost_grid(_dev(w, torch.float64), _dev(T, torch.int32), p, g, method=method)
+        ref = oracle_mod.cost_grid(w, T, oracle_mod.Prices(A1, B2, B3), np.array([0.0]),
+                                   np.array([t2, np.inf]), np.array([lam]))
+        got = cost.cpu().numpy()
+        assert np.max(np.abs(got - ref) / ref) <= 1e-9
+        best, _, branch = kvr.kvr_select_policy(cost, g.last_inf)
+        assert int(best.cpu()[0]) == 0 and int(branch.cpu()[0]) == kvr.KVR_EXPIRE
