@@ -1,0 +1,68 @@
+"""A seeded sweep of grid shapes through every grid entry point against the
+oracle's double loop: the policy count below, at and off multiples of the
+64-lane groups, one to several load tiles (up to 40 loads), single samples
+and bootstrap rows of every length, sample splits and fused selection,
+duplicated waits and waits sitting on timers.  Costs within 1e-9 relative,
+selections identical up to rounding-level near ties."""
+import numpy as np
+import pytest
+
+import workloads
+from tests.test_gpu_parity import (_dev, _f64, _i32, _lib_prices, _np, assert_costs,
+                                   assert_selection)
+
+pytestmark = pytest.mark.gpu
+
+
+def _shape(i):
+    rng = np.random.Generator(np.random.PCG64(5000 + i))
+    k1 = int(rng.choice([1, 1, 2, 3, 5]))
+    k2 = int(rng.choice([2, 9, 33, 63, 64, 65, 127, 128, 200]))
+    L = int(rng.choice([1, 3, 4, 5, 8, 16, 17, 31, 32, 40]))
+    n = int(rng.choice([1, 7, 64, 129, 1000, 5000, 20000]))
+    R = int(rng.choice([0, 0, 1, 2, 3, 7]))
+    m = None if R == 0 else int(rng.choice([1, 100, n, 3000]))
+    return 6000 + i, n, k1, k2, L, R, m
+
+
+CASES = [_shape(i) for i in range(40)]
+
+
+@pytest.fixture(scope="module")
+def kvr():
+    import torch
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    import paper_2608_30830_amd as k
+    k.load_library()
+    return k
+
+
+@pytest.mark.parametrize("case", CASES, ids=[f"s{c[0]}-n{c[1]}-k{c[2]}x{c[3]}-L{c[4]}-R{c[5]}"
+                                             for c in CASES])
+def test_grid_shapes(kvr, oracle_mod, case):
+    seed, n, k1, k2, L, R, m = case
+    wl = workloads.random_case(seed, n, k1, k2, L, resamples=R, m=m, ties=True,
+                               inf_last=(seed % 3 != 0))
+    pr = oracle_mod.workload_prices(wl)
+    lp = _lib_prices(kvr, wl)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    if wl.idx is None:
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+        rb = oracle_mod.select(ref, wl.t2)[0]
+        for method in (kvr.KVR_BRUTE, kvr.KVR_SORTED):
+            cost = kvr.kvr_cost_grid(w, T, lp, g, method=method)
+            assert_costs(_np(cost), ref)
+            best = kvr.kvr_select_policy(cost, g.last_inf)[0]
+            assert_selection(ref, _np(best), rb)
+        return
+    idx = _dev(wl.idx, _i32())
+    for factored in (False, True):
+        best, bc, cost = kvr.kvr_bootstrap(w, T, idx, lp, g, want_cost=True, factored=factored)
+        for r in range(wl.n_resamples):
+            ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                       idx_row=wl.idx[r])
+            assert_costs(_np(cost)[r], ref)
+            rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+            assert_selection(ref, _np(best)[r], rb)
+            assert_costs(_np(bc)[r], rbc)
