@@ -337,7 +337,7 @@ int kvr_select_policy(const double *d_cost, int64_t batch, int32_t n_lam, int32_
     if (!d_cost || !d_best || !d_best_cost) return KVR_E_NULL;
     if (batch < 1 || n_lam < 1 || n_t1 < 1 || n_t2 < 1 || n_lam > kMaxLoads) return KVR_E_SIZE;
     if ((int64_t)n_t1 * n_t2 > kMaxPolicies) return KVR_E_SIZE;
-    if (batch * n_lam > INT32_MAX) return KVR_E_SIZE;
+    if (batch > INT32_MAX / n_lam) return KVR_E_SIZE;
     if (last_t2_is_inf != 0 && last_t2_is_inf != 1) return KVR_E_GRID;
     KVR_TRY(kvr::launch_select(d_cost, batch, n_lam, (int64_t)n_t1 * n_t2, n_t2, last_t2_is_inf,
                                d_best, d_best_cost, d_branch, static_cast<hipStream_t>(hip_stream)));

@@ -199,6 +199,9 @@ def test_bootstrap_and_select_errors(lib):
     assert sel(FAKE, 0, 1, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
     assert sel(FAKE, 1, 0, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
     assert sel(FAKE, 1, 1, 1, 2, 2, FAKE, FAKE, None, None) == kvr.KVR_E_GRID
+    # batch x n_lam beyond int32, including products that would overflow int64
+    assert sel(FAKE, 1 << 20, 4096, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
+    assert sel(FAKE, 1 << 62, 4096, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
     assert lib.kvr_workspace_status(None, None) == kvr.KVR_E_NULL
 
 
