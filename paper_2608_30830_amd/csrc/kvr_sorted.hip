@@ -151,7 +151,9 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
 
 // Stable ranking scatter of one digit pass.  The destination of a key is
 // (keys with a smaller digit) + (keys with its digit in earlier tiles, from
-// digit_scan_kernel) + (keys with its digit earlier in this tile).
+// digit_scan_kernel) + (keys with its digit earlier in this tile).  The tile
+// is first reordered by digit in LDS, then written out in that order, so
+// consecutive threads store consecutive addresses within each digit's run.
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int64_t n, int shift,
     const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
@@ -160,6 +162,9 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     __shared__ uint32_t wcnt[4][256];
     __shared__ uint32_t wofs[4][256];
     __shared__ uint32_t dbase[256];
+    __shared__ uint32_t tstart[256];                 // first tile position of each digit
+    __shared__ uint64_t lkey[kSortTile];
+    __shared__ int32_t lval[kSortTile];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
 #pragma unroll
     for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
@@ -203,18 +208,38 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
             wofs[q][d] = run;
             run += wcnt[q][d];
         }
+        uint32_t all;
+        tstart[d] = block_exclusive_scan(run, &all);   // run = this tile's count of digit d
     }
     __syncthreads();
+    // tile positions are dense: the valid keys of the tile fill [0, nvalid)
 #pragma unroll
     for (int j = 0; j < kSortKPT; ++j) {
         const int64_t i = base + j * kWave + lane;
         if (i < n) {
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+            const uint32_t pos = tstart[d] + wofs[wave][d] + local[j];
+            if (pos < (uint32_t)kSortTile) {           // always true; never write outside
+                lkey[pos] = key[j];
+                lval[pos] = val[j];
+            }
+        }
+    }
+    __syncthreads();
+    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t left = n - tile0;
+    const int nvalid = left < kSortTile ? (int)left : kSortTile;
+#pragma unroll
+    for (int q = 0; q < kSortKPT; ++q) {
+        const int pos = q * kSortThreads + (int)threadIdx.x;
+        if (pos < nvalid) {
+            const uint64_t k = lkey[pos];
+            const uint32_t d = (uint32_t)(k >> shift) & 255u;
             const int64_t dest = (int64_t)dbase[d] + offs[(int64_t)d * nblocks + blockIdx.x] +
-                                 wofs[wave][d] + local[j];
-            if (dest < n) {  // always true when the histograms agree; never write outside
-                keys_out[dest] = key[j];
-                vals_out[dest] = val[j];
+                                 (pos - (int64_t)tstart[d]);
+            if (dest >= 0 && dest < n) {  // always true when the histograms agree
+                keys_out[dest] = k;
+                vals_out[dest] = lval[pos];
             }
         }
     }
@@ -239,15 +264,21 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
             ss += (double)t * __longlong_as_double((long long)skeys[j]);
         }
     }
-    __shared__ int64_t rn[kScanThreads];
-    __shared__ double rs[kScanThreads];
-    rn[threadIdx.x] = sn;
-    rs[threadIdx.x] = ss;
+    // fixed-order tree: butterfly within each wave, then the four waves in order
+    sn = wave_sum(sn);
+    ss = wave_sum(ss);
+    __shared__ int64_t rn[kScanThreads / kWave];
+    __shared__ double rs[kScanThreads / kWave];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    if (lane == 0) {
+        rn[wave] = sn;
+        rs[wave] = ss;
+    }
     __syncthreads();
     if (threadIdx.x == 0) {
         int64_t a = 0;
         double b = 0.0;
-        for (int q = 0; q < kScanThreads; ++q) {
+        for (int q = 0; q < kScanThreads / kWave; ++q) {
             a += rn[q];
             b += rs[q];
         }
@@ -256,19 +287,54 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     }
 }
 
-// Exclusive scan of the tile sums, in tile order (one thread).
-__global__ void scan_blocks_kernel(int64_t *blkN, double *blkS, int nb)
+// Exclusive scan of the tile sums in place (one block of kScanThreads, in
+// rounds of kScanThreads tiles; a fixed order, so the result is reproducible).
+__global__ void __launch_bounds__(kScanThreads) scan_blocks_kernel(int64_t *blkN, double *blkS,
+                                                                   int nb)
 {
-    if (threadIdx.x != 0) return;
-    int64_t a = 0;
-    double b = 0.0;
-    for (int q = 0; q < nb; ++q) {
-        const int64_t x = blkN[q];
-        const double y = blkS[q];
-        blkN[q] = a;
-        blkS[q] = b;
-        a += x;
-        b += y;
+    __shared__ int64_t wn[kScanThreads / kWave];
+    __shared__ double wsm[kScanThreads / kWave];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    int64_t carryN = 0;
+    double carryS = 0.0;
+    for (int base = 0; base < nb; base += kScanThreads) {
+        const int i = base + (int)threadIdx.x;
+        int64_t xn = i < nb ? blkN[i] : 0;
+        double xs = i < nb ? blkS[i] : 0.0;
+        for (int off = 1; off < kWave; off <<= 1) {   // inclusive scan within the wave
+            const int64_t yn = __shfl_up(xn, off, kWave);
+            const double ys = __shfl_up(xs, off, kWave);
+            if (lane >= off) {
+                xn += yn;
+                xs += ys;
+            }
+        }
+        int64_t en = __shfl_up(xn, 1, kWave);            // exclusive within the wave
+        double es = __shfl_up(xs, 1, kWave);
+        if (lane == 0) {
+            en = 0;
+            es = 0.0;
+        }
+        if (lane == kWave - 1) {
+            wn[wave] = xn;
+            wsm[wave] = xs;
+        }
+        __syncthreads();
+        int64_t pn = carryN;
+        double ps = carryS;
+        for (int q = 0; q < wave; ++q) {
+            pn += wn[q];
+            ps += wsm[q];
+        }
+        if (i < nb) {
+            blkN[i] = pn + en;
+            blkS[i] = ps + es;
+        }
+        for (int q = 0; q < kScanThreads / kWave; ++q) {
+            carryN += wn[q];
+            carryS += wsm[q];
+        }
+        __syncthreads();
     }
 }
 
@@ -413,8 +479,8 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
     if (err != hipSuccess) return err;
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
                        ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS);
-    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(64), 0, stream, ws.blkN, ws.blkS,
-                       ws.nblocks_scan);
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(kScanThreads), 0, stream, ws.blkN,
+                       ws.blkS, ws.nblocks_scan);
     hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
                        ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
                        perm_out);
