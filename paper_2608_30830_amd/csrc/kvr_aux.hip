@@ -48,63 +48,107 @@ hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hip
 
 // ------------------------------------------------------------------- X, G --
 // X[r][a] = sum_j T*min(w, t1_a), G[r][a] = sum_j T*[w > t1_a] over the
-// samples of resample r.  One 256-thread block per (resample, tile of kAT
-// timers, sample part); threads stride over the part's samples, then a
-// fixed-order reduction.  With several parts the block writes a partial pair
-// to xgp[part][r][a][2] and xg_reduce_kernel adds the parts in part order.
-constexpr int kAT = 8;
+// samples of resample r.  One 256-thread block per (resample, group of ng
+// tiles of kAT timers, sample part), ng = 1, 2, 4 or 8 (the smallest that
+// covers the timers, at most 8): the block gathers each draw of its part
+// once, in chunks of 256 staged in LDS, and thread (q, u) = (t % ng, t / ng)
+// adds draws u, u + 256/ng, ... of every chunk for the kAT timers of tile q.
+// A fixed-order tree over u follows.  With several parts the block writes a
+// partial pair to xgp[part][r][a][2] and xg_reduce_kernel adds the parts in
+// part order.
+constexpr int kAT = 8;                  // timers per tile
+constexpr int kAGMax = 8;               // tiles per block at most
+constexpr int kXT = 256;                // threads per block = draws per chunk
 
-__global__ void __launch_bounds__(256) xg_kernel(SampleSrc src, Tables tb, int parts,
+static int xg_tiles_per_block(int K1)
+{
+    const int natiles = (K1 + kAT - 1) / kAT;
+    int ng = 1;
+    while (ng < natiles && ng < kAGMax) ng *= 2;
+    return ng;
+}
+
+__global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int ng, int parts,
                                                  int64_t part_len, double *X, double *G,
                                                  double *xgp, int *status)
 {
     const int natiles = (tb.K1 + kAT - 1) / kAT;
+    const int ngroups = (natiles + ng - 1) / ng;
+    const int nu = kXT / ng;                         // threads per tile
     const int part = (int)(blockIdx.x % parts);
     const int64_t rest = blockIdx.x / parts;
-    const int64_t r = rest / natiles;
-    const int a0 = (int)(rest % natiles) * kAT;
+    const int64_t r = rest / ngroups;
+    const int tile0 = (int)(rest % ngroups) * ng;
+    const int q = (int)threadIdx.x % ng, u = (int)threadIdx.x / ng;
+    const int a0 = (tile0 + q) * kAT;                // first timer of this thread's tile
     double t1v[kAT], xs[kAT], gs[kAT];
 #pragma unroll
-    for (int q = 0; q < kAT; ++q) {
-        t1v[q] = (a0 + q < tb.K1) ? tb.t1[a0 + q] : 0.0;
-        xs[q] = 0.0;
-        gs[q] = 0.0;
+    for (int k = 0; k < kAT; ++k) {
+        t1v[k] = (a0 + k < tb.K1) ? tb.t1[a0 + k] : 0.0;
+        xs[k] = 0.0;
+        gs[k] = 0.0;
     }
     const int64_t row_off = r * src.m;
     const int64_t j0 = (int64_t)part * part_len;
     const int64_t j1 = (j0 + part_len < src.m) ? j0 + part_len : src.m;
-    for (int64_t j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
-        Sample s = fetch_sample(src, row_off, j, status);
+    const int64_t nch = (j1 - j0 + kXT - 1) / kXT;
+
+    __shared__ double2 stage[2][kXT];
+    auto fetch = [&](int64_t c) {                  // this thread's draw of chunk c
+        const int64_t j = j0 + c * kXT + threadIdx.x;
+        if (j < j1) return fetch_sample(src, row_off, j, status);
+        Sample z;                                  // padding: adds exact zeros
+        z.w = 0.0;
+        z.T = 0.0;
+        return z;
+    };
+    Sample pre = nch > 0 ? fetch(0) : Sample{0.0, 0.0};
+    for (int64_t c = 0; c < nch; ++c) {
+        // buffer c & 1 was last read in chunk c - 2; every thread finished
+        // those reads before passing the barrier of chunk c - 1
+        const int b = (int)(c & 1);
+        stage[b][threadIdx.x] = make_double2(pre.w, pre.T);
+        __syncthreads();
+        if (c + 1 < nch) pre = fetch(c + 1);
+        for (int v = 0; v < ng; ++v) {
+            const double2 sm = stage[b][u + v * nu];
 #pragma unroll
-        for (int q = 0; q < kAT; ++q) {
-            xs[q] = fma(s.T, fmin(s.w, t1v[q]), xs[q]);
-            gs[q] += (s.w > t1v[q]) ? s.T : 0.0;
+            for (int k = 0; k < kAT; ++k) {
+                xs[k] = fma(sm.y, fmin(sm.x, t1v[k]), xs[k]);
+                gs[k] += (sm.x > t1v[k]) ? sm.y : 0.0;
+            }
         }
     }
-    __shared__ double red[4][2 * kAT];
-    const int wave = threadIdx.x / kWave, lane = threadIdx.x % kWave;
+
+    // fixed-order tree over the nu threads of each tile
+    __shared__ double red[kXT][2 * kAT];
 #pragma unroll
-    for (int q = 0; q < kAT; ++q) {
-        double x = wave_sum(xs[q]);
-        double g = wave_sum(gs[q]);
-        if (lane == 0) {
-            red[wave][q] = x;
-            red[wave][kAT + q] = g;
-        }
+    for (int k = 0; k < kAT; ++k) {
+        red[threadIdx.x][k] = xs[k];
+        red[threadIdx.x][kAT + k] = gs[k];
     }
     __syncthreads();
-    if (threadIdx.x < kAT && a0 + (int)threadIdx.x < tb.K1) {
-        const int q = threadIdx.x;
-        double x = ((red[0][q] + red[1][q]) + red[2][q]) + red[3][q];
-        double g = ((red[0][kAT + q] + red[1][kAT + q]) + red[2][kAT + q]) + red[3][kAT + q];
-        const int64_t ra = r * tb.K1 + a0 + q;
-        if (parts == 1) {
-            X[ra] = x;
-            G[ra] = g;
-        } else {
-            const int64_t R = (int64_t)gridDim.x / parts / natiles;
-            xgp[2 * ((int64_t)part * R * tb.K1 + ra)] = x;
-            xgp[2 * ((int64_t)part * R * tb.K1 + ra) + 1] = g;
+    for (int stride = nu / 2; stride > 0; stride /= 2) {
+        if (u < stride) {
+#pragma unroll
+            for (int k = 0; k < 2 * kAT; ++k) red[threadIdx.x][k] += red[threadIdx.x + stride * ng][k];
+        }
+        __syncthreads();
+    }
+    if (threadIdx.x < ng * 2 * kAT) {
+        const int tq = (int)threadIdx.x / (2 * kAT), v = (int)threadIdx.x % (2 * kAT);
+        const double acc = red[tq][v];               // row u = 0 of tile tq
+        const int a = (tile0 + tq) * kAT + (v % kAT);
+        if (a < tb.K1) {
+            const bool isx = v < kAT;
+            const int64_t ra = r * tb.K1 + a;
+            if (parts == 1) {
+                if (isx) X[ra] = acc;
+                else G[ra] = acc;
+            } else {
+                const int64_t R = (int64_t)gridDim.x / parts / ngroups;
+                xgp[2 * ((int64_t)part * R * tb.K1 + ra) + (isx ? 0 : 1)] = acc;
+            }
         }
     }
 }
@@ -128,10 +172,11 @@ __global__ void __launch_bounds__(256) xg_reduce_kernel(int parts, int64_t RK1,
 
 int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len)
 {
-    const int64_t natiles = (K1 + kAT - 1) / kAT;
+    const int ng = xg_tiles_per_block(K1);
+    const int64_t ngroups = ((K1 + kAT - 1) / kAT + ng - 1) / ng;
     int64_t parts = 1;
-    if (R * natiles < 1024) {
-        parts = (1024 + R * natiles - 1) / (R * natiles);
+    if (R * ngroups < 1024) {
+        parts = (1024 + R * ngroups - 1) / (R * ngroups);
         const int64_t most = (m + 4095) / 4096;  // at least 4,096 samples per part
         if (parts > most) parts = most;
         if (parts < 1) parts = 1;
@@ -143,11 +188,12 @@ int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len)
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
                      double *xgp, int *status, hipStream_t stream)
 {
-    const int natiles = (tb.K1 + kAT - 1) / kAT;
+    const int ng = xg_tiles_per_block(tb.K1);
+    const int ngroups = ((tb.K1 + kAT - 1) / kAT + ng - 1) / ng;
     int64_t part_len = 0;
     const int parts = xg_parts(R, tb.K1, src.m, &part_len);
-    hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * natiles * parts)), dim3(256), 0, stream, src,
-                       tb, parts, part_len, X, G, xgp, status);
+    hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * ngroups * parts)), dim3(kXT), 0, stream, src,
+                       tb, ng, parts, part_len, X, G, xgp, status);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || parts == 1) return err;
     const int64_t RK1 = R * tb.K1;

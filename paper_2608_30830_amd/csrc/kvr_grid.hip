@@ -56,8 +56,10 @@ __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
     constexpr bool kTwo = MODE == kModeRows2;
     constexpr int kCh = kTwo ? kChunk / 2 : kChunk;   // samples per staged chunk
     constexpr int kPer = kCh / kWave;                  // samples each lane stages per stream
-    __shared__ double2 wt[2][kTwo ? 2 : 1][kCh];        // (w, T) per stream
-    __shared__ double2 dd[2][kStaged ? kCh : 1];        // (d for combination A, for B)
+    // per-lane d: (w, T) of each sample; staged d: (T, d) of each sample for
+    // combination A and for B, so a lane reads one 16-byte record per sample
+    __shared__ double2 wt[2][kStaged ? 1 : kCh];
+    __shared__ double2 td[2][kStaged ? kCh : 1][2];
 
     const int64_t logical = xcd_logical_block(blockIdx.x, nlogical);
     const int tile = (int)(logical % plan.ntiles);
@@ -95,8 +97,9 @@ __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
     const int64_t rA = FA / P, rB = FB / P;
     const int aA = (int)((FA % P) / tb.K2), aB = (int)((FB % P) / tb.K2);
     const double t1A = tb.t1[aA], t1B = tb.t1[aB];
-    const int sel = (r == rA && a == aA) ? 0 : 1;      // which staged d
-    const int stream = (kTwo && r != rA) ? 1 : 0;      // which staged (w, T)
+    // which staged combination; when the group straddles two resamples the
+    // combinations are (rA, last t1 row) and (rB, first row), one per stream
+    const int sel = (r == rA && a == aA) ? 0 : 1;
     const bool twoStreams = kTwo && rB != rA;
 
     double a2[LT], acc[LT];
@@ -133,10 +136,12 @@ __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
 #pragma unroll
         for (int q = 0; q < kPer; ++q) {
             const int s = q * kWave + lane;
-            wt[b][0][s] = make_double2(preA[q].w, preA[q].T);
-            if (kTwo) wt[b][kTwo ? 1 : 0][s] = make_double2(preB[q].w, preB[q].T);
-            if (kStaged)
-                dd[b][s] = make_double2(fmax(preA[q].w, t1A) - t1A, fmax(preB[q].w, t1B) - t1B);
+            if (kStaged) {
+                td[b][s][0] = make_double2(preA[q].T, fmax(preA[q].w, t1A) - t1A);
+                td[b][s][1] = make_double2(preB[q].T, fmax(preB[q].w, t1B) - t1B);
+            } else {
+                wt[b][s] = make_double2(preA[q].w, preA[q].T);
+            }
         }
     };
 
@@ -148,15 +153,19 @@ __global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4)))
     for (int64_t c = 0; c < nch; ++c) {
         const int cur = (int)(c & 1);
         if (c + 1 < nch) load_chunk(c + 1);
-        const double2 *wrow = &wt[cur][stream][0];   // uniform unless two streams
-        const double *drow = reinterpret_cast<const double *>(&dd[cur][0]) + sel;
 #pragma unroll 8
         for (int j = 0; j < kCh; ++j) {
-            const double2 s = wrow[j];
-            double d;
-            if (kStaged) d = drow[2 * j];             // this lane's combination
-            else d = fmax(s.x, t1) - t1;              // 0 when w <= t1
-            const double h = s.y * fmin(d, ep);       // T * host seconds held
+            double T, d;
+            if (kStaged) {                            // this lane's combination
+                const double2 s = td[cur][j][sel];
+                T = s.x;
+                d = s.y;
+            } else {
+                const double2 s = wt[cur][j];
+                T = s.y;
+                d = fmax(s.x, t1) - t1;               // 0 when w <= t1
+            }
+            const double h = T * fmin(d, ep);         // T * host seconds held
 #pragma unroll
             for (int l = 0; l < LT; ++l) acc[l] = fma(a2[l], h, acc[l]);
         }

@@ -26,6 +26,8 @@ namespace kvr {
 
 constexpr int kR3Threads = 1024;
 constexpr int kR3BinsPerPass = 16384;  // 128 KiB of LDS counters per pass
+constexpr int kR3BinsSmall = 2048;     // 16 KiB: grids with few deadlines
+constexpr int kR3Unroll = 4;           // draws per thread and step, fetched together
 
 // Number of grid deadlines fl(t1[a] + t2[k]) strictly below x.
 __device__ int32_t deadlines_below(const Tables &tb, double x)
@@ -77,37 +79,54 @@ __global__ void __launch_bounds__(256) r3_zero_kernel(unsigned long long *__rest
 }
 
 // One block per (resample, split of its draws): histogram of T over the
-// stored bins 1..nbins (index b - 1) in LDS, one pass per range of
-// kR3BinsPerPass bins.  A resample with one split owns its row of hist and
-// stores it; several splits add into a zeroed row.
+// stored bins 1..nbins (index b - 1) in LDS, one pass per range of PER bins
+// (a small PER for grids with few deadlines leaves room for more resident
+// blocks).  A resample with one split owns its row of hist and stores it;
+// several splits add into a zeroed row.
+template <int PER>
 __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
     const int32_t *__restrict__ idx, int64_t n, int64_t m, const int2 *__restrict__ binT,
     int64_t nbins, int nsplit, int64_t split_len, unsigned long long *__restrict__ hist,
     int *status)
 {
-    __shared__ unsigned long long lh[kR3BinsPerPass];
+    __shared__ unsigned long long lh[PER];
+    constexpr int64_t per = PER;
     const int64_t r = blockIdx.x / nsplit;
     const int s = (int)(blockIdx.x % nsplit);
     const int64_t j0 = (int64_t)s * split_len;
     const int64_t j1 = (j0 + split_len < m) ? j0 + split_len : m;
+    const int64_t B = blockDim.x;
     unsigned long long *row = hist + r * nbins;
-    for (int64_t b0 = 0; b0 < nbins; b0 += kR3BinsPerPass) {
-        const int64_t nb = (nbins - b0 < kR3BinsPerPass) ? nbins - b0 : kR3BinsPerPass;
+    for (int64_t b0 = 0; b0 < nbins; b0 += per) {
+        const int64_t nb = (nbins - b0 < per) ? nbins - b0 : per;
         for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) lh[x] = 0ull;
         __syncthreads();
-        for (int64_t j = j0 + threadIdx.x; j < j1; j += blockDim.x) {
-            int64_t i = j;
-            if (idx != nullptr) {
-                int32_t ii = idx[r * m + j];
-                if (ii < 0 || (int64_t)ii >= n) {
-                    flag_domain(status);
-                    ii = 0;
+        for (int64_t j = j0 + threadIdx.x; j < j1; j += kR3Unroll * B) {
+            int64_t i[kR3Unroll];
+#pragma unroll
+            for (int u = 0; u < kR3Unroll; ++u) {
+                const int64_t jj = j + u * B;
+                i[u] = -1;                              // past the split: no draw
+                if (jj < j1) {
+                    i[u] = jj;
+                    if (idx != nullptr) {
+                        int32_t ii = idx[r * m + jj];
+                        if (ii < 0 || (int64_t)ii >= n) {
+                            flag_domain(status);
+                            ii = 0;
+                        }
+                        i[u] = ii;
+                    }
                 }
-                i = ii;
             }
-            const int2 bt = binT[i];
-            const int64_t b = (int64_t)bt.x - 1 - b0;   // bin 0 gives b < 0
-            if (b >= 0 && b < nb) atomicAdd(&lh[b], (unsigned long long)bt.y);
+            int2 bt[kR3Unroll];
+#pragma unroll
+            for (int u = 0; u < kR3Unroll; ++u) bt[u] = (i[u] >= 0) ? binT[i[u]] : make_int2(0, 0);
+#pragma unroll
+            for (int u = 0; u < kR3Unroll; ++u) {
+                const int64_t b = (int64_t)bt[u].x - 1 - b0;   // bin 0 gives b < 0
+                if (b >= 0 && b < nb) atomicAdd(&lh[b], (unsigned long long)bt[u].y);
+            }
         }
         __syncthreads();
         for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) {
@@ -183,9 +202,14 @@ hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3
                            stream, ws.S, cnt);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    hipLaunchKernelGGL(r3_hist_kernel, dim3((unsigned)(R * ws.nsplit)), dim3(kR3Threads), 0,
-                       stream, src.idx, src.n, src.m, ws.binT, ws.nbins, ws.nsplit,
-                       ws.split_len, ws.S, status);
+    if (ws.nbins <= kR3BinsSmall)
+        hipLaunchKernelGGL(r3_hist_kernel<kR3BinsSmall>, dim3((unsigned)(R * ws.nsplit)),
+                           dim3(kR3Threads), 0, stream, src.idx, src.n, src.m, ws.binT, ws.nbins,
+                           ws.nsplit, ws.split_len, ws.S, status);
+    else
+        hipLaunchKernelGGL(r3_hist_kernel<kR3BinsPerPass>, dim3((unsigned)(R * ws.nsplit)),
+                           dim3(kR3Threads), 0, stream, src.idx, src.n, src.m, ws.binT, ws.nbins,
+                           ws.nsplit, ws.split_len, ws.S, status);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     hipLaunchKernelGGL(r3_suffix_kernel, dim3((unsigned)R), dim3(kR3Threads), 0, stream, ws.S,
                        ws.nbins);
