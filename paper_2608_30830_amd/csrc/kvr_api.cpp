@@ -411,7 +411,8 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     if (n_resamples * g->n_lam > INT32_MAX) return KVR_E_SIZE;
     const int64_t P = (int64_t)g->n_t1 * g->n_t2;
     const int32_t Lpad = (int32_t)(cdiv(g->n_lam, 32) * 32);
-    const int64_t Rb = kvr::factored_batch(n, n_resamples);
+    const int64_t nqs = kvr::factored_query_slots(n, g->n_t1, P);
+    const int64_t Rb = kvr::factored_batch(nqs, n_resamples);
     size_t off = kStatusBytes;
     auto take = [&](size_t bytes) {
         size_t o = off;
@@ -427,8 +428,10 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     const size_t off_sw = take(sizeof(double) * n);
     const size_t off_u1 = take(sizeof(int32_t) * g->n_t1);
     const size_t off_ue = take(sizeof(int32_t) * P);
-    const size_t off_N = take(sizeof(uint64_t) * Rb * (n + 1));
-    const size_t off_S = take(sizeof(double) * Rb * (n + 1));
+    const size_t off_qslot = take(sizeof(int32_t) * (n + 1));
+    const size_t off_TN = take(sizeof(uint64_t) * Rb * nqs);
+    const size_t off_TS = take(sizeof(double) * Rb * nqs);
+    const size_t off_tot = take(sizeof(uint64_t) * Rb);
     const size_t need = off;
     if (d_ws == nullptr) {
         *ws_bytes = need;
@@ -449,8 +452,11 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     fw.sw = at<double>(d_ws, off_sw);
     fw.u1 = at<int32_t>(d_ws, off_u1);
     fw.ue = at<int32_t>(d_ws, off_ue);
-    fw.N = at<unsigned long long>(d_ws, off_N);
-    fw.S = at<double>(d_ws, off_S);
+    fw.qslot = at<int32_t>(d_ws, off_qslot);
+    fw.nqs = nqs;
+    fw.TN = at<unsigned long long>(d_ws, off_TN);
+    fw.TS = at<double>(d_ws, off_TS);
+    fw.tot = at<unsigned long long>(d_ws, off_tot);
     fw.Rb = Rb;
     SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
     KVR_MARK(g_prof_begin, s);

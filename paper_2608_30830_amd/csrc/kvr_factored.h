@@ -11,13 +11,17 @@ struct FactoredWs {
     int32_t *rank;            // [n] sorted position of each base sample
     int32_t *Ts;              // [n] context size (clamped to >= 1) at each sorted position
     double *sw;               // [n] sorted waits
-    int32_t *u1;              // [K1] sorted waits <= t1
-    int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2
-    unsigned long long *N;    // [Rb][n+1] multiplicities, then exclusive prefix of mult x T
-    double *S;                // [Rb][n+1] exclusive prefix of mult x T x w
+    int32_t *u1;              // [K1] sorted waits <= t1, then that position's query slot
+    int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2, then its query slot
+    int32_t *qslot;           // [n+1] query slot of each sorted position, -1 if none
+    int64_t nqs;              // query slots per row (an upper bound on the distinct positions)
+    unsigned long long *TN;   // [Rb][nqs] N at each query slot: prefix of mult x T
+    double *TS;               // [Rb][nqs] S at each query slot: prefix of mult x T x w
+    unsigned long long *tot;  // [Rb] N over every position
     int64_t Rb;               // resamples per batch
 };
-int64_t factored_batch(int64_t n, int64_t R);
+int64_t factored_query_slots(int64_t n, int64_t K1, int64_t P);
+int64_t factored_batch(int64_t nqs, int64_t R);
 hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, const PriceDev &pr,
                            FactoredWs &ws, int32_t *best, double *best_cost, double *cost_out,
                            int *status, hipStream_t stream);

@@ -16,21 +16,27 @@
 // differently from the brute force's per-sample sums, so the two methods
 // agree within rounding and their selections up to rounding-level ties.
 //
-// Per batch of resamples: factored_hist_kernel (one block per resample,
-// 32-bit LDS counters of multiplicity over ranges of sorted positions),
-// factored_scan_kernel (one block per resample: weights c_i T_i and the N and
-// S prefix sums in place), factored_policy_kernel (one block per (resample,
-// tile of 32 loads): every policy, fused arg-min on the numerators m*C).
+// Once per call: the base waits are radix-sorted; each t1 and each deadline
+// gets its count of waits at or below it (a sorted position, a query), and
+// the distinct query positions are numbered in order (slots).  Per batch of
+// resamples: factored_prefix_kernel (one block per resample: the draws'
+// multiplicities per sorted position in LDS, then, from LDS, a fixed-order
+// scan of the weights c_k T_k (exact) and c_k T_k w_k over the positions that
+// records N and S only at the query positions), factored_policy_kernel (one
+// block per (resample, tile of 32 or 16 loads): every policy from its two slots,
+// fused arg-min on the numerators m*C).
 #include "kvr_device.h"
 #include "kvr_factored.h"
 
 namespace kvr {
 
 constexpr int kFThreads = 1024;
-constexpr int kFRanksPerPass = 32768;   // 128 KiB of 32-bit LDS counters per pass
+constexpr int kFLdsWords = 32768;      // 128 KiB of LDS counters
 constexpr int kFScanPer = 4;            // consecutive positions per thread in the scan
-constexpr int kFLoads = 32;             // loads per policy-kernel block
+constexpr int kFUnroll = 4;             // draws per thread and step, fetched together
+constexpr int kFLoads = 32;             // loads per policy-kernel block (16 when L <= 16)
 constexpr int kFPolThreads = 256;
+constexpr int kFPU = 2;                 // policies per thread and step in the policy kernel
 
 // Per sorted position k: the sorted wait and the context size there (below
 // 1 counts as 1; sort_prep_kernel has flagged it); per base sample: its
@@ -80,183 +86,312 @@ __global__ void __launch_bounds__(256) factored_bounds_kernel(const double *__re
     }
 }
 
-// One block per resample of the batch: row[1 + k] = the number of its draws of
-// the base sample at sorted position k (exact: at most m < 2^31); row[0] = 0.
-__global__ void __launch_bounds__(kFThreads) factored_hist_kernel(
-    const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
-    const int32_t *__restrict__ rank, unsigned long long *__restrict__ N, int *status)
+__global__ void __launch_bounds__(256) factored_fill_kernel(int32_t *__restrict__ qslot,
+                                                            int64_t len)
 {
-    __shared__ uint32_t lh[kFRanksPerPass];
-    const int64_t rb = blockIdx.x;
-    const int64_t r = r0 + rb;
-    unsigned long long *row = N + rb * (n + 1);
-    for (int64_t k0 = 0; k0 < n; k0 += kFRanksPerPass) {
-        const int64_t nk = (n - k0 < kFRanksPerPass) ? n - k0 : kFRanksPerPass;
-        for (int64_t x = threadIdx.x; x < nk; x += blockDim.x) lh[x] = 0u;
-        __syncthreads();
-        for (int64_t j = threadIdx.x; j < m; j += blockDim.x) {
-            int32_t ii = idx[r * m + j];
-            if (ii < 0 || (int64_t)ii >= n) {
-                flag_domain(status);
-                ii = 0;
-            }
-            const int64_t kk = (int64_t)rank[ii] - k0;
-            if (kk >= 0 && kk < nk) atomicAdd(&lh[kk], 1u);
-        }
-        __syncthreads();
-        for (int64_t x = threadIdx.x; x < nk; x += blockDim.x) row[1 + k0 + x] = lh[x];
-        __syncthreads();
-    }
-    if (threadIdx.x == 0) row[0] = 0ull;
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < len) qslot[i] = -1;
 }
 
-// One block per resample of the batch: weights c_k T_k (exact) and inclusive
-// prefix sums over positions 1..n of the weights (N) and of weight x sorted
-// wait (S, fp64), in place.  Each thread sums kFScanPer consecutive positions
-// in order, then the thread totals are scanned across the block: a fixed
-// order, so S is reproducible.
-__global__ void __launch_bounds__(kFThreads) factored_scan_kernel(unsigned long long *__restrict__ N,
-                                                                  double *__restrict__ S,
-                                                                  const double *__restrict__ sw,
-                                                                  const int32_t *__restrict__ Ts,
-                                                                  int64_t n)
+// Marks every query position (several threads may store the same 0).
+__global__ void __launch_bounds__(256) factored_mark_kernel(const int32_t *__restrict__ u1,
+                                                            const int32_t *__restrict__ ue,
+                                                            int32_t K1, int64_t P,
+                                                            int32_t *__restrict__ qslot)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g < K1) qslot[u1[g]] = 0;
+    else if (g - K1 < P) qslot[ue[g - K1]] = 0;
+}
+
+// One block: numbers the marked positions 0, 1, ... in position order
+// (exclusive count of marks below), unmarked positions stay -1.
+__global__ void __launch_bounds__(kFThreads) factored_slot_kernel(int32_t *__restrict__ qslot,
+                                                                  int64_t len)
+{
+    constexpr int nw = kFThreads / kWave;
+    __shared__ int32_t wcount[nw];
+    const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+    int32_t carry = 0;
+    for (int64_t base = 0; base < len; base += kFThreads) {
+        const int64_t p = base + threadIdx.x;
+        const bool marked = p < len && qslot[p] >= 0;
+        const uint64_t bal = __ballot(marked);
+        const int32_t below = (int32_t)__builtin_amdgcn_mbcnt_hi(
+            (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+        if (lane == 0) wcount[wv] = (int32_t)__popcll(bal);
+        __syncthreads();
+        int32_t before = carry, all = 0;
+        for (int q = 0; q < nw; ++q) {
+            if (q < wv) before += wcount[q];
+            all += wcount[q];
+        }
+        if (marked) qslot[p] = before + below;
+        carry += all;
+        __syncthreads();
+    }
+}
+
+// u1[a] and ue[f] from sorted positions to slots.
+__global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict__ u1,
+                                                             int32_t *__restrict__ ue, int32_t K1,
+                                                             int64_t P,
+                                                             const int32_t *__restrict__ qslot)
+{
+    const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (g < K1) u1[g] = qslot[u1[g]];
+    else if (g - K1 < P) ue[g - K1] = qslot[ue[g - K1]];
+}
+
+// One block per resample of the batch.  Per pass over a range of sorted
+// positions: the number of the resample's draws of each position, counted in
+// LDS, then a scan over the range in a fixed order (each thread its
+// kFScanPer consecutive positions, the thread totals across the block: waves
+// in order, lanes of a wave in order, then the earlier passes), which records
+// at every query position k N(k) = sum_{j < k} c_j T_j (exact) and S(k) =
+// sum_{j < k} c_j T_j w_j (reproducible) in the query row.  Position n (every
+// wait) closes the row; tot[rb] = N(n).
+//
+// Counters: 16-bit halves of 32-bit LDS words, kFLdsWords * 2 positions per
+// pass.  A half that passes 65535 carries into (or out of) its word, and that
+// only ever lowers the decoded total, so comparing the decoded total with the
+// number of draws in the range (counted exactly) detects it; the resample then
+// restarts with 32-bit counters, kFLdsWords positions per pass.
+__global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
+    const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
+    const int32_t *__restrict__ rank, const int32_t *__restrict__ Ts,
+    const double *__restrict__ sw, const int32_t *__restrict__ qslot, int64_t nqs,
+    unsigned long long *__restrict__ TN, double *__restrict__ TS,
+    unsigned long long *__restrict__ tot, int *status)
 {
     constexpr int nw = kFThreads / kWave;
     constexpr int kTile = kFThreads * kFScanPer;
+    __shared__ uint32_t lh[kFLdsWords];
     __shared__ unsigned long long wn[nw];
     __shared__ double wsd[nw];
-    __shared__ unsigned long long carry_n;
-    __shared__ double carry_s;
+    __shared__ long long wchk[nw];
     const int64_t rb = blockIdx.x;
-    unsigned long long *nrow = N + rb * (n + 1);
-    double *srow = S + rb * (n + 1);
+    const int64_t r = r0 + rb;
+    unsigned long long *nrow = TN + rb * nqs;
+    double *srow = TS + rb * nqs;
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
-    if (threadIdx.x == 0) {
+    const int64_t B = blockDim.x;
+    unsigned long long carry_n = 0ull;   // totals of the earlier positions (same in every thread)
+    double carry_s = 0.0;
+    for (int wide = 0; wide < 2; ++wide) {
+        const int64_t PP = wide ? kFLdsWords : 2 * (int64_t)kFLdsWords;   // positions per pass
+        bool overflow = false;
         carry_n = 0ull;
         carry_s = 0.0;
-        srow[0] = 0.0;
+        for (int64_t k0 = 0; k0 < n && !overflow; k0 += PP) {
+            const int64_t nk = (n - k0 < PP) ? n - k0 : PP;
+            const int64_t nwords = wide ? nk : (nk + 1) / 2;
+            for (int64_t x = threadIdx.x; x < nwords; x += B) lh[x] = 0u;
+            __syncthreads();
+            long long inr = 0;                              // draws counted in this range
+            for (int64_t j = threadIdx.x; j < m; j += kFUnroll * B) {
+                int32_t ii[kFUnroll];
+#pragma unroll
+                for (int u = 0; u < kFUnroll; ++u) {
+                    ii[u] = -1;                             // past the row: no draw
+                    if (j + u * B < m) {
+                        int32_t v = idx[r * m + j + u * B];
+                        if (v < 0 || (int64_t)v >= n) {
+                            flag_domain(status);
+                            v = 0;
+                        }
+                        ii[u] = v;
+                    }
+                }
+                int64_t kk[kFUnroll];
+#pragma unroll
+                for (int u = 0; u < kFUnroll; ++u) kk[u] = (ii[u] >= 0) ? (int64_t)rank[ii[u]] - k0 : -1;
+#pragma unroll
+                for (int u = 0; u < kFUnroll; ++u) {
+                    if (kk[u] >= 0 && kk[u] < nk) {
+                        ++inr;
+                        if (wide) atomicAdd(&lh[kk[u]], 1u);
+                        else atomicAdd(&lh[kk[u] >> 1], 1u << (16 * (int)(kk[u] & 1)));
+                    }
+                }
+            }
+            __syncthreads();
+            if (!wide) {
+                // decoded total minus the draws counted, over the whole block
+                long long d = -inr;
+                for (int64_t x = threadIdx.x; x < nwords; x += B)
+                    d += (long long)(lh[x] & 0xffffu) + (long long)(lh[x] >> 16);
+                d = wave_sum(d);
+                if (lane == 0) wchk[wv] = d;
+                __syncthreads();
+                long long all = 0;
+                for (int q = 0; q < nw; ++q) all += wchk[q];
+                overflow = all != 0;                        // the same in every thread
+                __syncthreads();
+                if (overflow) break;
+            }
+            for (int64_t base = 0; base < nk; base += kTile) {
+                const int64_t kl = base + (int64_t)threadIdx.x * kFScanPer;   // position in the pass
+                unsigned long long cw[kFScanPer];
+                double sv[kFScanPer];
+                int32_t qs[kFScanPer];
+                unsigned long long tn = 0ull;
+                double ts = 0.0;
+#pragma unroll
+                for (int q = 0; q < kFScanPer; ++q) {
+                    const int64_t k = kl + q;
+                    const bool in = k < nk;
+                    uint32_t c = 0u;
+                    if (in) c = wide ? lh[k] : (lh[k >> 1] >> (16 * (int)(k & 1))) & 0xffffu;
+                    const unsigned long long cwq =
+                        in ? (unsigned long long)c * (unsigned long long)Ts[k0 + k] : 0ull;
+                    cw[q] = cwq;
+                    sv[q] = in ? (double)cwq * sw[k0 + k] : 0.0;
+                    qs[q] = in ? qslot[k0 + k] : -1;
+                    tn += cwq;
+                    ts += sv[q];
+                }
+                unsigned long long xn = tn;            // inclusive scan of the thread totals
+                double xs = ts;
+                for (int off = 1; off < kWave; off <<= 1) {
+                    const unsigned long long on = __shfl_up(xn, off, kWave);
+                    const double os = __shfl_up(xs, off, kWave);
+                    if (lane >= off) {
+                        xn += on;
+                        xs += os;
+                    }
+                }
+                unsigned long long en = __shfl_up(xn, 1, kWave);   // exclusive within the wave
+                double es = __shfl_up(xs, 1, kWave);
+                if (lane == 0) {
+                    en = 0ull;
+                    es = 0.0;
+                }
+                if (lane == kWave - 1) {
+                    wn[wv] = xn;
+                    wsd[wv] = xs;
+                }
+                __syncthreads();
+                unsigned long long pn = carry_n;
+                double ps = carry_s;
+                for (int q = 0; q < wv; ++q) {
+                    pn += wn[q];
+                    ps += wsd[q];
+                }
+                pn += en;
+                ps += es;
+                for (int q = 0; q < nw; ++q) {
+                    carry_n += wn[q];
+                    carry_s += wsd[q];
+                }
+#pragma unroll
+                for (int q = 0; q < kFScanPer; ++q) {
+                    if (qs[q] >= 0 && qs[q] < nqs) {
+                        nrow[qs[q]] = pn;
+                        srow[qs[q]] = ps;
+                    }
+                    pn += cw[q];
+                    ps += sv[q];
+                }
+                __syncthreads();   // wn and wsd are rewritten by the next tile
+            }
+        }
+        if (!overflow) break;
     }
-    __syncthreads();
-    for (int64_t base = 0; base < n; base += kTile) {
-        const int64_t k0 = base + (int64_t)threadIdx.x * kFScanPer;
-        unsigned long long cw[kFScanPer];
-        double sv[kFScanPer];
-        unsigned long long tn = 0ull;
-        double ts = 0.0;
-#pragma unroll
-        for (int q = 0; q < kFScanPer; ++q) {
-            const int64_t k = k0 + q;
-            const unsigned long long c = (k < n) ? nrow[1 + k] * (unsigned long long)Ts[k] : 0ull;
-            cw[q] = c;
-            sv[q] = (k < n) ? (double)c * sw[k] : 0.0;
-            tn += c;
-            ts += sv[q];
+    if (threadIdx.x == 0) {
+        const int32_t q = qslot[n];
+        if (q >= 0 && q < nqs) {
+            nrow[q] = carry_n;
+            srow[q] = carry_s;
         }
-        // inclusive scan of the thread totals within the wave, then across waves
-        unsigned long long c = tn;
-        double s = ts;
-        for (int off = 1; off < kWave; off <<= 1) {
-            const unsigned long long oc = __shfl_up(c, off, kWave);
-            const double os = __shfl_up(s, off, kWave);
-            if (lane >= off) {
-                c += oc;
-                s += os;
-            }
-        }
-        if (lane == kWave - 1) {
-            wn[wv] = c;
-            wsd[wv] = s;
-        }
-        __syncthreads();
-        unsigned long long bn = carry_n;
-        double bs = carry_s;
-        for (int q = 0; q < wv; ++q) {
-            bn += wn[q];
-            bs += wsd[q];
-        }
-        // this thread's exclusive offset, then its positions in order
-        bn += c - tn;
-        bs += s - ts;
-#pragma unroll
-        for (int q = 0; q < kFScanPer; ++q) {
-            const int64_t k = k0 + q;
-            bn += cw[q];
-            bs += sv[q];
-            if (k < n) {
-                nrow[1 + k] = bn;
-                srow[1 + k] = bs;
-            }
-        }
-        __syncthreads();
-        if (threadIdx.x == 0) {
-            unsigned long long t2 = carry_n;
-            double s2 = carry_s;
-            for (int q = 0; q < nw; ++q) {
-                t2 += wn[q];
-                s2 += wsd[q];
-            }
-            carry_n = t2;
-            carry_s = s2;
-        }
-        __syncthreads();
+        tot[rb] = carry_n;
     }
 }
 
-// One block per (resample of the batch, tile of kFLoads loads): every policy's
+// One block per (resample of the batch, tile of FL loads): every policy's
 // closed-form total m*C for the tile's loads, the optional cost output, and
 // the arg-min per load under the library's total order (smaller first, then
 // larger flat index).  Dividing by m is monotone, so the arg-min compares the
 // totals and only the selected one is divided.
+template <int FL>
 __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
-    const unsigned long long *__restrict__ N, const double *__restrict__ S, int64_t n, int64_t m,
-    int64_t r0, int ntl, Tables tb, PriceDev pr, const int32_t *__restrict__ u1,
-    const int32_t *__restrict__ ue, int32_t *__restrict__ best, double *__restrict__ best_cost,
-    double *__restrict__ cost_out)
+    const unsigned long long *__restrict__ TN, const double *__restrict__ TS, int64_t nqs,
+    const unsigned long long *__restrict__ totN, int64_t m, int64_t r0, int ntl, Tables tb,
+    PriceDev pr, const int32_t *__restrict__ u1, const int32_t *__restrict__ ue,
+    int32_t *__restrict__ best, double *__restrict__ best_cost, double *__restrict__ cost_out)
 {
     constexpr int nw = kFPolThreads / kWave;
-    __shared__ double rc[nw][kFLoads];
-    __shared__ int32_t rf[nw][kFLoads];
+    __shared__ double rc[nw][FL];
+    __shared__ int32_t rf[nw][FL];
     const int64_t rb = blockIdx.x / ntl;
     const int tile = (int)(blockIdx.x % ntl);
     const int64_t r = r0 + rb;
-    const unsigned long long *nrow = N + rb * (n + 1);
-    const double *srow = S + rb * (n + 1);
+    const unsigned long long *nrow = TN + rb * nqs;   // N and S at the query slots
+    const double *srow = TS + rb * nqs;
     const int64_t P = (int64_t)tb.K1 * tb.K2;
-    const int l0 = tile * kFLoads;
-    const int nl = (tb.L - l0 < kFLoads) ? tb.L - l0 : kFLoads;
-    const double tot = (double)nrow[n];
+    const int l0 = tile * FL;
+    const int nl = (tb.L - l0 < FL) ? tb.L - l0 : FL;
+    const double tot = (double)totN[rb];
     const double md = (double)m;
-    double a2[kFLoads], bc[kFLoads];
-    int32_t bf[kFLoads];
+    double a2[FL], bc[FL];
+    int32_t bf[FL];
 #pragma unroll
-    for (int l = 0; l < kFLoads; ++l) {
+    for (int l = 0; l < FL; ++l) {
         a2[l] = tb.a2[l0 + l];   // zero-padded to whole tiles
         bc[l] = INFINITY;
         bf[l] = -1;
     }
-    for (int64_t f = threadIdx.x; f < P; f += blockDim.x) {
-        const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
-        const double t1 = tb.t1[a];
-        const double e = t1 + tb.t2[k];
-        const int32_t p1 = u1[a], pe = ue[f];
-        const double n1 = (double)nrow[p1], ne = (double)nrow[pe];
-        const double s1 = srow[p1], se = srow[pe];
-        const double hbm = s1 + t1 * (tot - n1);
-        double hold = (se - s1) - t1 * (ne - n1);
-        if (!isinf(e)) hold = hold + (e - t1) * (tot - ne);
-        const double fixed = pr.a1 * hbm + pr.b2 * (ne - n1) + pr.b3 * (tot - ne);
+    // kFPU policies per thread and step: their slots, then their prefix
+    // values, are fetched together before any is used.  P < 2^24, so policy
+    // indices are split in 32-bit arithmetic.
+    const uint32_t B = blockDim.x, K2 = (uint32_t)tb.K2, P32 = (uint32_t)P;
+    for (uint32_t f0 = threadIdx.x; f0 < P32; f0 += kFPU * B) {
+        int32_t p1[kFPU], pe[kFPU];
+        double t1[kFPU], e[kFPU];
 #pragma unroll
-        for (int l = 0; l < kFLoads; ++l) {
-            if (l < nl) {
+        for (int u = 0; u < kFPU; ++u) {
+            const uint32_t f = (f0 + u * B < P32) ? f0 + u * B : f0;   // a repeat of f0 is skipped below
+            const uint32_t a = f / K2, k = f - a * K2;
+            t1[u] = tb.t1[a];
+            e[u] = t1[u] + tb.t2[k];
+            p1[u] = u1[a];
+            pe[u] = ue[f];
+        }
+        double n1[kFPU], ne[kFPU], s1[kFPU], se[kFPU];
+#pragma unroll
+        for (int u = 0; u < kFPU; ++u) {
+            n1[u] = (double)nrow[p1[u]];
+            ne[u] = (double)nrow[pe[u]];
+            s1[u] = srow[p1[u]];
+            se[u] = srow[pe[u]];
+        }
+#pragma unroll
+        for (int u = 0; u < kFPU; ++u) {
+            const uint32_t f = f0 + u * B;
+            if (f >= P32) break;
+            const double hbm = s1[u] + t1[u] * (tot - n1[u]);
+            double hold = (se[u] - s1[u]) - t1[u] * (ne[u] - n1[u]);
+            if (!isinf(e[u])) hold = hold + (e[u] - t1[u]) * (tot - ne[u]);
+            const double fixed = pr.a1 * hbm + pr.b2 * (ne[u] - n1[u]) + pr.b3 * (tot - ne[u]);
+            if (cost_out != nullptr) {
+                for (int l = 0; l < nl; ++l)
+                    cost_out[(r * tb.L + l0 + l) * P + f] = (fixed + a2[l] * hold) / md;
+            }
+            // every load of the tile (a2 is zero-padded past L; those lanes are
+            // never stored); a thread visits its policies in increasing f, so
+            // "not larger" keeps the larger index on a tie, as the total order asks
+#pragma unroll
+            for (int l = 0; l < FL; ++l) {
                 const double tc = fixed + a2[l] * hold;
-                if (cost_out != nullptr) cost_out[(r * tb.L + l0 + l) * P + f] = tc / md;
-                argmin_merge(bc[l], bf[l], tc, (int32_t)f);
+                const bool take = tc <= bc[l];
+                bc[l] = take ? tc : bc[l];
+                bf[l] = take ? (int32_t)f : bf[l];
             }
         }
     }
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
 #pragma unroll
-    for (int l = 0; l < kFLoads; ++l) {
+    for (int l = 0; l < FL; ++l) {
         wave_argmin(bc[l], bf[l]);
         if (lane == 0) {
             rc[wv][l] = bc[l];
@@ -274,12 +409,22 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
     }
 }
 
-int64_t factored_batch(int64_t n, int64_t R)
+int64_t factored_query_slots(int64_t n, int64_t K1, int64_t P)
 {
-    // at most 1 GiB of prefix rows (16 bytes per position) per batch
-    int64_t rb = ((int64_t)1 << 30) / ((n + 1) * 16);
+    // distinct query positions: at most one per t1 and deadline, at most n + 1
+    return (K1 + P < n + 1) ? K1 + P : n + 1;
+}
+
+int64_t factored_batch(int64_t nqs, int64_t R)
+{
+    // at most 2 GiB of query rows per batch, and batches of equal size (a
+    // short last batch would leave most of the chip idle)
+    const int64_t per = nqs * 16 + 8;
+    int64_t rb = ((int64_t)1 << 31) / per;
     if (rb < 1) rb = 1;
-    return rb < R ? rb : R;
+    if (rb >= R) return R;
+    const int64_t nb = (R + rb - 1) / rb;
+    return (R + nb - 1) / nb;
 }
 
 hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, const PriceDev &pr,
@@ -295,19 +440,32 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
                        stream, ws.sort.keys[cur], ws.sort.vals[cur], src.T, n, ws.sw, ws.Ts,
                        ws.rank);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    hipLaunchKernelGGL(factored_bounds_kernel, dim3((unsigned)((tb.K1 + P + 255) / 256)), dim3(256),
-                       0, stream, ws.sw, n, tb, ws.u1, ws.ue);
+    const unsigned gq = (unsigned)((tb.K1 + P + 255) / 256);
+    hipLaunchKernelGGL(factored_bounds_kernel, dim3(gq), dim3(256), 0, stream, ws.sw, n, tb, ws.u1,
+                       ws.ue);
+    hipLaunchKernelGGL(factored_fill_kernel, dim3((unsigned)((n + 1 + 255) / 256)), dim3(256), 0,
+                       stream, ws.qslot, n + 1);
+    hipLaunchKernelGGL(factored_mark_kernel, dim3(gq), dim3(256), 0, stream, ws.u1, ws.ue, tb.K1, P,
+                       ws.qslot);
+    hipLaunchKernelGGL(factored_slot_kernel, dim3(1), dim3(kFThreads), 0, stream, ws.qslot, n + 1);
+    hipLaunchKernelGGL(factored_remap_kernel, dim3(gq), dim3(256), 0, stream, ws.u1, ws.ue, tb.K1, P,
+                       ws.qslot);
     if ((err = hipGetLastError()) != hipSuccess) return err;
-    const int ntl = (tb.L + kFLoads - 1) / kFLoads;
+    const int FL = tb.L <= 16 ? 16 : kFLoads;                 // loads per policy block
+    const int ntl = (tb.L + FL - 1) / FL;
     for (int64_t r0 = 0; r0 < R; r0 += ws.Rb) {
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
-        hipLaunchKernelGGL(factored_hist_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
-                           src.idx, n, m, r0, ws.rank, ws.N, status);
-        hipLaunchKernelGGL(factored_scan_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
-                           ws.N, ws.S, ws.sw, ws.Ts, n);
-        hipLaunchKernelGGL(factored_policy_kernel, dim3((unsigned)(rb * ntl)), dim3(kFPolThreads), 0,
-                           stream, ws.N, ws.S, n, m, r0, ntl, tb, pr, ws.u1, ws.ue, best, best_cost,
-                           cost_out);
+        hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
+                           src.idx, n, m, r0, ws.rank, ws.Ts, ws.sw, ws.qslot, ws.nqs, ws.TN, ws.TS,
+                           ws.tot, status);
+        if (FL == 16)
+            hipLaunchKernelGGL(factored_policy_kernel<16>, dim3((unsigned)(rb * ntl)),
+                               dim3(kFPolThreads), 0, stream, ws.TN, ws.TS, ws.nqs, ws.tot, m, r0,
+                               ntl, tb, pr, ws.u1, ws.ue, best, best_cost, cost_out);
+        else
+            hipLaunchKernelGGL(factored_policy_kernel<kFLoads>, dim3((unsigned)(rb * ntl)),
+                               dim3(kFPolThreads), 0, stream, ws.TN, ws.TS, ws.nqs, ws.tot, m, r0,
+                               ntl, tb, pr, ws.u1, ws.ue, best, best_cost, cost_out);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
     return hipSuccess;

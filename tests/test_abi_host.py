@@ -228,9 +228,16 @@ def test_factored_bootstrap_host_errors(lib):
     assert boot(grid=kvr.PolicyGrid([0.0], [math.inf, 5.0], [0.1])) == kvr.KVR_E_GRID
     assert boot() == kvr.KVR_OK
     small = sz.value
-    assert small > 2 * 1001 * 16                      # two prefix rows of n + 1 entries
+    # per resample one row of N and S at the query slots: at most one slot per
+    # t1 and deadline (2 + 4 here), at most n + 1
+    assert small > 2 * 6 * 16 + 1001 * 4
+    wide = kvr.PolicyGrid([0.0], list(np.geomspace(1.0, 1e5, 3000)), [0.1])
+    assert boot(grid=wide) == kvr.KVR_OK
+    assert sz.value - small > 2 * 1001 * 16           # slots capped at n + 1 = 1001 per row
     assert boot(R=100000, m=65536, n=65536) == kvr.KVR_OK
-    assert sz.value < (1 << 30) + (64 << 20)          # prefix rows are batched under 1 GiB
+    assert sz.value < (2 << 30) + (64 << 20)          # count and query rows batched under 2 GiB
+    assert boot(R=100000, m=65536, n=65536, grid=wide) == kvr.KVR_OK
+    assert sz.value < (2 << 30) + (64 << 20)
     boot()
     sz.value = 1
     assert boot(ws=FAKE) == kvr.KVR_E_WORKSPACE

@@ -113,3 +113,32 @@ def test_factored_domain_errors(kvr):
             kvr.kvr_bootstrap(_dev(w, _f64()), _dev(wl.ctx_tokens, _i32()), _dev(idx, _i32()),
                               _lib_prices(kvr, wl), g, factored=True)
         assert ei.value.code == kvr.KVR_E_DOMAIN
+
+
+@pytest.mark.parametrize("n", [1000, 100000])
+def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
+    """Rows that draw one base sample 65,535, 65,536 or 70,000 times (at an even
+    and at an odd sorted position), so that a 16-bit multiplicity counter
+    wraps: the kernel must detect it and recount the row with 32-bit counters.
+    With n = 100,000 the positions take two counting passes."""
+    m = 70000
+    wl = workloads.random_case(208, n, 1, 9, 3, resamples=6, m=m, ties=True)
+    order = np.argsort(wl.wait_s, kind="stable")
+    even, odd = int(order[10]), int(order[11])       # sorted positions 10 and 11
+    rng = np.random.Generator(np.random.PCG64(209))
+    idx = rng.integers(0, n, size=(6, m), dtype=np.int32)
+    idx[0, :] = even                                  # 70,000 draws of one sample
+    idx[1, :] = odd
+    idx[2, :65536] = even                             # exactly 65,536
+    idx[3, :65536] = odd
+    idx[4, :65535] = odd                              # the largest count that fits
+    wl.idx = idx                                      # row 5 stays random
+    best, bc, cost = _factored(kvr, wl, want_cost=True)
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(6):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref, _np(best)[r], rb)
+        assert_costs(_np(bc)[r], rbc)
