@@ -203,17 +203,18 @@ int hip_ok(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_E_HIP; }
         if (rc_ != KVR_OK) return rc_;      \
     } while (0)
 
-// Uploads t1, t2 (canonical zeros) and the padded a2 table; clears the status word.
+// Uploads t1, t2 (canonical zeros) and the padded a2 table and clears the status
+// word (one launch when the tables are small).
 int stage_tables(void *ws, size_t off_t1, size_t off_t2, size_t off_a2, int32_t Lpad,
                  const kvr_prices &p, const kvr_policy_grid &g, hipStream_t s, Tables &tb)
 {
     std::vector<double> t1(g.t1, g.t1 + g.n_t1), t2(g.t2, g.t2 + g.n_t2), a2;
     for (double &v : t1) v = v + 0.0;
     congestion_prices(p, g, Lpad, a2);
-    KVR_TRY(kvr::launch_clear_status(static_cast<int *>(ws), s));
-    KVR_TRY(kvr::launch_upload(at<double>(ws, off_t1), t1.data(), g.n_t1, s));
-    KVR_TRY(kvr::launch_upload(at<double>(ws, off_t2), t2.data(), g.n_t2, s));
-    KVR_TRY(kvr::launch_upload(at<double>(ws, off_a2), a2.data(), Lpad, s));
+    double *const dst[3] = {at<double>(ws, off_t1), at<double>(ws, off_t2), at<double>(ws, off_a2)};
+    const double *const src[3] = {t1.data(), t2.data(), a2.data()};
+    const int64_t cnt[3] = {g.n_t1, g.n_t2, Lpad};
+    KVR_TRY(kvr::launch_stage(static_cast<int *>(ws), dst, src, cnt, s));
     tb.t1 = at<double>(ws, off_t1);
     tb.t2 = at<double>(ws, off_t2);
     tb.a2 = at<double>(ws, off_a2);

@@ -32,6 +32,44 @@ hipError_t launch_clear_status(int *status, hipStream_t stream)
     return hipGetLastError();
 }
 
+// Clears the status word and stores up to three host tables in one launch
+// when they fit one payload together.
+struct StagePlan {
+    double *dst[3];
+    int cnt[3];
+};
+
+__global__ void stage_kernel(int *status, StagePlan sp, UploadPayload p)
+{
+    if (threadIdx.x == 0) status[0] = 0;
+    int off = 0;
+    for (int t = 0; t < 3; ++t) {
+        for (int i = threadIdx.x; i < sp.cnt[t]; i += blockDim.x) sp.dst[t][i] = p.v[off + i];
+        off += sp.cnt[t];
+    }
+}
+
+hipError_t launch_stage(int *status, double *const dst[3], const double *const src[3],
+                        const int64_t cnt[3], hipStream_t stream)
+{
+    if (cnt[0] + cnt[1] + cnt[2] <= kUploadMax) {
+        StagePlan sp;
+        UploadPayload p;
+        int off = 0;
+        for (int t = 0; t < 3; ++t) {
+            sp.dst[t] = dst[t];
+            sp.cnt[t] = (int)cnt[t];
+            for (int64_t i = 0; i < cnt[t]; ++i) p.v[off++] = src[t][i];
+        }
+        for (int i = off; i < kUploadMax; ++i) p.v[i] = 0.0;
+        hipLaunchKernelGGL(stage_kernel, dim3(1), dim3(256), 0, stream, status, sp, p);
+        return hipGetLastError();
+    }
+    hipError_t err = launch_clear_status(status, stream);
+    for (int t = 0; t < 3 && err == hipSuccess; ++t) err = launch_upload(dst[t], src[t], cnt[t], stream);
+    return err;
+}
+
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream)
 {
     for (int64_t off = 0; off < count; off += kUploadMax) {

@@ -73,6 +73,8 @@ struct R3Ws {
 // ---- launches (all asynchronous on `stream`) --------------------------------
 hipError_t launch_clear_status(int *status, hipStream_t stream);
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
+hipError_t launch_stage(int *status, double *const dst[3], const double *const src[3],
+                        const int64_t cnt[3], hipStream_t stream);
 
 // X and G per (resample, t1); with few resamples the samples are cut into
 // parts (partials in xgp[parts][R][K1][2], summed in part order).

@@ -245,6 +245,159 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     }
 }
 
+// n <= kSortTile: the whole sorted path's sort (and, with Nsum, its prefix
+// arrays) in one block, so a small sample costs two launches instead of
+// thirty.  Keys and payload stay in LDS for the eight digit passes, ranked as
+// in sort_scatter_kernel with the tile as the whole array (a stable counting
+// sort per digit); then the sorted keys and payload are stored, and, with
+// Nsum, the inclusive prefix arrays of T and T*w in a fixed order (each thread
+// its kSortKPT consecutive positions, the thread totals across the block).
+__global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
+    const double *__restrict__ w, const int32_t *__restrict__ T, int64_t n,
+    uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int64_t *__restrict__ Nsum,
+    double *__restrict__ Ssum, int32_t *__restrict__ perm_out, int *status)
+{
+    __shared__ uint64_t lk[2][kSortTile];
+    __shared__ int32_t lv[2][kSortTile];
+    __shared__ uint32_t wcnt[4][256];
+    __shared__ uint32_t wofs[4][256];
+    __shared__ uint32_t dbase[256];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int nn = (int)n;   // at most kSortTile
+    for (int i = threadIdx.x; i < nn; i += kSortThreads) {
+        uint64_t b = (uint64_t)__double_as_longlong(w[i]);
+        if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
+        if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
+            flag_domain(status);
+            b = 0;
+        }
+        if (T[i] < 1) flag_domain(status);
+        lk[0][i] = b;
+        lv[0][i] = i;
+    }
+    int cur = 0;
+    for (int pass = 0; pass < 8; ++pass) {
+        const int shift = 8 * pass;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
+        __syncthreads();
+        uint64_t key[kSortKPT];
+        int32_t val[kSortKPT];
+        uint32_t local[kSortKPT];
+#pragma unroll
+        for (int j = 0; j < kSortKPT; ++j) {
+            const int i = wave * kWaveKeys + j * kWave + lane;
+            const bool valid = i < nn;
+            key[j] = valid ? lk[cur][i] : 0;
+            val[j] = valid ? lv[cur][i] : 0;
+            const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+            uint64_t peers = __ballot(valid);
+#pragma unroll
+            for (int b = 0; b < 8; ++b) {
+                const bool bit = (d >> b) & 1u;
+                const uint64_t m = __ballot(bit);
+                peers &= bit ? m : ~m;
+            }
+            const uint32_t rank = lanes_below(peers);
+            const uint32_t before = wcnt[wave][d];
+            local[j] = before + rank;
+            __builtin_amdgcn_wave_barrier();
+            if (valid && rank == 0) wcnt[wave][d] = before + (uint32_t)__popcll(peers);
+            __builtin_amdgcn_wave_barrier();
+        }
+        __syncthreads();
+        {
+            const int d = threadIdx.x;
+            uint32_t run = 0;
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+                wofs[q][d] = run;
+                run += wcnt[q][d];
+            }
+            uint32_t all;
+            dbase[d] = block_exclusive_scan(run, &all);   // run = the count of digit d
+        }
+        __syncthreads();
+#pragma unroll
+        for (int j = 0; j < kSortKPT; ++j) {
+            const int i = wave * kWaveKeys + j * kWave + lane;
+            if (i < nn) {
+                const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+                const uint32_t pos = dbase[d] + wofs[wave][d] + local[j];
+                if (pos < (uint32_t)nn) {                 // always true; never write outside
+                    lk[cur ^ 1][pos] = key[j];
+                    lv[cur ^ 1][pos] = val[j];
+                }
+            }
+        }
+        __syncthreads();
+        cur ^= 1;
+    }
+    for (int i = threadIdx.x; i < nn; i += kSortThreads) {
+        keys_out[i] = lk[cur][i];
+        vals_out[i] = lv[cur][i];
+    }
+    if (Nsum == nullptr) return;   // uniform: the sort alone
+    const int k0 = (int)threadIdx.x * kSortKPT;
+    int64_t tn[kSortKPT];
+    double ts[kSortKPT];
+    int64_t sn = 0;
+    double ss = 0.0;
+#pragma unroll
+    for (int q = 0; q < kSortKPT; ++q) {
+        const int k = k0 + q;
+        if (k < nn) {
+            const int32_t pj = lv[cur][k];
+            const int32_t p = (pj >= 0 && pj < nn) ? pj : 0;   // a permutation of [0, n)
+            const int32_t t = T[p] < 1 ? 1 : T[p];
+            sn += t;
+            ss += (double)t * __longlong_as_double((long long)lk[cur][k]);
+            if (perm_out != nullptr) perm_out[k] = p;
+        }
+        tn[q] = sn;
+        ts[q] = ss;
+    }
+    int64_t xn = sn;                 // inclusive scan of the thread totals in the wave
+    double xs = ss;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int64_t yn = __shfl_up(xn, off, kWave);
+        const double ys = __shfl_up(xs, off, kWave);
+        if (lane >= off) {
+            xn += yn;
+            xs += ys;
+        }
+    }
+    int64_t en = __shfl_up(xn, 1, kWave);   // exclusive within the wave
+    double es = __shfl_up(xs, 1, kWave);
+    if (lane == 0) {
+        en = 0;
+        es = 0.0;
+    }
+    __shared__ int64_t wn[kSortThreads / kWave];
+    __shared__ double wsm[kSortThreads / kWave];
+    if (lane == kWave - 1) {
+        wn[wave] = xn;
+        wsm[wave] = xs;
+    }
+    __syncthreads();
+    int64_t pn = 0;
+    double ps = 0.0;
+    for (int q = 0; q < wave; ++q) {
+        pn += wn[q];
+        ps += wsm[q];
+    }
+    pn += en;
+    ps += es;
+#pragma unroll
+    for (int q = 0; q < kSortKPT; ++q) {
+        const int k = k0 + q;
+        if (k < nn) {
+            Nsum[k] = pn + tn[q];
+            Ssum[k] = ps + ts[q];
+        }
+    }
+}
+
 // Per scan tile: sums of T and T*w over the sorted order.
 __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
@@ -450,6 +603,12 @@ hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs
                             int *status, hipStream_t stream)
 {
     hipError_t err;
+    if (n <= kSortTile) {   // one block
+        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
+                           ws.keys[0], ws.vals[0], nullptr, nullptr, nullptr, status);
+        *cur_out = 0;
+        return hipGetLastError();
+    }
     hipLaunchKernelGGL(sort_prep_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, stream, w, T,
                        n, ws.keys[0], ws.vals[0], status);
     if ((err = hipGetLastError()) != hipSuccess) return err;
@@ -474,6 +633,14 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
                               const PriceDev &pr, SortWs &ws, double *cost_out,
                               int32_t *perm_out, int *status, hipStream_t stream)
 {
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    if (n <= kSortTile) {   // sort and prefix arrays in one block
+        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
+                           ws.keys[0], ws.vals[0], ws.Nsum, ws.Ssum, perm_out, status);
+        hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
+                           ws.keys[0], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
+        return hipGetLastError();
+    }
     int cur = 0;
     hipError_t err = launch_sort_keys(w, T, n, ws, &cur, status, stream);
     if (err != hipSuccess) return err;
@@ -484,7 +651,6 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
     hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
                        ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
                        perm_out);
-    const int64_t P = (int64_t)tb.K1 * tb.K2;
     hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
                        ws.keys[cur], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
     return hipGetLastError();
