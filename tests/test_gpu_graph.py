@@ -1,4 +1,5 @@
-"""HIP-graph capture of prepared calls.  The entry points only enqueue kernels
+"""HIP-graph capture of prepared calls (the brute-force and the factored
+bootstrap, the controller).  The entry points only enqueue kernels
 on the caller's stream (no allocation, no memset, no synchronisation; the
 host tables travel as kernel arguments), so a prepared BootstrapCall or
 ControllerCall can be captured once and replayed.  Every replay, with eager
@@ -25,7 +26,8 @@ def kvr():
     return k
 
 
-def test_bootstrap_graph_replays(kvr):
+@pytest.mark.parametrize("factored", [False, True])
+def test_bootstrap_graph_replays(kvr, factored):
     import torch
     wl = workloads.make("boot-1024x64k", resamples=64)
     pf = wl.platform
@@ -33,7 +35,8 @@ def test_bootstrap_graph_replays(kvr):
                                       pf["host_link_bytes_per_s"], pf["prefill_tokens_per_s"])
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
     call = kvr.BootstrapCall(torch.as_tensor(wl.wait_s).cuda(), torch.as_tensor(wl.ctx_tokens).cuda(),
-                             torch.as_tensor(wl.idx).cuda(), pr, g, want_cost=True)
+                             torch.as_tensor(wl.idx).cuda(), pr, g, want_cost=True,
+                             factored=factored)
     call.launch()
     torch.cuda.synchronize()
     assert call.status() == kvr.KVR_OK
