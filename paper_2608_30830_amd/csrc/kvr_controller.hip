@@ -13,6 +13,7 @@ namespace kvr {
 
 constexpr int kCountThreads = 256;
 constexpr int kCountMaxBlocks = 2048;
+constexpr int kCountUnroll = 4;
 
 struct CountWs {
     unsigned long long n_short;
@@ -28,7 +29,9 @@ __global__ void zero_counts_kernel(CountWs *c)
 }
 
 // counts.n_short += #(w <= t_star); counts.tokens += sum of context tokens
-// (one per request without contexts).  Waits must be finite and >= 0.
+// (one per request without contexts).  Waits must be finite and >= 0.  Each
+// thread fetches kCountUnroll elements before using them; each block adds its
+// totals with one integer atomic per counter.
 __global__ void __launch_bounds__(kCountThreads) short_count_kernel(
     const double *__restrict__ wait, const int32_t *__restrict__ ctx, int64_t N, double t_star,
     CountWs *counts, int *status)
@@ -36,19 +39,44 @@ __global__ void __launch_bounds__(kCountThreads) short_count_kernel(
     int64_t n_short = 0, tokens = 0;
     bool bad = false;
     const int64_t stride = (int64_t)gridDim.x * blockDim.x;
-    for (int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i < N; i += stride) {
-        const double w = wait[i];
-        const uint64_t bits = (uint64_t)__double_as_longlong(w);
-        bad |= !(bits < 0x7ff0000000000000ull || bits == 0x8000000000000000ull);
-        n_short += (w <= t_star) ? 1 : 0;
-        tokens += ctx ? (int64_t)ctx[i] : 1;
+    for (int64_t i0 = (int64_t)blockIdx.x * blockDim.x + threadIdx.x; i0 < N;
+         i0 += kCountUnroll * stride) {
+        double w[kCountUnroll];
+        int32_t t[kCountUnroll];
+#pragma unroll
+        for (int u = 0; u < kCountUnroll; ++u) {
+            const int64_t i = i0 + u * stride;
+            const bool in = i < N;
+            w[u] = in ? wait[i] : 0.0;
+            t[u] = in ? (ctx ? ctx[i] : 1) : 0;
+        }
+#pragma unroll
+        for (int u = 0; u < kCountUnroll; ++u) {
+            const bool in = i0 + u * stride < N;
+            const uint64_t bits = (uint64_t)__double_as_longlong(w[u]);
+            bad |= !(bits < 0x7ff0000000000000ull || bits == 0x8000000000000000ull);
+            n_short += (in && w[u] <= t_star) ? 1 : 0;
+            tokens += t[u];
+        }
     }
     if (bad) flag_domain(status);
     n_short = wave_sum(n_short);
     tokens = wave_sum(tokens);
-    if ((threadIdx.x & (kWave - 1)) == 0) {
-        atomicAdd(&counts->n_short, (unsigned long long)n_short);
-        atomicAdd(&counts->tokens, (unsigned long long)tokens);
+    __shared__ int64_t part[2][kCountThreads / kWave];
+    const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+    if (lane == 0) {
+        part[0][wv] = n_short;
+        part[1][wv] = tokens;
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        int64_t a = 0, b = 0;
+        for (int q = 0; q < kCountThreads / kWave; ++q) {
+            a += part[0][q];
+            b += part[1][q];
+        }
+        atomicAdd(&counts->n_short, (unsigned long long)a);
+        atomicAdd(&counts->tokens, (unsigned long long)b);
     }
 }
 
@@ -117,7 +145,7 @@ hipError_t launch_short_count(const double *wait, const int32_t *ctx, int64_t N,
     hipLaunchKernelGGL(zero_counts_kernel, dim3(1), dim3(64), 0, stream, c);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
-    int64_t blocks = (N + kCountThreads * 8 - 1) / (kCountThreads * 8);
+    int64_t blocks = (N + kCountThreads * 16 - 1) / (kCountThreads * 16);
     if (blocks > kCountMaxBlocks) blocks = kCountMaxBlocks;
     if (blocks < 1) blocks = 1;
     hipLaunchKernelGGL(short_count_kernel, dim3((unsigned)blocks), dim3(kCountThreads), 0, stream,
