@@ -593,12 +593,6 @@ __global__ void __launch_bounds__(256) closed_form_kernel(const uint64_t *__rest
     for (int l = 0; l < tb.L; ++l) cost[(int64_t)l * P + f] = (fixed + tb.a2[l] * hold) / nd;
 }
 
-__global__ void zero_u32_kernel(uint32_t *p, int64_t len)
-{
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < len) p[i] = 0;
-}
-
 hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs &ws, int *cur_out,
                             int *status, hipStream_t stream)
 {
