@@ -171,9 +171,12 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
                   void *d_ws, size_t *ws_bytes, void *hip_stream);
 
 /*
- * Synchronise hip_stream and read the status word of a workspace used by
- * kvr_cost_grid or kvr_bootstrap: KVR_OK, KVR_E_DOMAIN, or KVR_E_HIP if the
- * synchronisation or the read failed.  d_ws NULL is KVR_E_NULL.
+ * Synchronise hip_stream and read the status word (the first bytes of the
+ * workspace) of a call of any compute entry point here (kvr_cost_grid,
+ * kvr_bootstrap, kvr_bootstrap_factored, kvr_capacity_replay,
+ * kvr_controller_select, kvr_crossover_statistic): KVR_OK, KVR_E_DOMAIN, or
+ * KVR_E_HIP if the synchronisation or the read failed.  d_ws NULL is
+ * KVR_E_NULL.
  */
 int kvr_workspace_status(const void *d_ws, void *hip_stream);
 
