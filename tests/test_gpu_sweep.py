@@ -66,3 +66,27 @@ def test_grid_shapes(kvr, oracle_mod, case):
             rb, rbc, _ = oracle_mod.select(ref, wl.t2)
             assert_selection(ref, _np(best)[r], rb)
             assert_costs(_np(bc)[r], rbc)
+
+
+@pytest.mark.parametrize("n", [2047, 2048, 2049, 4096, 4097])
+def test_sort_path_boundaries(kvr, oracle_mod, n):
+    """Sample sizes around the one-block sort (at most 2,048 waits) and the
+    2,048-key tiles of the multi-block sort: the SORTED grid and its order
+    against the oracle, and the factored bootstrap, which sorts the same way."""
+    wl = workloads.random_case(7000 + n, n, 2, 70, 5, resamples=2, m=n, ties=True)
+    pr = oracle_mod.workload_prices(wl)
+    lp = _lib_prices(kvr, wl)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    cost, perm = kvr.kvr_cost_grid(w, T, lp, g, method=kvr.KVR_SORTED, want_perm=True)
+    assert np.array_equal(_np(perm), oracle_mod.stable_order(wl.wait_s))
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    assert_costs(_np(cost), ref)
+    best, bc, cost = kvr.kvr_bootstrap(w, T, _dev(wl.idx, _i32()), lp, g, want_cost=True,
+                                       factored=True)
+    for r in range(2):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb = oracle_mod.select(ref, wl.t2)[0]
+        assert_selection(ref, _np(best)[r], rb)
