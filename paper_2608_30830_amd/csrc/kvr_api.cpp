@@ -102,6 +102,7 @@ struct BrutePlan {
     int64_t r3_bins;         // finite grid deadlines (bins kept per resample)
     int r3_nsplit;
     int64_t r3_split_len;
+    int64_t max_blocks;      // largest launch grid of the plan
 };
 
 int choose_tile(int32_t L)
@@ -178,6 +179,20 @@ BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, 
         if (bootstrap && !want_cost) bp.off_cost = take(sizeof(double) * R * L * P);
     }
     bp.total = off;
+    // the largest launch grid of the plan, in blocks (every launch takes a
+    // 32-bit grid; the callers' bounds keep these products inside int64)
+    const int64_t rows = R * gp.ntiles * gp.LT;
+    const int64_t grids[] = {gp.ngroups * gp.nsplit * gp.ntiles,
+                             R * cdiv(K1, 8) * parts,
+                             cdiv(R * K1, 256),
+                             cdiv(R * bp.r3_bins, 256),
+                             R * bp.r3_nsplit,
+                             cdiv(rows * P, 256),
+                             cdiv(R * gp.ntiles * P, 256),
+                             cdiv(R * L, 4),
+                             R * L};
+    bp.max_blocks = 0;
+    for (int64_t v : grids) bp.max_blocks = std::max(bp.max_blocks, v);
     return bp;
 }
 
@@ -287,6 +302,7 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     int32_t Lpad = g->n_lam;
     if (method == KVR_BRUTE) {
         bp = plan_brute(1, n, n, *g, false, true);
+        if (bp.max_blocks > INT32_MAX) return KVR_E_SIZE;
         need = bp.total;
     } else {
         off_t2 = off_t1 + align256(sizeof(double) * g->n_t1);
@@ -359,6 +375,7 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     if (n_resamples * g->n_lam > INT32_MAX) return KVR_E_SIZE;
     const bool want_cost = d_cost != nullptr;
     BrutePlan bp = plan_brute(n_resamples, n, m, *g, true, want_cost);
+    if (bp.max_blocks > INT32_MAX) return KVR_E_SIZE;
     if (d_ws == nullptr) {
         *ws_bytes = bp.total;
         return KVR_OK;

@@ -194,6 +194,14 @@ def test_bootstrap_and_select_errors(lib):
     assert boot(n=0) == kvr.KVR_E_SIZE
     assert boot(R=1 << 30, m=1 << 11) == kvr.KVR_E_SIZE
     assert boot() == kvr.KVR_OK and sz.value > 0
+    # 2^26 one-draw rows of an 8,192-policy grid: 2^33 waves, more than a launch holds
+    big = kvr.PolicyGrid(list(np.arange(32.0)), list(np.geomspace(1.0, 1e5, 256)), [0.5])
+    assert lib.kvr_bootstrap(FAKE, FAKE, 10, FAKE, 1 << 26, 1, ctypes.byref(p),
+                             ctypes.byref(big.c), FAKE, FAKE, None, None, ctypes.byref(sz),
+                             None) == kvr.KVR_E_SIZE
+    assert lib.kvr_bootstrap(FAKE, FAKE, 10, FAKE, 1 << 16, 1, ctypes.byref(p),
+                             ctypes.byref(big.c), FAKE, FAKE, None, None, ctypes.byref(sz),
+                             None) == kvr.KVR_OK
     sel = lib.kvr_select_policy
     assert sel(None, 1, 1, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_NULL
     assert sel(FAKE, 0, 1, 1, 2, 1, FAKE, FAKE, None, None) == kvr.KVR_E_SIZE
