@@ -50,7 +50,10 @@
  *     the word after synchronising the stream.  Outputs of such a call are
  *     meaningless.
  *   - Sizes: 1 <= n <= 2^31 - 1 samples; 1 <= n_t1, n_t2, n_lam;
- *     n_t1 * n_t2 <= 2^24 policies; n_lam <= 4096; n_resamples * m <= 2^40.
+ *     n_t1 * n_t2 <= 2^24 policies; n_lam <= 4096; n_resamples * m <= 2^40;
+ *     n_resamples * n_lam <= 2^31 - 1; and every launch of the brute-force
+ *     plan fits 2^31 - 1 workgroups (about n_resamples * n_t1 * n_t2 / 64
+ *     for the grid kernel).  Beyond these: KVR_E_SIZE.
  */
 #ifndef KVR_H
 #define KVR_H
