@@ -250,7 +250,15 @@ __global__ void __launch_bounds__(256) reduce_splits_kernel(int64_t nsplit, int6
     const int64_t gid = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     if (gid >= slice) return;
     double s = partials[gid];
-    for (int64_t q = 1; q < nsplit; ++q) s += partials[q * slice + gid];
+    int64_t q = 1;
+    for (; q + 8 <= nsplit; q += 8) {   // eight loads in flight, added in split order
+        double v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = partials[(q + u) * slice + gid];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s += v[u];
+    }
+    for (; q < nsplit; ++q) s += partials[q * slice + gid];
     partials[gid] = s;
 }
 
