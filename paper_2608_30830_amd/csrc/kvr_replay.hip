@@ -242,12 +242,14 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_expiry_kernel(
     }
 }
 
-// Bits [lo, hi) of a word, 0 <= lo <= 32; zero when hi <= lo (lo = 32 only
-// happens then, so its masked shift never matters).
+// Bits [lo, hi) of a word, 0 <= lo <= 32; zero when hi <= lo.  The width
+// min(hi, 32) - lo is at most 32, so the mask is formed in 64 bits without a
+// special case for a full word.
 __device__ __forceinline__ uint32_t bit_range(int lo, int hi)
 {
-    const uint32_t upto = (hi >= 32) ? 0xffffffffu : ((1u << (hi < 0 ? 0 : hi)) - 1u);
-    return (hi > lo) ? (upto & ~((1u << (lo & 31)) - 1u)) : 0u;
+    int w = (hi < 32 ? hi : 32) - lo;
+    w = w > 0 ? w : 0;
+    return (uint32_t)((((uint64_t)1 << w) - 1u) << lo);
 }
 
 // Set bits of a lane's column in [from, to) beyond the first word (the rare
