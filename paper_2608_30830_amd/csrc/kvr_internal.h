@@ -133,6 +133,7 @@ struct SortWs {
     int64_t *blkN;        // [nblocks_scan]
     double *blkS;         // [nblocks_scan]
     int nblocks;          // sort tiles
+    int kpt;              // keys per thread of a sort tile (tile = 256 * kpt keys)
     int nblocks_scan;     // scan tiles
 };
 

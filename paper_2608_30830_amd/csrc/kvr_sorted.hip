@@ -31,9 +31,16 @@ constexpr int kScanTile = kScanThreads * kScanIPT;
 static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
+// Keys per thread of the multi-block sort: the largest tile (256 * kpt keys,
+// kpt = 2, 4 or 8) that still gives about one block per CU, since below that
+// each pass is bound by the length of a block's chain (measured on MI355X:
+// 65,536 keys 0.150 ms with kpt = 2 against 0.203 ms with 8; 2^20 keys
+// 0.31 ms with 8 against 0.41 ms with 2).
+static int sort_kpt(int64_t n) { return n >= (int64_t(1) << 19) ? 8 : n >= (int64_t(1) << 18) ? 4 : 2; }
+
 size_t sort_ws_bytes(int64_t n)
 {
-    const int64_t nb = cdiv(n, kSortTile), ns = cdiv(n, kScanTile);
+    const int64_t nb = cdiv(n, kSortThreads * sort_kpt(n)), ns = cdiv(n, kScanTile);
     size_t b = 0;
     b += 2 * align256(sizeof(uint64_t) * n);
     b += 2 * align256(sizeof(int32_t) * n);
@@ -49,7 +56,8 @@ size_t sort_ws_bytes(int64_t n)
 void sort_ws_carve(void *base, int64_t n, SortWs &ws)
 {
     char *p = static_cast<char *>(base);
-    ws.nblocks = (int)cdiv(n, kSortTile);
+    ws.kpt = sort_kpt(n);
+    ws.nblocks = (int)cdiv(n, kSortThreads * ws.kpt);
     ws.nblocks_scan = (int)cdiv(n, kScanTile);
     auto take = [&](size_t bytes) {
         char *q = p;
@@ -87,7 +95,9 @@ __global__ void __launch_bounds__(256) sort_prep_kernel(const double *__restrict
     vals[i] = (int32_t)i;
 }
 
-// Per-tile digit histogram, digit-major: hist[d * nblocks + tile].
+// Per-tile digit histogram (tiles of 256 * KPT keys), digit-major:
+// hist[d * nblocks + tile].
+template <int KPT>
 __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t *__restrict__ keys,
                                                                  int64_t n, int shift,
                                                                  uint32_t *__restrict__ hist,
@@ -96,8 +106,8 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t 
     __shared__ uint32_t h[256];
     h[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kSortTile;
-    for (int q = 0; q < kSortKPT; ++q) {
+    const int64_t base = (int64_t)blockIdx.x * (kSortThreads * KPT);
+    for (int q = 0; q < KPT; ++q) {
         const int64_t i = base + q * kSortThreads + threadIdx.x;
         if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
     }
@@ -154,6 +164,7 @@ __device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
 // digit_scan_kernel) + (keys with its digit earlier in this tile).  The tile
 // is first reordered by digit in LDS, then written out in that order, so
 // consecutive threads store consecutive addresses within each digit's run.
+template <int KPT>
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int64_t n, int shift,
     const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
@@ -163,8 +174,9 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     __shared__ uint32_t wofs[4][256];
     __shared__ uint32_t dbase[256];
     __shared__ uint32_t tstart[256];                 // first tile position of each digit
-    __shared__ uint64_t lkey[kSortTile];
-    __shared__ int32_t lval[kSortTile];
+    constexpr int kTile = kSortThreads * KPT, kWaveK = kWave * KPT;
+    __shared__ uint64_t lkey[kTile];
+    __shared__ int32_t lval[kTile];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
 #pragma unroll
     for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
@@ -174,12 +186,12 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     }
     __syncthreads();
 
-    const int64_t base = (int64_t)blockIdx.x * kSortTile + (int64_t)wave * kWaveKeys;
-    uint64_t key[kSortKPT];
-    int32_t val[kSortKPT];
-    uint32_t local[kSortKPT];
+    const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)wave * kWaveK;
+    uint64_t key[KPT];
+    int32_t val[KPT];
+    uint32_t local[KPT];
 #pragma unroll
-    for (int j = 0; j < kSortKPT; ++j) {
+    for (int j = 0; j < KPT; ++j) {
         const int64_t i = base + j * kWave + lane;
         const bool valid = i < n;
         key[j] = valid ? keys_in[i] : 0;
@@ -214,23 +226,23 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     __syncthreads();
     // tile positions are dense: the valid keys of the tile fill [0, nvalid)
 #pragma unroll
-    for (int j = 0; j < kSortKPT; ++j) {
+    for (int j = 0; j < KPT; ++j) {
         const int64_t i = base + j * kWave + lane;
         if (i < n) {
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
             const uint32_t pos = tstart[d] + wofs[wave][d] + local[j];
-            if (pos < (uint32_t)kSortTile) {           // always true; never write outside
+            if (pos < (uint32_t)kTile) {           // always true; never write outside
                 lkey[pos] = key[j];
                 lval[pos] = val[j];
             }
         }
     }
     __syncthreads();
-    const int64_t tile0 = (int64_t)blockIdx.x * kSortTile;
+    const int64_t tile0 = (int64_t)blockIdx.x * kTile;
     const int64_t left = n - tile0;
-    const int nvalid = left < kSortTile ? (int)left : kSortTile;
+    const int nvalid = left < kTile ? (int)left : kTile;
 #pragma unroll
-    for (int q = 0; q < kSortKPT; ++q) {
+    for (int q = 0; q < KPT; ++q) {
         const int pos = q * kSortThreads + (int)threadIdx.x;
         if (pos < nvalid) {
             const uint64_t k = lkey[pos];
@@ -609,13 +621,29 @@ hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs
     int cur = 0;
     for (int pass = 0; pass < 8; ++pass) {
         const int shift = 8 * pass;
-        hipLaunchKernelGGL(sort_hist_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                           ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+        if (ws.kpt == 8)
+            hipLaunchKernelGGL(sort_hist_kernel<8>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
+                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+        else if (ws.kpt == 4)
+            hipLaunchKernelGGL(sort_hist_kernel<4>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
+                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+        else
+            hipLaunchKernelGGL(sort_hist_kernel<2>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
+                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
         hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(256), 0, stream, ws.hist, ws.nblocks,
                            ws.counts);
-        hipLaunchKernelGGL(sort_scatter_kernel, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                           ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts, ws.nblocks,
-                           ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        if (ws.kpt == 8)
+            hipLaunchKernelGGL(sort_scatter_kernel<8>, dim3(ws.nblocks), dim3(kSortThreads), 0,
+                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
+                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        else if (ws.kpt == 4)
+            hipLaunchKernelGGL(sort_scatter_kernel<4>, dim3(ws.nblocks), dim3(kSortThreads), 0,
+                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
+                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        else
+            hipLaunchKernelGGL(sort_scatter_kernel<2>, dim3(ws.nblocks), dim3(kSortThreads), 0,
+                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
+                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
         if ((err = hipGetLastError()) != hipSuccess) return err;
         cur ^= 1;
     }

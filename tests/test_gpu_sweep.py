@@ -68,11 +68,13 @@ def test_grid_shapes(kvr, oracle_mod, case):
             assert_costs(_np(bc)[r], rbc)
 
 
-@pytest.mark.parametrize("n", [2047, 2048, 2049, 4096, 4097])
+@pytest.mark.parametrize("n", [2047, 2048, 2049, 4096, 4097, 262143, 262144, 300001, 524288])
 def test_sort_path_boundaries(kvr, oracle_mod, n):
-    """Sample sizes around the one-block sort (at most 2,048 waits) and the
-    2,048-key tiles of the multi-block sort: the SORTED grid and its order
-    against the oracle, and the factored bootstrap, which sorts the same way."""
+    """Sample sizes around the one-block sort (at most 2,048 waits), around the
+    tile sizes of the multi-block sort (512-key tiles below 2^18 waits, 1,024
+    below 2^19, 2,048 from there) and a ragged last tile: the SORTED grid and
+    its order against the oracle, and the factored bootstrap, which sorts the
+    same way."""
     wl = workloads.random_case(7000 + n, n, 2, 70, 5, resamples=2, m=n, ties=True)
     pr = oracle_mod.workload_prices(wl)
     lp = _lib_prices(kvr, wl)
