@@ -32,6 +32,7 @@ if ROOT not in sys.path:
     sys.path.insert(0, ROOT)
 
 FP64_PEAK_TFLOPS = 78.6
+HBM_PEAK_TBS = 8.0
 GRID_SOURCES = ("paper_2608_30830_amd/csrc/kvr_grid.hip",
                 "paper_2608_30830_amd/csrc/kvr_device.h",
                 "paper_2608_30830_amd/csrc/kvr_internal.h")
@@ -126,6 +127,8 @@ def main() -> int:
     ap.add_argument("--replay-only", action="store_true",
                     help="time only the admission replay and the controller, then exit")
     ap.add_argument("--replay-reps", type=int, default=8192)
+    ap.add_argument("--sort-scale", action="store_true",
+                    help="time the SORTED path on 2^20, 2^22 and 2^24 waits, then exit")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
@@ -144,6 +147,10 @@ def main() -> int:
 
     if args.table:
         print(json.dumps({"table": results_table(kvr, workloads, torch)}), flush=True)
+        return 0
+
+    if args.sort_scale:
+        print(json.dumps({"sort_scale": time_sort_scale(kvr, workloads, torch)}), flush=True)
         return 0
 
     if args.replay_only:
@@ -276,6 +283,46 @@ def time_paths(kvr, workloads, torch):
         log(f"[bench] path {key}: {ms:.3f} ms")
     res.update(time_platforms(kvr, workloads, torch))
     res.update(time_replay(kvr, workloads, torch))
+    return res
+
+
+# Algorithmic bytes per key of the SORTED path: eight digit passes, each an
+# 8-byte histogram read, a 12-byte scatter read (key and payload) and a 12-byte
+# write; key preparation (12 B read, 12 B written); the prefix scans (12 B read
+# twice, 16 B written).
+SORT_BYTES_PER_KEY = 8 * (8 + 12 + 12) + 24 + 40
+
+
+def time_sort_scale(kvr, workloads, torch):
+    """Median milliseconds per SORTED kvr_cost_grid call at 2^20, 2^22 and
+    2^24 waits and the algorithmic bytes per second that implies."""
+    res = {}
+    for lg in (20, 22, 24):
+        wl = workloads.sort_scale_case(lg)
+        pf = wl.platform
+        pr = kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
+                                          pf["host_link_bytes_per_s"],
+                                          pf["prefill_tokens_per_s"])
+        g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+        w = torch.as_tensor(wl.wait_s).cuda()
+        T = torch.as_tensor(wl.ctx_tokens).cuda()
+        out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
+                          device="cuda")
+        kvr.kvr_cost_grid(w, T, pr, g, method=kvr.KVR_SORTED, out=out)
+        torch.cuda.synchronize()
+        times = []
+        for _ in range(9):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            kvr.kvr_cost_grid(w, T, pr, g, method=kvr.KVR_SORTED, out=out, check=False)
+            b.record()
+            torch.cuda.synchronize()
+            times.append(a.elapsed_time(b))
+        ms = sorted(times)[len(times) // 2]
+        bps = SORT_BYTES_PER_KEY * wl.n / (ms * 1e-3)
+        res[wl.name] = {"ms": ms, "keys_per_s": wl.n / (ms * 1e-3), "algorithmic_bytes_per_s": bps,
+                        "hbm_frac": bps / (HBM_PEAK_TBS * 1e12)}
+        log(f"[bench] sorted {wl.name}: {ms:.3f} ms, {bps / 1e12:.2f} TB/s algorithmic")
     return res
 
 

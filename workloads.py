@@ -168,6 +168,21 @@ def make(name: str, resamples: Optional[int] = None) -> Workload:
     raise KeyError(f"unknown workload {name!r}; known: {NAMES}")
 
 
+def sort_scale_case(log2n: int) -> Workload:
+    """A large single sample for the sorted path's scaling: 2^log2n waits from
+    the weibull-1m law (truncated Weibull(0.5, 1,800 s)) and its context law,
+    with a small policy grid (t1 = 0, 64 log-spaced host timers 1 s - 24 h
+    plus infinity, 4 loads) so that the sort and the scans dominate."""
+    rw, rt, _ = _streams(1100 + log2n)
+    n = 1 << log2n
+    w = truncated_weibull_waits(rw, n)
+    z = rt.standard_normal(n)
+    t = np.clip(np.rint(16384.0 * np.exp(0.7 * z)), 1024, 131072).astype(np.int32)
+    return Workload(f"sort-scale-2^{log2n}", w, t, np.array([0.0]),
+                    _with_inf(np.geomspace(1.0, 86400.0, 64)),
+                    np.array([0.25, 0.5, 0.75, 1.0]), float(KV_320K))
+
+
 FAMILIES = ("lognormal", "exponential", "mixture")
 
 
