@@ -142,3 +142,28 @@ def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
         rb, rbc, _ = oracle_mod.select(ref, wl.t2)
         assert_selection(ref, _np(best)[r], rb)
         assert_costs(_np(bc)[r], rbc)
+
+
+@pytest.mark.parametrize("name", sorted(__import__("tests.test_gpu_parity",
+                                                   fromlist=["DEGENERATE"]).DEGENERATE))
+def test_factored_degenerate_inputs(kvr, oracle_mod, name):
+    """The grid's degenerate cases (every wait zero, waits on deadlines, retain
+    only, no congestion, one sample, repeated deadlines, t1 + t2 overflowing to
+    +inf, one host timer) through the factored method, with an identity row
+    and a seeded row: costs and selections against the oracle."""
+    from tests.test_gpu_parity import DEGENERATE
+    w, T, t1, t2, lam = DEGENERATE[name]
+    n = w.size
+    rng = np.random.Generator(np.random.PCG64(300 + n))
+    idx = np.stack([np.arange(n, dtype=np.int32), rng.integers(0, n, n, dtype=np.int32)])
+    wl = workloads.Workload(name, w.astype(np.float64), T, t1, t2, lam,
+                            float(workloads.KV_128K), idx=idx)
+    best, bc, cost = _factored(kvr, wl, want_cost=True)
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(2):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref, _np(best)[r], rb)
+        assert_costs(_np(bc)[r], rbc)
