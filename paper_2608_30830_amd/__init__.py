@@ -167,10 +167,17 @@ def _need(t, dtype, name):
         raise ValueError(f"{name} must be a contiguous {dtype} CUDA tensor")
 
 
+def _need_shape(t, shape, name):
+    if tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, not {tuple(t.shape)}")
+
+
 def _workspace(nbytes: int, ws=None):
     torch = _torch()
-    if ws is not None and ws.numel() >= nbytes:
-        return ws
+    if ws is not None:
+        _need(ws, torch.uint8, "workspace")
+        if ws.numel() >= nbytes:
+            return ws
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
 
 
@@ -183,10 +190,14 @@ def kvr_cost_grid(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid, meth
     _need(wait_s, torch.float64, "wait_s")
     _need(ctx_tokens, torch.int32, "ctx_tokens")
     n = wait_s.numel()
+    _need_shape(ctx_tokens, wait_s.shape, "ctx_tokens")
     need = ctypes.c_size_t(0)
     _check(lib.kvr_cost_grid(None, None, n, ctypes.byref(prices), ctypes.byref(grid.c), method,
                              None, None, None, ctypes.byref(need), None), "kvr_cost_grid(size)")
     ws = _workspace(need.value, workspace)
+    if out is not None:
+        _need(out, torch.float64, "out")
+        _need_shape(out, (grid.n_lam, grid.n_t1, grid.n_t2), "out")
     cost = out if out is not None else torch.empty((grid.n_lam, grid.n_t1, grid.n_t2),
                                                    dtype=torch.float64, device="cuda")
     perm = torch.empty(n, dtype=torch.int32, device="cuda") if want_perm else None
@@ -231,6 +242,7 @@ class BootstrapCall:
         _need(idx, torch.int32, "idx")
         if idx.dim() != 2:
             raise ValueError("idx must be [n_resamples, m]")
+        _need_shape(ctx_tokens, wait_s.shape, "ctx_tokens")
         self.lib = load_library()
         self.name = "kvr_bootstrap_factored" if factored else "kvr_bootstrap"
         self.fn = getattr(self.lib, self.name)
@@ -293,6 +305,8 @@ def kvr_capacity_replay(arrival_s, wait_s, prices: kvr_prices, t2: Sequence[floa
         _need(ctx_tokens, torch.int32, "ctx_tokens")
     if arrival_s.dim() != 2 or tuple(wait_s.shape) != tuple(arrival_s.shape):
         raise ValueError("arrival_s and wait_s must both be [n_reps, n]")
+    if ctx_tokens is not None:
+        _need_shape(ctx_tokens, arrival_s.shape, "ctx_tokens")
     reps, n = arrival_s.shape
     K = len(t2)
     t2c = (ctypes.c_double * K)(*[float(x) for x in t2])

@@ -316,6 +316,37 @@ def test_domain_errors_are_reported(kvr):
     torch.cuda.synchronize()
 
 
+def test_binding_rejects_mismatched_arguments(kvr):
+    """The binding checks what the C ABI cannot see (tensor shapes, dtypes,
+    devices) and raises before anything is launched."""
+    import torch
+    wl = workloads.random_case(304, 500, 1, 9, 3, resamples=2)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    pr = _lib_prices(kvr, wl)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    with pytest.raises(ValueError):
+        kvr.kvr_cost_grid(w, T[:-1], pr, g)                                  # short contexts
+    with pytest.raises(ValueError):
+        kvr.kvr_cost_grid(w, T, pr, g, out=torch.empty((3, 1, 8), dtype=torch.float64,
+                                                        device="cuda"))      # small output
+    with pytest.raises(ValueError):
+        kvr.kvr_cost_grid(w, T, pr, g, out=torch.empty((3, 1, 9), dtype=torch.float32,
+                                                        device="cuda"))      # wrong dtype
+    with pytest.raises(ValueError):
+        kvr.kvr_cost_grid(w, T, pr, g, workspace=torch.empty(1 << 20, dtype=torch.float64,
+                                                              device="cuda"))
+    with pytest.raises(ValueError):
+        kvr.kvr_cost_grid(w.cpu(), T, pr, g)                                 # host tensor
+    with pytest.raises(ValueError):
+        kvr.kvr_bootstrap(w, T[:-1], _dev(wl.idx, _i32()), pr, g)
+    arr = torch.cumsum(torch.ones((2, 50), dtype=torch.float64, device="cuda"), 1)
+    with pytest.raises(ValueError):
+        kvr.kvr_capacity_replay(arr, arr.clone(), pr, [60.0],
+                                ctx_tokens=torch.ones((2, 49), dtype=torch.int32, device="cuda"))
+    cost = kvr.kvr_cost_grid(w, T, pr, g)                                    # a valid call
+    assert tuple(cost.shape) == (3, 1, 9)
+
+
 def test_profile_events_bracket_the_grid_kernel(kvr):
     """kvr_set_profile_events: the library records the caller's events around
     its main kernel on the call's stream."""
