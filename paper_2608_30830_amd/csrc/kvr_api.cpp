@@ -29,14 +29,14 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // Sample splits per resample for the grid kernel (measured on MI355X: 1,024
 // SIMDs, 4 resident grid waves each).  With at least 32K waves already there
 // is no split (the selection is fused into the grid kernel).  Otherwise the
-// samples are cut into splits of >= 4,096 samples, or of >= 512 samples when
+// samples are cut into splits of >= 2,048 samples, or of >= 512 samples when
 // that is what it takes to give every resident slot a wave; never more than
 // 16 rounds of waves, and never more than 1 GiB of split partials.
 int64_t choose_splits(int64_t base_waves, int64_t m, int64_t partial_doubles_per_split)
 {
     constexpr int64_t kSlots = 4096, kFull = 32768, kMaxRounds = 16;
     if (base_waves >= kFull) return 1;
-    int64_t ns = std::max<int64_t>(1, m / 4096);
+    int64_t ns = std::max<int64_t>(1, m / 2048);
     if (base_waves * ns < kSlots)
         ns = std::max<int64_t>(1, std::min<int64_t>(m / 512, cdiv(kSlots, base_waves)));
     ns = std::min<int64_t>(ns, cdiv(kMaxRounds * kSlots, base_waves));
