@@ -44,14 +44,14 @@ def _configure(lib):
     lib.oracle_congestion_prices.argtypes = [P, I32, D, D, D, P]
     lib.oracle_eq3_timer.argtypes = [D, D, D, D, D]
     lib.oracle_eq3_timer.restype = D
-    lib.oracle_cost_grid.argtypes = [P, P, I64, P, I64, D, D, D, D, D,
+    lib.oracle_cost_grid.argtypes = [P, P, I64, P, I64, D, D, D, D, D, D,
                                      P, I32, P, I32, P, I32, P]
     lib.oracle_select.argtypes = [P, I64, I32, I32, I32, P, P, P, P]
     lib.oracle_stable_order.argtypes = [P, I64, P]
-    lib.oracle_closed_form_grid.argtypes = [P, P, I64, P, P, I64, D, D, D, D, D,
+    lib.oracle_closed_form_grid.argtypes = [P, P, I64, P, P, I64, D, D, D, D, D, D,
                                             P, I32, P, I32, P, I32, P]
     lib.oracle_closed_form_bootstrap.argtypes = [P, P, I64, P, I64, I64, D, D, D,
-                                                 D, D, P, I32, P, I32, P, I32,
+                                                 D, D, D, P, I32, P, I32, P, I32,
                                                  P, P]
     lib.oracle_num_threads.restype = ctypes.c_int
     lib.oracle_set_num_threads.argtypes = [ctypes.c_int]
@@ -91,30 +91,36 @@ def _i32(a):
 
 
 class Prices:
-    """Per-token price vector plus host capacity and reference wait."""
+    """Per-token price vector plus host capacity and reference wait.  boff is
+    the optional per-token charge for the device-to-host copy at offload (0:
+    uncharged, the paper's model)."""
 
-    def __init__(self, a1, b2, b3, c2=425.0, w_ref=1800.0):
+    def __init__(self, a1, b2, b3, c2=425.0, w_ref=1800.0, boff=0.0):
         self.a1, self.b2, self.b3 = float(a1), float(b2), float(b3)
-        self.c2, self.w_ref = float(c2), float(w_ref)
+        self.c2, self.w_ref, self.boff = float(c2), float(w_ref), float(boff)
 
     def tuple(self):
-        return (self.a1, self.b2, self.b3, self.c2, self.w_ref)
+        return (self.a1, self.b2, self.b3, self.boff, self.c2, self.w_ref)
 
     def __repr__(self):
-        return f"Prices(a1={self.a1!r}, b2={self.b2!r}, b3={self.b3!r}, c2={self.c2!r}, w_ref={self.w_ref!r})"
+        return (f"Prices(a1={self.a1!r}, b2={self.b2!r}, b3={self.b3!r}, c2={self.c2!r}, "
+                f"w_ref={self.w_ref!r}, boff={self.boff!r})")
 
 
 def prices_from_platform(kv_bytes_per_token, hbm_usable_bytes, host_link_bytes_per_s,
                          prefill_tokens_per_s, n_gpu=1.0, host_slots_c2=425.0,
-                         w_ref_s=1800.0) -> Prices:
-    """Appendix B price vector, per token."""
+                         w_ref_s=1800.0, charge_offload=False) -> Prices:
+    """Appendix B price vector, per token.  With charge_offload the offload
+    copy is charged at the restore's per-token time (the host link has the
+    same bandwidth each way)."""
     lib = _load()
     a1, b2, b3 = ctypes.c_double(), ctypes.c_double(), ctypes.c_double()
     lib.oracle_prices_from_platform(float(kv_bytes_per_token), float(hbm_usable_bytes),
                                     float(host_link_bytes_per_s), float(prefill_tokens_per_s),
                                     float(n_gpu), ctypes.byref(a1), ctypes.byref(b2),
                                     ctypes.byref(b3))
-    return Prices(a1.value, b2.value, b3.value, host_slots_c2, w_ref_s)
+    return Prices(a1.value, b2.value, b3.value, host_slots_c2, w_ref_s,
+                  b2.value if charge_offload else 0.0)
 
 
 def workload_prices(wl) -> Prices:

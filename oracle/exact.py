@@ -7,7 +7,9 @@ in ``fractions.Fraction`` arithmetic (every float input is converted exactly):
   T * a1 per second, no resume cost (Section 3.1, Eq. 1, beta_1 = 0);
 * at t1, if the request has not resumed, the copy moves to host DRAM
   (state 2), holding price T * a2(lambda) per second, where
-  a2 = max(0, lambda - C2/W_ref) * b3 / C2 (Section 3.3, Eq. 3);
+  a2 = max(0, lambda - C2/W_ref) * b3 / C2 (Section 3.3, Eq. 3); the move
+  itself costs boff * T (zero in the paper's model, which leaves the copy
+  uncharged; a positive boff is the optional offload charge);
 * the one-shot host timer fires at the deadline e (Appendix D); e is the
   deadline the controller actually arms, the binary64 value of t1 + t2;
   if the request is still suspended the host copy is discarded (state 3,
@@ -31,7 +33,8 @@ def _fr(x: float) -> Fraction:
 
 
 def _request_cost(w: Fraction, T: int, t1: Fraction, e, a1: Fraction,
-                  a2: Fraction, b2: Fraction, b3: Fraction) -> Fraction:
+                  a2: Fraction, b2: Fraction, b3: Fraction,
+                  boff: Fraction = Fraction(0)) -> Fraction:
     """Walk one request's timeline.  ``e`` is a Fraction or None (no timer)."""
     # events after suspension, in time order: offload at t1, expiry at e, resume at w
     events = [(t1, 1, "offload")]
@@ -49,6 +52,7 @@ def _request_cost(w: Fraction, T: int, t1: Fraction, e, a1: Fraction,
             return total
         if kind == "offload" and state == "hbm":
             state = "host"
+            total += boff * T
         elif kind == "expire" and state == "host":
             state = "gone"
     raise AssertionError("unreachable: every request resumes")
@@ -65,6 +69,7 @@ def cost_grid(wait_s: Sequence[float], ctx: Sequence[int], prices, t1: Sequence[
               t2: Sequence[float], lam: Sequence[float], idx_row=None) -> List[List[List[Fraction]]]:
     """Exact mean cost[l][a][k] as Fractions."""
     a1, b2, b3 = _fr(prices.a1), _fr(prices.b2), _fr(prices.b3)
+    boff = _fr(getattr(prices, "boff", 0.0))
     rows = list(range(len(wait_s))) if idx_row is None else [int(i) for i in idx_row]
     m = len(rows)
     out = []
@@ -78,7 +83,8 @@ def cost_grid(wait_s: Sequence[float], ctx: Sequence[int], prices, t1: Sequence[
                 e = None if math.isinf(tk) else _fr(float(ta) + float(tk))
                 tot = Fraction(0)
                 for i in rows:
-                    tot += _request_cost(_fr(wait_s[i]), int(ctx[i]), t1f, e, a1, a2, b2, b3)
+                    tot += _request_cost(_fr(wait_s[i]), int(ctx[i]), t1f, e, a1, a2, b2, b3,
+                                         boff)
                 per_k.append(tot / m)
             per_a.append(per_k)
         out.append(per_a)

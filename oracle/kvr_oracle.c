@@ -29,7 +29,11 @@
  *   still in HBM (w <= t1) pays nothing.  t2 = +inf is host-retain.
  *
  *   Per sample:  c = T * ( a1*min(w,t1)
- *                          + [w > t1] * ( a2*(min(w,e) - t1) + (w <= e ? b2 : b3) ) )
+ *                          + [w > t1] * ( a2*(min(w,e) - t1) + (w <= e ? b2 : b3) + boff ) )
+ *   boff is an optional per-token charge for the device-to-host copy made at
+ *   offload.  The paper leaves that copy uncharged (Section 3.2: transfer time
+ *   overlaps GPU work; Eq. 1 has resume costs only), so boff = 0 is the
+ *   paper's model; a positive boff charges it once per offloaded request.
  *   Per policy (t1_a, t2_k, lambda_l): mean of c over the sample (GPU-s per
  *   request, the unit of Table 6), summed with Neumaier compensation.
  *   Selection (Section 3.4, the calibration replay freezes the cheaper
@@ -97,7 +101,7 @@ double oracle_eq3_timer(double lam, double b2, double b3, double c2, double w_re
 /* The per-sample cost written out state by state (Eq. 1 summed over the
  * states visited, Appendix D one-shot timer semantics). */
 static double sample_cost(double w, double T, double t1, double e,
-                          double a1, double a2, double b2, double b3)
+                          double a1, double a2, double b2, double b3, double boff)
 {
     double hbm_time = (w < t1) ? w : t1;          /* seconds in HBM        */
     double cost = a1 * hbm_time;                   /* alpha_1 * l, beta_1=0 */
@@ -105,7 +109,7 @@ static double sample_cost(double w, double T, double t1, double e,
         double host_end = (w < e) ? w : e;         /* resume or deadline    */
         double host = a2 * (host_end - t1);        /* alpha_2(lambda) * l   */
         double resume = (w <= e) ? b2 : b3;        /* restore or recompute  */
-        cost = cost + (host + resume);
+        cost = cost + (host + resume + boff);      /* boff: the offload copy */
     }
     return T * cost;
 }
@@ -130,7 +134,7 @@ static inline double nsum_get(const nsum *a) { return a->s + a->c; }
  */
 void oracle_cost_grid(const double *wait_s, const int32_t *ctx, int64_t n,
                       const int32_t *idx, int64_t m,
-                      double a1, double b2, double b3, double c2, double w_ref,
+                      double a1, double b2, double b3, double boff, double c2, double w_ref,
                       const double *t1, int32_t n_t1,
                       const double *t2, int32_t n_t2,
                       const double *lam, int32_t n_lam,
@@ -150,7 +154,7 @@ void oracle_cost_grid(const double *wait_s, const int32_t *ctx, int64_t n,
         for (int64_t j = 0; j < m; ++j) {
             int64_t i = idx ? (int64_t)idx[j] : j;
             nsum_add(&acc, sample_cost(wait_s[i], (double)ctx[i], t1[a], e,
-                                       a1, a2[l], b2, b3));
+                                       a1, a2[l], b2, b3, boff));
         }
         cost_out[p] = nsum_get(&acc) / (double)m;
     }
@@ -226,7 +230,7 @@ static int64_t upper_bound(const double *sw, int64_t n, double x)
  *   Ttot = N(inf),
  *   m*C = a1*[S(t1) + t1*(Ttot - N(t1))]
  *       + a2*[(S(e) - S(t1)) - t1*(N(e) - N(t1)) + (e - t1)*(Ttot - N(e))]
- *       + b2*(N(e) - N(t1)) + b3*(Ttot - N(e)),
+ *       + b2*(N(e) - N(t1)) + b3*(Ttot - N(e)) + boff*(Ttot - N(t1)),
  * where the (e - t1)*(Ttot - N(e)) term is dropped when e = +inf (no sample
  * lies past an infinite deadline).  Integer sums N are exact in int64.
  *
@@ -236,8 +240,8 @@ static int64_t upper_bound(const double *sw, int64_t n, double x)
  */
 void oracle_closed_form_grid(const double *wait_s, const int32_t *ctx, int64_t n,
                              const int32_t *perm, const int32_t *idx, int64_t m,
-                             double a1, double b2, double b3, double c2, double w_ref,
-                             const double *t1, int32_t n_t1,
+                             double a1, double b2, double b3, double boff, double c2,
+                             double w_ref, const double *t1, int32_t n_t1,
                              const double *t2, int32_t n_t2,
                              const double *lam, int32_t n_lam,
                              double *cost_out)
@@ -269,7 +273,7 @@ void oracle_closed_form_grid(const double *wait_s, const int32_t *ctx, int64_t n
             double Ne = (double)N[pe], Se = S[pe];
             double hold = (Se - S1) - t1[a] * (Ne - N1);
             if (!isinf(e)) hold = hold + (e - t1[a]) * (Ttot - Ne);
-            double fixed = a1 * hbm + b2 * (Ne - N1) + b3 * (Ttot - Ne);
+            double fixed = a1 * hbm + b2 * (Ne - N1) + b3 * (Ttot - Ne) + boff * (Ttot - N1);
             for (int32_t l = 0; l < n_lam; ++l)
                 cost_out[((int64_t)l * n_t1 + a) * n_t2 + k] =
                     (fixed + a2[l] * hold) / (double)m;
@@ -282,8 +286,8 @@ void oracle_closed_form_grid(const double *wait_s, const int32_t *ctx, int64_t n
  * large batch): best[R][n_lam], best_cost[R][n_lam]. */
 void oracle_closed_form_bootstrap(const double *wait_s, const int32_t *ctx, int64_t n,
                                   const int32_t *idx, int64_t n_rows, int64_t m,
-                                  double a1, double b2, double b3, double c2, double w_ref,
-                                  const double *t1, int32_t n_t1,
+                                  double a1, double b2, double b3, double boff, double c2,
+                                  double w_ref, const double *t1, int32_t n_t1,
                                   const double *t2, int32_t n_t2,
                                   const double *lam, int32_t n_lam,
                                   int32_t *best, double *best_cost)
@@ -294,8 +298,8 @@ void oracle_closed_form_bootstrap(const double *wait_s, const int32_t *ctx, int6
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t r = 0; r < n_rows; ++r) {
         double *cost = (double *)malloc(sizeof(double) * (size_t)(P * n_lam));
-        oracle_closed_form_grid(wait_s, ctx, n, perm, idx + r * m, m, a1, b2, b3, c2,
-                                w_ref, t1, n_t1, t2, n_t2, lam, n_lam, cost);
+        oracle_closed_form_grid(wait_s, ctx, n, perm, idx + r * m, m, a1, b2, b3, boff,
+                                c2, w_ref, t1, n_t1, t2, n_t2, lam, n_lam, cost);
         oracle_select(cost, 1, n_lam, n_t1, n_t2, t2, best + r * n_lam,
                       best_cost + r * n_lam, NULL);
         free(cost);

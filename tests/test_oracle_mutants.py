@@ -31,21 +31,24 @@ MUTANTS = {
     "tie_to_smaller": ("if (row[f] <= bc)", "if (row[f] < bc)"),
     "deadline_from_zero": ("double e = t1[a] + t2[k];\n        nsum acc", "double e = t2[k];\n        nsum acc"),
     "divide_by_n": ("cost_out[p] = nsum_get(&acc) / (double)m;", "cost_out[p] = nsum_get(&acc) / (double)(m + 1);"),
+    "offload_charge_dropped": ("(host + resume + boff)", "(host + resume)"),
+    "offload_charge_in_hbm": ("double cost = a1 * hbm_time;", "double cost = a1 * hbm_time + boff;"),
 }
 
 
 def _pins_pass(mod):
     """The exact-simulation cases, a two-tier bootstrap case, and the
     uncongested expectation pin; returns False at the first failure."""
-    pr = mod.Prices(0.0524288, 0.0262144, 5e-5, 425.0, 1800.0)
-    for (w, T, t1, t2, lam) in _tiny_cases():
-        got = mod.cost_grid(w, T, pr, t1, t2, lam)
-        ex = np.array(exact.cost_grid(w, T, pr, t1, t2, lam), dtype=float)
-        if not np.allclose(got, ex, rtol=4 * len(w) * H.EPS, atol=0):
-            return False
-        if list(np.atleast_1d(mod.select(got, t2)[0])) != exact.select(
-                exact.cost_grid(w, T, pr, t1, t2, lam)):
-            return False
+    for pr in (mod.Prices(0.0524288, 0.0262144, 5e-5, 425.0, 1800.0),
+               mod.Prices(0.0524288, 0.0262144, 5e-5, 425.0, 1800.0, boff=0.0131072)):
+        for (w, T, t1, t2, lam) in _tiny_cases():
+            got = mod.cost_grid(w, T, pr, t1, t2, lam)
+            ex = np.array(exact.cost_grid(w, T, pr, t1, t2, lam), dtype=float)
+            if not np.allclose(got, ex, rtol=4 * len(w) * H.EPS, atol=0):
+                return False
+            if list(np.atleast_1d(mod.select(got, t2)[0])) != exact.select(
+                    exact.cost_grid(w, T, pr, t1, t2, lam)):
+                return False
     w = H.stratified_family("exponential", 20000)
     c = mod.cost_grid(w, np.ones(w.size, np.int32), mod.Prices(0.0176, 0.02, 1.91),
                       np.array([0.0]), np.array([600.0, np.inf]), np.array([0.1]))

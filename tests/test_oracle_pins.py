@@ -335,6 +335,71 @@ def test_p10_identity_resample_and_permutation(oracle_mod):
                   1e-13)
 
 
+# ------------------------------------------------------ offload charge --
+# The paper leaves the device-to-host copy at offload uncharged (Section 3.2:
+# transfer time overlaps GPU execution; Eq. 1 prices resumes only).  The
+# optional charge boff * T is paid once by every request that leaves HBM,
+# i.e. exactly when w > t1.
+
+def _offload_prices(oracle_mod):
+    pr = oracle_mod.workload_prices(workloads.make("tiny-exp-1k"))
+    return oracle_mod.Prices(pr.a1 * 100, pr.b2 * 10, pr.b3, 425.0, 1800.0, boff=pr.b2 * 7)
+
+
+@pytest.mark.parametrize("case", range(12))
+def test_offload_charge_exact_event_simulation(oracle_mod, case):
+    """With the offload charge on, the oracle still agrees with the exact
+    rational simulation, which charges it at the offload event of each
+    timeline (never when the request resumes at or before t1)."""
+    w, T, t1, t2, lam = _tiny_cases()[case]
+    pr = _offload_prices(oracle_mod)
+    got = oracle_mod.cost_grid(w, T, pr, t1, t2, lam)
+    ex = exact.cost_grid(w, T, pr, t1, t2, lam)
+    np.testing.assert_allclose(got, np.array(ex, dtype=float), rtol=4 * len(w) * H.EPS, atol=0)
+    assert list(oracle_mod.select(got, t2)[0]) == exact.select(ex)
+
+
+def test_offload_charge_is_the_offloaded_token_mass(oracle_mod):
+    """Switching the charge on adds boff times the mean offloaded tokens,
+    (1/m) sum of T over w > t1, to every policy with that t1, whatever t2
+    and the load; a wait equal to t1 is not offloaded."""
+    w = np.array([0.0, 5.0, 5.0, 30.0, 400.0, 2000.0, 9000.0])
+    T = np.array([3, 11, 7, 5, 13, 2, 17], np.int32)
+    t1, t2, lam = np.array([0.0, 5.0, 400.0]), np.array([10.0, 600.0, np.inf]), np.array([0.1, 1.7])
+    on = _offload_prices(oracle_mod)
+    off = oracle_mod.Prices(on.a1, on.b2, on.b3, on.c2, on.w_ref)
+    diff = oracle_mod.cost_grid(w, T, on, t1, t2, lam) - oracle_mod.cost_grid(w, T, off, t1, t2, lam)
+    mass = {0.0: 3 + 11 + 7 + 5 + 13 + 2 + 17 - 3, 5.0: 5 + 13 + 2 + 17, 400.0: 2 + 17}
+    for a, ta in enumerate(t1):
+        want = on.boff * mass[ta] / w.size
+        np.testing.assert_allclose(diff[:, a, :], want, rtol=1e-12)
+
+
+def test_offload_charge_closed_form(oracle_mod):
+    """The closed form's offload term (boff times the tokens past t1) agrees
+    with the double loop, bootstrap rows included."""
+    wl = workloads.random_case(21, 2500, 3, 20, 4, resamples=2, ties=True)
+    base = oracle_mod.workload_prices(wl)
+    pr = oracle_mod.Prices(base.a1, base.b2, base.b3, base.c2, base.w_ref, boff=base.b2)
+    for row in [None] + list(wl.idx):
+        a = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam, idx_row=row)
+        b = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                        idx_row=row)
+        assert np.max(H.rel_err(b, a)) <= 8 * wl.m * H.EPS
+
+
+def test_offload_charge_default_and_link_rate(oracle_mod):
+    """Off by default (the paper's model).  Switched on, it is charged at the
+    restore's per-token time: Appendix B measures the copy in both directions
+    at the same rate (0.0480 s down, 0.0478 s up for 2.75 GB)."""
+    assert abs(0.0480 / 0.0478 - 1.0) < 0.005
+    pf = workloads.PLATFORM
+    args = (131072, pf["hbm_usable_bytes"], pf["host_link_bytes_per_s"], pf["prefill_tokens_per_s"])
+    assert oracle_mod.prices_from_platform(*args).boff == 0.0
+    pr = oracle_mod.prices_from_platform(*args, charge_offload=True)
+    assert pr.boff == pr.b2
+
+
 # ------------------------------------------------------------------- sort --
 def test_stable_order_matches_library_sort(oracle_mod):
     rng = np.random.Generator(np.random.PCG64(9))
