@@ -81,13 +81,27 @@ enum { KVR_BRUTE = 0, KVR_SORTED = 1 };   /* kvr_cost_grid methods            */
 enum { KVR_RETAIN = 0, KVR_EXPIRE = 1 };  /* branch codes of kvr_select_policy */
 
 /* Price vector per token (Appendix B) plus the host-tier constants of
- * Section 3.3.  Every field must be finite and > 0. */
+ * Section 3.3.  The first five fields must be finite and > 0;
+ * offload_per_token must be finite and >= 0 (anything else is KVR_E_PRICE).
+ *
+ * offload_per_token is an optional charge for the device-to-host copy made
+ * when a context leaves HBM at t1: each request with w > t1 pays
+ * T * offload_per_token once.  The paper leaves that copy uncharged (Section
+ * 3.2: transfer time overlaps GPU execution; Eq. 1 prices resumes only), so
+ * 0, what kvr_prices_from_platform writes, is the paper's model.  The grid
+ * entry points (kvr_cost_grid, kvr_bootstrap, kvr_bootstrap_factored) add
+ * it; kvr_eq3_timer and kvr_crossover_statistic do not depend on it (it is
+ * paid before the host timer starts, and t* compares HBM holding with
+ * recompute); the finite-capacity replay entry points (kvr_capacity_replay,
+ * kvr_controller_select) model Table 6 without it and return KVR_E_METHOD
+ * when it is not 0. */
 typedef struct {
-    double a1_per_token;   /* alpha_1 / T: GPU-s per second of HBM residency     */
-    double b2_per_token;   /* beta_2 / T: GPU-s to restore from host at resume   */
-    double b3_per_token;   /* beta_3 / T: GPU-s to recompute at resume           */
-    double host_slots_c2;  /* C2: suspended contexts that fit in host DRAM       */
-    double w_ref_s;        /* W_ref: reference residence time, seconds           */
+    double a1_per_token;       /* alpha_1 / T: GPU-s per second of HBM residency */
+    double b2_per_token;       /* beta_2 / T: GPU-s to restore from host at resume */
+    double b3_per_token;       /* beta_3 / T: GPU-s to recompute at resume       */
+    double host_slots_c2;      /* C2: suspended contexts that fit in host DRAM   */
+    double w_ref_s;            /* W_ref: reference residence time, seconds       */
+    double offload_per_token;  /* GPU-s per token for the copy at offload; 0 = uncharged */
 } kvr_prices;
 
 /* Candidate policies and loads; all three arrays are HOST pointers.
@@ -109,8 +123,11 @@ typedef struct {
  *   a1 = n_gpu * kv_bytes_per_token / hbm_usable_bytes   (share of usable HBM)
  *   b2 = n_gpu * kv_bytes_per_token / host_link_bytes_per_s (restore time)
  *   b3 = n_gpu / prefill_tokens_per_s                     (re-prefill time)
- * host_slots_c2 and w_ref_s are copied through.  Every argument must be
- * finite and > 0 (else KVR_E_PRICE); out must not be NULL (KVR_E_NULL).
+ * host_slots_c2 and w_ref_s are copied through and offload_per_token is set to
+ * 0 (the copy at offload uncharged; a caller who charges it sets the field,
+ * e.g. to b2 for a link with the same bandwidth both ways).  Every argument
+ * must be finite and > 0 (else KVR_E_PRICE); out must not be NULL
+ * (KVR_E_NULL).
  */
 int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
                              double host_link_bytes_per_s, double prefill_tokens_per_s,
@@ -227,7 +244,8 @@ int kvr_eq3_timer(const kvr_prices *p, double lambda, double *t2_out);
  *   d_wait_s        device, float64 [n_reps][n]: waits, finite, >= 0.
  *   d_ctx_tokens    device, int32 [n_reps][n] or NULL (every context 1 token).
  *   p               host: b2, b3 and host_slots_c2 are used (all fields must be
- *                   valid; C2 not an integer >= 1 is KVR_E_PRICE).
+ *                   valid; C2 not an integer >= 1 is KVR_E_PRICE; a nonzero
+ *                   offload_per_token is KVR_E_METHOD).
  *   t2[n_t2]        host: host timers, > 0 (+INFINITY = host-retain), any order.
  *   d_cost          device, float64 [n_reps][n_t2]: mean GPU-s per request,
  *                   (b2*R + b3*(Ttot - R)) / n with R the restored tokens.
@@ -274,7 +292,8 @@ typedef struct {
  *                   laid out and validated as in kvr_capacity_replay (its
  *                   arrivals are expected to be drawn at the load lambda).
  *   p               host: every field is used (alpha_1 for t*); C2 must be an
- *                   integer >= 1 (else KVR_E_PRICE).
+ *                   integer >= 1 (else KVR_E_PRICE); a nonzero
+ *                   offload_per_token is KVR_E_METHOD.
  *   lambda          host: calibration load, suspended requests per second,
  *                   finite and >= 0 (else KVR_E_GRID).
  *   d_out           device: one kvr_controller_out, written by the call.

@@ -38,7 +38,7 @@ EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy", "kv
 class kvr_prices(ctypes.Structure):
     _fields_ = [("a1_per_token", ctypes.c_double), ("b2_per_token", ctypes.c_double),
                 ("b3_per_token", ctypes.c_double), ("host_slots_c2", ctypes.c_double),
-                ("w_ref_s", ctypes.c_double)]
+                ("w_ref_s", ctypes.c_double), ("offload_per_token", ctypes.c_double)]
 
 
 class kvr_policy_grid(ctypes.Structure):
@@ -121,12 +121,16 @@ def _check(code: int, where: str) -> None:
 def kvr_prices_from_platform(kv_bytes_per_token: float, hbm_usable_bytes: float,
                              host_link_bytes_per_s: float, prefill_tokens_per_s: float,
                              n_gpu: float = 1.0, host_slots_c2: float = 425.0,
-                             w_ref_s: float = 1800.0) -> kvr_prices:
+                             w_ref_s: float = 1800.0, charge_offload: bool = False) -> kvr_prices:
+    """With charge_offload the device-to-host copy at offload is charged at
+    the restore's per-token time (offload_per_token = b2_per_token)."""
     out = kvr_prices()
     _check(load_library().kvr_prices_from_platform(
         float(kv_bytes_per_token), float(hbm_usable_bytes), float(host_link_bytes_per_s),
         float(prefill_tokens_per_s), float(n_gpu), float(host_slots_c2), float(w_ref_s),
         ctypes.byref(out)), "kvr_prices_from_platform")
+    if charge_offload:
+        out.offload_per_token = out.b2_per_token
     return out
 
 

@@ -52,7 +52,18 @@ int check_prices(const kvr_prices *p)
     if (!pos_finite(p->a1_per_token) || !pos_finite(p->b2_per_token) ||
         !pos_finite(p->b3_per_token) || !pos_finite(p->host_slots_c2) || !pos_finite(p->w_ref_s))
         return KVR_E_PRICE;
+    if (!std::isfinite(p->offload_per_token) || p->offload_per_token < 0.0) return KVR_E_PRICE;
     return KVR_OK;
+}
+
+// Prices of the grid kernels.  The optional offload charge is paid once by
+// every request with w > t1, which are exactly the requests that pay b2 (host
+// copy restored) or b3 (discarded, recomputed), so it is added to both; the
+// congestion price a2 keeps the plain b3 of Eq. 3.
+PriceDev device_prices(const kvr_prices *p)
+{
+    return PriceDev{p->a1_per_token, p->b2_per_token + p->offload_per_token,
+                    p->b3_per_token + p->offload_per_token};
 }
 
 int check_grid(const kvr_policy_grid *g)
@@ -281,6 +292,7 @@ int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
     out->b3_per_token = n_gpu / prefill_tokens_per_s;
     out->host_slots_c2 = host_slots_c2;
     out->w_ref_s = w_ref_s;
+    out->offload_per_token = 0.0;
     return KVR_OK;
 }
 
@@ -319,7 +331,7 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
 
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     int *status = static_cast<int *>(d_ws);
-    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    const PriceDev pr = device_prices(p);
     Tables tb{};
     if (method == KVR_BRUTE) {
         if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
@@ -385,7 +397,7 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
 
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     int *status = static_cast<int *>(d_ws);
-    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    const PriceDev pr = device_prices(p);
     Tables tb{};
     if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
         return rc;
@@ -460,7 +472,7 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
 
     hipStream_t s = static_cast<hipStream_t>(hip_stream);
     int *status = static_cast<int *>(d_ws);
-    PriceDev pr{p->a1_per_token, p->b2_per_token, p->b3_per_token};
+    const PriceDev pr = device_prices(p);
     Tables tb{};
     if ((rc = stage_tables(d_ws, off_t1, off_t2, off_a2, Lpad, *p, *g, s, tb)) != KVR_OK) return rc;
     kvr::FactoredWs fw{};
@@ -508,6 +520,7 @@ int kvr_capacity_replay(const double *d_arrival_s, const double *d_wait_s,
     if (!ws_bytes || !t2) return KVR_E_NULL;
     int rc;
     if ((rc = check_prices(p)) != KVR_OK) return rc;
+    if (p->offload_per_token != 0.0) return KVR_E_METHOD;   // no offload charge in the replay
     const double c2d = p->host_slots_c2;
     if (!(c2d >= 1.0) || c2d != std::floor(c2d) || c2d > 9.0e15) return KVR_E_PRICE;
     if (n_reps < 1 || n < 1 || n > 8192 || n_t2 < 1 || n_t2 > kMaxLoads) return KVR_E_SIZE;
@@ -542,6 +555,7 @@ int kvr_controller_select(const double *d_arrival_s, const double *d_wait_s,
     int rc;
     double t2 = 0.0;
     if ((rc = kvr_eq3_timer(p, lambda, &t2)) != KVR_OK) return rc;
+    if (p->offload_per_token != 0.0) return KVR_E_METHOD;   // no offload charge in the replay
     const double c2d = p->host_slots_c2;
     if (!(c2d >= 1.0) || c2d != std::floor(c2d) || c2d > 9.0e15) return KVR_E_PRICE;
     if (n_reps < 1 || n < 1 || n > 8192 || n_reps > INT32_MAX / 2) return KVR_E_SIZE;

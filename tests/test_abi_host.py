@@ -157,6 +157,37 @@ def test_bad_price_rejected(lib, field, value):
     assert _cost_grid_rc(lib, g, prices=p)[0] == kvr.KVR_E_PRICE
 
 
+@pytest.mark.parametrize("value", [-1e-9, -math.inf, math.nan, math.inf])
+def test_bad_offload_charge_rejected(lib, value):
+    """The optional offload charge may be 0 or positive, never negative or
+    non-finite."""
+    p = _prices()
+    p.offload_per_token = value
+    g = kvr.PolicyGrid([0.0], [5.0], [0.1])
+    assert _cost_grid_rc(lib, g, prices=p)[0] == kvr.KVR_E_PRICE
+
+
+def test_offload_charge_field(lib):
+    """The header's price struct and the binding's agree field by field; the
+    platform helper leaves the offload copy uncharged unless asked, and then
+    charges it at the restore's per-token time; a positive charge passes the
+    grid entry points' checks."""
+    text = open(HEADER).read()
+    body = text[text.index("typedef struct {\n    double a1_per_token;"):]
+    body = body[:body.index("} kvr_prices;")]
+    assert re.findall(r"double ([a-z0-9_]+);", body) == [f[0] for f in kvr.kvr_prices._fields_]
+    assert ctypes.sizeof(kvr.kvr_prices) == 48
+    assert _prices().offload_per_token == 0.0
+    p = kvr.kvr_prices_from_platform(131072, 250e9, 50e9, 20000.0, charge_offload=True)
+    assert p.offload_per_token == p.b2_per_token > 0.0
+    g = kvr.PolicyGrid([0.0, 4.0], [5.0, math.inf], [0.1])
+    assert _cost_grid_rc(lib, g, prices=p)[0] == kvr.KVR_OK
+    t2 = ctypes.c_double()
+    assert lib.kvr_eq3_timer(ctypes.byref(p), 0.5, ctypes.byref(t2)) == kvr.KVR_OK
+    q = _prices()
+    assert lib.kvr_eq3_timer(ctypes.byref(q), 0.5, ctypes.byref(ctypes.c_double())) == kvr.KVR_OK
+
+
 def test_method_and_size_errors(lib):
     g = kvr.PolicyGrid([0.0], [5.0, math.inf], [0.1])
     assert _cost_grid_rc(lib, g, method=7)[0] == kvr.KVR_E_METHOD
@@ -288,6 +319,9 @@ def test_capacity_replay_host_errors(lib):
     frac = _prices()
     frac.host_slots_c2 = 425.5
     assert call(prices=frac) == kvr.KVR_E_PRICE
+    charged = _prices()
+    charged.offload_per_token = charged.b2_per_token   # the replay has no offload charge
+    assert call(prices=charged) == kvr.KVR_E_METHOD
     sz.value = 1                                   # far below the size needed
     assert call(ws=FAKE) == kvr.KVR_E_WORKSPACE
     assert lib.kvr_capacity_replay(FAKE, FAKE, None, 4, 100, ctypes.byref(p), None, 2, FAKE,
@@ -330,6 +364,9 @@ def test_controller_host_errors(lib):
     zero = _prices()
     zero.a1_per_token = 0.0
     assert call(prices=zero) == kvr.KVR_E_PRICE
+    charged = _prices()
+    charged.offload_per_token = 1e-6                   # the replay has no offload charge
+    assert call(prices=charged) == kvr.KVR_E_METHOD
     assert lib.kvr_controller_select(FAKE, FAKE, None, 4, 100, None, 0.5, FAKE, None,
                                      ctypes.byref(sz), None) == kvr.KVR_E_NULL
     assert lib.kvr_controller_select(FAKE, FAKE, None, 4, 100, ctypes.byref(p), 0.5, FAKE, None,

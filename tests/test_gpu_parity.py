@@ -196,6 +196,39 @@ def test_bootstrap_random(kvr, oracle_mod, case):
     assert_costs(_np(bc2), _np(bc), rtol=1e-15)
 
 
+@pytest.mark.parametrize("seed,n,k1,k2,L", [(211, 3000, 3, 70, 5), (212, 700, 2, 9, 33)])
+def test_offload_charge_every_grid_method(kvr, oracle_mod, seed, n, k1, k2, L):
+    """The optional charge for the copy at offload (T * b2 per request with
+    w > t1, the link's per-token time) through BRUTE, SORTED, the bootstrap
+    and the factored bootstrap, against the oracle's double loop with the
+    same charge."""
+    wl = workloads.random_case(seed, n, k1, k2, L, resamples=3, ties=True)
+    pf = wl.platform
+    args = (wl.kv_bytes_per_token, pf["hbm_usable_bytes"], pf["host_link_bytes_per_s"],
+            pf["prefill_tokens_per_s"], pf["n_gpu"], pf["host_slots_c2"], pf["w_ref_s"])
+    lp = kvr.kvr_prices_from_platform(*args, charge_offload=True)
+    pr = oracle_mod.prices_from_platform(*args, charge_offload=True)
+    assert lp.offload_per_token == pr.boff > 0.0
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    for method in (kvr.KVR_BRUTE, kvr.KVR_SORTED):
+        cost = kvr.kvr_cost_grid(w, T, lp, g, method=method)
+        assert_costs(_np(cost), ref)
+        assert_selection(ref, _np(kvr.kvr_select_policy(cost, g.last_inf)[0]),
+                         oracle_mod.select(ref, wl.t2)[0])
+    idx = _dev(wl.idx, _i32())
+    for factored in (False, True):
+        best, bc, cost = kvr.kvr_bootstrap(w, T, idx, lp, g, want_cost=True, factored=factored)
+        for r in range(3):
+            rr = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                      idx_row=wl.idx[r])
+            assert_costs(_np(cost)[r], rr)
+            rb, rbc, _ = oracle_mod.select(rr, wl.t2)
+            assert_selection(rr, _np(best)[r], rb)
+            assert_costs(_np(bc)[r], rbc)
+
+
 def _boot_full(kvr, oracle_mod, name, sample_rows):
     wl = workloads.make(name)
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
