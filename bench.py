@@ -117,7 +117,7 @@ def main() -> int:
     ap.add_argument("--resamples", type=int, default=None,
                     help="truncate the bootstrap batch (for quick local runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=1,
+    ap.add_argument("--cpu-rows", type=int, default=2,
                     help="bootstrap rows the CPU oracle evaluates for cpu_baseline")
     ap.add_argument("--paths", action="store_true",
                     help="also time the other entry points on their workloads")
