@@ -2,7 +2,8 @@
 oracle's double loop: the policy count below, at and off multiples of the
 64-lane groups, one to several load tiles (up to 40 loads), single samples
 and bootstrap rows of every length, sample splits and fused selection,
-duplicated waits and waits sitting on timers.  Costs within 1e-9 relative,
+duplicated waits and waits sitting on timers; every fourth case charges the
+copy at offload.  Costs within 1e-9 relative,
 selections identical up to rounding-level near ties."""
 import numpy as np
 import pytest
@@ -45,6 +46,9 @@ def test_grid_shapes(kvr, oracle_mod, case):
                                inf_last=(seed % 3 != 0))
     pr = oracle_mod.workload_prices(wl)
     lp = _lib_prices(kvr, wl)
+    if seed % 4 == 1:   # the optional charge for the copy at offload, on both sides
+        pr.boff = pr.b2
+        lp.offload_per_token = lp.b2_per_token
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
     w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
     if wl.idx is None:
