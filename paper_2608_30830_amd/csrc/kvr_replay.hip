@@ -254,8 +254,8 @@ __device__ __forceinline__ uint32_t bit_range(int lo, int hi)
 
 // Set bits of a lane's column in [from, to) beyond the first word (the rare
 // case of a range that crosses a word boundary).
-template <int NW>
-__device__ __forceinline__ int count_tail(const uint32_t (*bits)[kWave], int lane, int from, int to)
+template <int LPW>
+__device__ __forceinline__ int count_tail(const uint32_t (*bits)[LPW], int lane, int from, int to)
 {
     int c = 0;
     for (int b = ((from >> 5) + 1) << 5; b < to; b += 32) {
@@ -266,25 +266,31 @@ __device__ __forceinline__ int count_tail(const uint32_t (*bits)[kWave], int lan
     return c;
 }
 
-// One lane per (sequence, timer k0 + k), k < kc; NW 32-bit words per bitset
-// bound n <= 32*NW.  Lanes past the last sequence walk the last one and write
+// One lane per (timer k0 + k, sequence) pair, k < kc, the pairs numbered
+// timer-major and dealt LPW to a wave: 64, or 40 so that four waves, one per
+// SIMD, fit in a CU's LDS (the other lanes leave at once: no lane touches
+// another's LDS column and there is no barrier).  NW 32-bit words per bitset
+// bound n <= 32*NW.  Lanes past the last pair walk the last one and write
 // nothing.  The step loop reads only the packed per-arrival words (and the
 // context sizes when CTX), kRing arrivals ahead, with no conditional loads.
-template <int NW, bool CTX>
+template <int NW, int LPW, bool CTX>
 __global__ void __launch_bounds__(kWave) replay_merge_kernel(
     const int32_t *__restrict__ ctx, int64_t reps, int n, int64_t c2,
     const uint32_t *__restrict__ pr, const uint16_t *__restrict__ ec, double b2, double b3,
     double *__restrict__ cost, int64_t *__restrict__ restored_out,
-    int64_t *__restrict__ admitted_out, int k0, int K)
+    int64_t *__restrict__ admitted_out, int k0, int kn, int K)
 {
-    __shared__ uint32_t rbits[NW][kWave];
-    __shared__ uint32_t ebits[NW][kWave];
+    __shared__ uint32_t rbits[NW][LPW];
+    __shared__ uint32_t ebits[NW][LPW];
     const int lane = threadIdx.x;
-    const int64_t groups = (reps + kWave - 1) / kWave;
-    const int k = (int)(blockIdx.x / groups);
-    const int64_t row = (blockIdx.x % groups) * kWave + lane;
-    const bool active = row < reps;
-    const int64_t rr = active ? row : reps - 1;
+    if (lane >= LPW) return;
+    const int64_t pairs = reps * kn;
+    const int64_t F = (int64_t)blockIdx.x * LPW + lane;
+    const bool active = F < pairs;
+    const int64_t Fa = active ? F : pairs - 1;
+    const int k = (int)(Fa / reps);
+    const int64_t row = Fa % reps;
+    const int64_t rr = row;
     const int32_t *C = CTX ? ctx + rr * n : nullptr;
     const uint32_t *PR = pr + rr * n;
     const uint16_t *EC = ec + ((int64_t)k * reps + rr) * n;
@@ -332,8 +338,8 @@ __global__ void __launch_bounds__(kWave) replay_merge_kernel(
                 int gone = __popc(rw0 & bit_range(rdone - (rq << 5), rc - (rq << 5))) +
                            __popc(ew0 & bit_range(edone - (eq << 5), ex - (eq << 5)));
                 if (rc > ((rq + 1) << 5) || ex > ((eq + 1) << 5))
-                    gone += count_tail<NW>(rbits, lane, rdone, rc) +
-                            count_tail<NW>(ebits, lane, edone, ex);
+                    gone += count_tail<LPW>(rbits, lane, rdone, rc) +
+                            count_tail<LPW>(ebits, lane, edone, ex);
                 occ -= gone;
                 rdone = (rc > rdone) ? rc : rdone;
                 edone = (ex > edone) ? ex : edone;
@@ -384,6 +390,22 @@ size_t replay_ws_bytes(int64_t reps, int64_t n, int K)
            a256(sizeof(double) * K);
 }
 
+// Lanes per merge wave.  A wave's step is bound by its own instruction
+// stream, so two waves on one SIMD take twice as long: the time goes with the
+// most waves any SIMD runs.  Each lane keeps 2*NW words of LDS and a CU (four
+// SIMDs, 160 KiB of LDS; 256 CUs) holds only so many waves; 40-lane waves are
+// taken when they put fewer waves on the busiest SIMD than 64-lane ones.
+static int merge_lanes(int64_t reps, int kn, int nw)
+{
+    auto load = [&](int64_t lpw) {
+        int64_t per_cu = (int64_t)160 * 1024 / (8 * (int64_t)nw * lpw);
+        per_cu = per_cu < 4 ? per_cu : 4;
+        const int64_t waves = (reps * kn + lpw - 1) / lpw;
+        return (waves + 256 * per_cu - 1) / (256 * per_cu);
+    };
+    return load(40) < load(64) ? 40 : 64;
+}
+
 template <int MAXN, int NW>
 static hipError_t launch_replay_n(const double *arrival, const double *wait, const int32_t *ctx,
                                   int64_t reps, int n, const double *t2, int K, int64_t c2,
@@ -394,20 +416,29 @@ static hipError_t launch_replay_n(const double *arrival, const double *wait, con
     hipLaunchKernelGGL(replay_sort_kernel<MAXN>, dim3((unsigned)reps), dim3(kReplaySortThreads), 0,
                        stream, arrival, wait, ctx, n, pr, status);
     const int kc = replay_timer_chunk(reps, n, K);
-    const int64_t groups = (reps + kWave - 1) / kWave;
     for (int k0 = 0; k0 < K; k0 += kc) {
         const int kn = (K - k0 < kc) ? K - k0 : kc;
         hipLaunchKernelGGL(replay_expiry_kernel<MAXN>, dim3((unsigned)reps),
                            dim3(kReplaySortThreads), 0, stream, arrival, wait, n, t2 + k0, kn, reps,
                            ec);
-        if (ctx != nullptr)
-            hipLaunchKernelGGL((replay_merge_kernel<NW, true>), dim3((unsigned)(groups * kn)),
-                               dim3(kWave), 0, stream, ctx, reps, n, c2, pr, ec, b2, b3, cost,
-                               restored, admitted, k0, K);
+        const int lpw = merge_lanes(reps, kn, NW);
+        const unsigned blocks = (unsigned)((reps * kn + lpw - 1) / lpw);
+        if (lpw == 40 && ctx != nullptr)
+            hipLaunchKernelGGL((replay_merge_kernel<NW, 40, true>), dim3(blocks), dim3(kWave), 0,
+                               stream, ctx, reps, n, c2, pr, ec, b2, b3, cost, restored, admitted,
+                               k0, kn, K);
+        else if (lpw == 40)
+            hipLaunchKernelGGL((replay_merge_kernel<NW, 40, false>), dim3(blocks), dim3(kWave), 0,
+                               stream, ctx, reps, n, c2, pr, ec, b2, b3, cost, restored, admitted,
+                               k0, kn, K);
+        else if (ctx != nullptr)
+            hipLaunchKernelGGL((replay_merge_kernel<NW, 64, true>), dim3(blocks), dim3(kWave), 0,
+                               stream, ctx, reps, n, c2, pr, ec, b2, b3, cost, restored, admitted,
+                               k0, kn, K);
         else
-            hipLaunchKernelGGL((replay_merge_kernel<NW, false>), dim3((unsigned)(groups * kn)),
-                               dim3(kWave), 0, stream, ctx, reps, n, c2, pr, ec, b2, b3, cost,
-                               restored, admitted, k0, K);
+            hipLaunchKernelGGL((replay_merge_kernel<NW, 64, false>), dim3(blocks), dim3(kWave), 0,
+                               stream, ctx, reps, n, c2, pr, ec, b2, b3, cost, restored, admitted,
+                               k0, kn, K);
         hipError_t err = hipGetLastError();
         if (err != hipSuccess) return err;
     }
