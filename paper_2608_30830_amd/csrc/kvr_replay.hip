@@ -242,18 +242,18 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_expiry_kernel(
     }
 }
 
-// Bits [lo, hi) of a word, 0 <= lo <= 32; zero when hi <= lo.  The width
-// min(hi, 32) - lo is at most 32, so the mask is formed in 64 bits without a
-// special case for a full word.
-__device__ __forceinline__ uint32_t bit_range(int lo, int hi)
+// Set bits in [lo, hi) of the 64-bit window w1:w0, for 0 <= lo <= 32 and
+// hi <= 64; zero when hi <= lo (lo = 32 only comes with an empty range).
+__device__ __forceinline__ int count_window(uint32_t w0, uint32_t w1, int lo, int hi)
 {
-    int w = (hi < 32 ? hi : 32) - lo;
-    w = w > 0 ? w : 0;
-    return (uint32_t)((((uint64_t)1 << w) - 1u) << lo);
+    const int width = hi - lo;
+    const uint64_t win = ((uint64_t)w1 << 32) | w0;
+    const uint64_t mask = width > 0 ? (~0ull >> (64 - width)) << lo : 0ull;
+    return __popcll(win & mask);
 }
 
-// Set bits of a lane's column in [from, to) beyond the first word (the rare
-// case of a range that crosses a word boundary).
+// Set bits of a lane's column in [from, to) from the word after from's on
+// (the rare case of a range longer than the two-word window).
 template <int LPW>
 __device__ __forceinline__ int count_tail(const uint32_t (*bits)[LPW], int lane, int from, int to)
 {
@@ -330,16 +330,23 @@ __global__ void __launch_bounds__(kWave) replay_merge_kernel(
                 const bool stays = (ew[u] >> 15) != 0u;
                 // departures at or before this arrival: set bits of rbits in
                 // [rdone, rc) (resumes) and of ebits in [edone, ex) (timers);
-                // the first word of each range is always read, so the common
-                // single-word case has no branch
+                // the two words from each range's start are always read, so a
+                // range of up to 33 bits, which nearly every step has, takes
+                // no branch.  The second word's row is clamped to the last
+                // row: a range ends at n <= 32*NW, so past the last row its
+                // window bits are never counted.
                 const int rq = ((rdone < n) ? rdone : n - 1) >> 5;
                 const int eq = ((edone < n) ? edone : n - 1) >> 5;
-                const uint32_t rw0 = rbits[rq][lane], ew0 = ebits[eq][lane];
-                int gone = __popc(rw0 & bit_range(rdone - (rq << 5), rc - (rq << 5))) +
-                           __popc(ew0 & bit_range(edone - (eq << 5), ex - (eq << 5)));
-                if (rc > ((rq + 1) << 5) || ex > ((eq + 1) << 5))
-                    gone += count_tail<LPW>(rbits, lane, rdone, rc) +
-                            count_tail<LPW>(ebits, lane, edone, ex);
+                const int rq1 = (rq + 1 < NW) ? rq + 1 : rq;
+                const int eq1 = (eq + 1 < NW) ? eq + 1 : eq;
+                const uint32_t r0 = rbits[rq][lane], r1 = rbits[rq1][lane];
+                const uint32_t e0 = ebits[eq][lane], e1 = ebits[eq1][lane];
+                const int rhi = rc - (rq << 5), ehi = ex - (eq << 5);
+                int gone = count_window(r0, r1, rdone - (rq << 5), rhi < 64 ? rhi : 64) +
+                           count_window(e0, e1, edone - (eq << 5), ehi < 64 ? ehi : 64);
+                if (rhi > 64 || ehi > 64)
+                    gone += count_tail<LPW>(rbits, lane, (rq << 5) + 32, rc) +
+                            count_tail<LPW>(ebits, lane, (eq << 5) + 32, ex);
                 occ -= gone;
                 rdone = (rc > rdone) ? rc : rdone;
                 edone = (ex > edone) ? ex : edone;
