@@ -26,17 +26,17 @@
 // requests have reached their timer by a_j (a binary search, the arrivals
 // being sorted) and whether j itself resumes before its timer.
 //
-// The merge runs one lane per (sequence, timer), 64 sequences with the same
-// timer per wave, and keeps two lane-private bitsets in LDS: rbits[p] for "the
-// request at resume place p was admitted and resumes before its timer", set at
-// its admission through its place, and ebits[i] for "request i was admitted
-// and is discarded at its timer".  At arrival j the departures that free slots
+// The merge runs one lane per (timer, sequence) pair, 64 or 40 pairs per wave,
+// and keeps two lane-private bitsets in LDS: rbits[p] for "the request at
+// resume place p was admitted and resumes before its timer", set at its
+// admission through its place, and ebits[i] for "request i was admitted and
+// is discarded at its timer".  At arrival j the departures that free slots
 // are the set bits of rbits between the previous and the current resume
-// cursor and of ebits between the previous and the current expiry cursor (two
-// popcounts).  The step loop reads only the packed per-arrival words, in
-// register buffers of eight arrivals filled one buffer ahead of use: no load
-// in it depends on another, so the walk is bound by LDS latency rather than
-// by chains of global loads.
+// cursor and of ebits between the previous and the current expiry cursor
+// (popcounts over a two-word window of each).  The step loop reads only the
+// packed per-arrival words, in register buffers of eight arrivals filled one
+// buffer ahead of use: no load in it depends on another, and a wave's walk is
+// bound by its own instruction stream rather than by chains of global loads.
 #include "kvr_device.h"
 
 namespace kvr {
