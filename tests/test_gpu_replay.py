@@ -116,3 +116,22 @@ def test_replay_many_timers_in_chunks(kvr, oracle_mod):
     oc, orr = oracle_mod.capacity_replay_batch(rc.arrival_s, rc.wait_s, 425, t2, 0.02, 1.91)
     assert np.array_equal(rest, orr)
     assert np.all(np.abs(cost - oc) <= 4 * np.spacing(oc))
+
+
+@pytest.mark.parametrize("reps,n,n_timers", [(4096, 2500, 9), (4096, 5000, 5)])
+def test_replay_forty_lane_waves(kvr, oracle_mod, reps, n, n_timers):
+    """Batches whose (timer, sequence) lanes would need a second round of
+    64-lane waves (LDS holds two per CU) run as 40-lane waves, four per CU:
+    36,864 lanes with up to 4,096 requests per sequence, 20,480 with up to
+    8,192.  Sampled rows against the oracle, every row's admissions within
+    their bounds."""
+    rc = workloads.replay_case("lognormal", 2 * LC, reps=reps, n=n, seed=123)
+    t2 = np.concatenate([np.geomspace(60.0, 20000.0, n_timers - 1), [np.inf]])
+    cost, rest, adm = _run(kvr, rc.arrival_s, rc.wait_s, t2, 425)
+    rows = np.unique(np.linspace(0, reps - 1, 61).astype(int))
+    oc, orr = oracle_mod.capacity_replay_batch(rc.arrival_s[rows], rc.wait_s[rows], 425, t2,
+                                               0.02, 1.91)
+    assert np.array_equal(rest[rows], orr)
+    assert np.all(np.abs(cost[rows] - oc) <= 4 * np.spacing(oc))
+    assert np.all((adm >= np.minimum(n, 425)) & (adm <= n))
+    assert np.all(rest <= adm)
