@@ -169,6 +169,27 @@ def test_weibull_1m_sorted_brute_and_sampled_oracle(kvr, oracle_mod):
     assert_selection(closed, b2, rb)
 
 
+def test_max_size_2p24_waits(kvr, oracle_mod):
+    """2^24 waits, sixteen times the largest workload (the sorted path's
+    scaling sample): the stable order bit for bit, and BRUTE and SORTED against
+    the oracle's closed form on the whole grid, with every selection."""
+    wl = workloads.sort_scale_case(24)
+    pr = oracle_mod.workload_prices(wl)
+    cb, _, g = run_grid(kvr, wl, "brute")
+    cs, perm, _ = run_grid(kvr, wl, "sorted")
+    ref_perm = oracle_mod.stable_order(wl.wait_s)
+    assert np.array_equal(perm, ref_perm)
+    closed = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                         perm=ref_perm)
+    assert_costs(cb, closed)
+    assert_costs(cs, closed)
+    import torch
+    rb = oracle_mod.select(closed, wl.t2)[0]
+    for c in (cb, cs):
+        assert_selection(closed, _np(kvr.kvr_select_policy(torch.as_tensor(c).cuda(),
+                                                           g.last_inf)[0]), rb)
+
+
 @pytest.mark.parametrize("case", [(201, 500, 2, 70, 5, 3, None), (202, 1300, 1, 65, 16, 4, 777),
                                   (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None),
                                   # few resamples, many draws: several recompute-share blocks
