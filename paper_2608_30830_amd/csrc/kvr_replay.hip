@@ -221,23 +221,45 @@ __global__ void __launch_bounds__(kReplaySortThreads) replay_expiry_kernel(
     const double *__restrict__ arrival, const double *__restrict__ wait, int n,
     const double *__restrict__ t2s, int kc, int64_t reps, uint16_t *__restrict__ ec)
 {
+    constexpr int kPer = (MAXN + kReplaySortThreads - 1) / kReplaySortThreads;
     __shared__ double A[MAXN];
     const int64_t row = blockIdx.x;
-    for (int i = threadIdx.x; i < n; i += blockDim.x) A[i] = arrival[row * n + i];
+    const int t = threadIdx.x;
+    for (int i = t; i < n; i += blockDim.x) A[i] = arrival[row * n + i];
     __syncthreads();
+    // this thread's arrivals j = t + q*512 and their waits, read once
+    double aj[kPer], wj[kPer];
+#pragma unroll
+    for (int q = 0; q < kPer; ++q) {
+        const int j = t + q * kReplaySortThreads;
+        aj[q] = (j < n) ? A[j] : 0.0;
+        wj[q] = (j < n) ? wait[row * n + j] : 0.0;
+    }
     for (int k = 0; k < kc; ++k) {
         const double t2 = t2s[k];
         uint16_t *out = ec + ((int64_t)k * reps + row) * n;
-        for (int j = threadIdx.x; j < n; j += blockDim.x) {
-            const double a = A[j];
-            int lo = 0, hi = j;   // first i < j with fl(a_i + t2) > a
-            while (lo < hi) {
-                const int mid = (lo + hi) >> 1;
-                if (A[mid] + t2 <= a) lo = mid + 1;
-                else hi = mid;
+        // #{i < j : fl(a_i + t2) <= a_j}, a prefix of [0, j) since the left
+        // side is non-decreasing in i: fixed-step searches (steps MAXN/2 .. 1
+        // sum to MAXN - 1 >= j) that advance together, so the kPer LDS reads
+        // of a step overlap instead of forming kPer serial chains
+        int pos[kPer];
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) pos[q] = 0;
+        for (int step = MAXN / 2; step > 0; step >>= 1) {
+#pragma unroll
+            for (int q = 0; q < kPer; ++q) {
+                const int j = t + q * kReplaySortThreads;
+                const int m = pos[q] + step - 1;   // < MAXN always
+                if (m < j && A[m] + t2 <= aj[q]) pos[q] += step;
             }
-            const uint32_t stays = (wait[row * n + j] <= t2) ? 1u : 0u;
-            out[j] = (uint16_t)((uint32_t)lo | (stays << 15));
+        }
+#pragma unroll
+        for (int q = 0; q < kPer; ++q) {
+            const int j = t + q * kReplaySortThreads;
+            if (j < n) {
+                const uint32_t stays = (wj[q] <= t2) ? 1u : 0u;
+                out[j] = (uint16_t)((uint32_t)pos[q] | (stays << 15));
+            }
         }
     }
 }
