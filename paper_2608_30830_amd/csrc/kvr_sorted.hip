@@ -414,17 +414,22 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
 __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
     const int32_t *__restrict__ T, int64_t n, int64_t *__restrict__ blkN,
-    double *__restrict__ blkS)
+    double *__restrict__ blkS, int32_t *__restrict__ Tsorted)
 {
-    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanIPT;
+    // striped over the tile (element q*256 + t of it), so that every load and
+    // store of a wave covers consecutive positions; the tile's total is summed
+    // in this fixed order
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x;
     int64_t sn = 0;
     double ss = 0.0;
+#pragma unroll
     for (int q = 0; q < kScanIPT; ++q) {
-        const int64_t j = base + q;
+        const int64_t j = base + (int64_t)q * kScanThreads;
         if (j < n) {
             const int32_t pj = perm[j];
             const int32_t pi = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
             const int32_t t = T[pi] < 1 ? 1 : T[pi];
+            Tsorted[j] = t;   // the gather is done once; the final pass streams it
             sn += t;
             ss += (double)t * __longlong_as_double((long long)skeys[j]);
         }
@@ -503,10 +508,11 @@ __global__ void __launch_bounds__(kScanThreads) scan_blocks_kernel(int64_t *blkN
     }
 }
 
-// Inclusive prefix within each tile plus the tile's offset; also emits perm.
+// Inclusive prefix within each tile plus the tile's offset, over the context
+// sizes in sorted order that scan_reduce_kernel gathered; also emits perm.
 __global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
     const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
-    const int32_t *__restrict__ T, int64_t n, const int64_t *__restrict__ blkN,
+    const int32_t *__restrict__ Tsorted, int64_t n, const int64_t *__restrict__ blkN,
     const double *__restrict__ blkS, int64_t *__restrict__ Nsum, double *__restrict__ Ssum,
     int32_t *__restrict__ perm_out)
 {
@@ -515,16 +521,40 @@ __global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
     double ts[kScanIPT];
     int64_t sn = 0;
     double ss = 0.0;
+    // a thread's kScanIPT positions are adjacent and start on a multiple of 8
+    // elements, so a full run is read with 16-byte loads (the workspace
+    // arrays are 256-byte aligned)
+    const bool full = base + kScanIPT <= n;
+    int32_t tv[kScanIPT];
+    uint64_t kv[kScanIPT];
+    if (full) {
+        static_assert(kScanIPT == 8, "vector loads below assume 8 positions per thread");
+        const int4 *tp = reinterpret_cast<const int4 *>(Tsorted + base);
+        const ulonglong2 *kp = reinterpret_cast<const ulonglong2 *>(skeys + base);
+        const int4 t0 = tp[0], t1 = tp[1];
+        const ulonglong2 k0 = kp[0], k1 = kp[1], k2 = kp[2], k3 = kp[3];
+        tv[0] = t0.x; tv[1] = t0.y; tv[2] = t0.z; tv[3] = t0.w;
+        tv[4] = t1.x; tv[5] = t1.y; tv[6] = t1.z; tv[7] = t1.w;
+        kv[0] = k0.x; kv[1] = k0.y; kv[2] = k1.x; kv[3] = k1.y;
+        kv[4] = k2.x; kv[5] = k2.y; kv[6] = k3.x; kv[7] = k3.y;
+    } else {
+#pragma unroll
+        for (int q = 0; q < kScanIPT; ++q) {
+            const int64_t j = base + q;
+            tv[q] = (j < n) ? Tsorted[j] : 0;
+            kv[q] = (j < n) ? skeys[j] : 0;
+        }
+    }
 #pragma unroll
     for (int q = 0; q < kScanIPT; ++q) {
         const int64_t j = base + q;
         if (j < n) {
-            const int32_t pj = perm[j];
-            const int32_t p = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
-            const int32_t t = T[p] < 1 ? 1 : T[p];
-            sn += t;
-            ss += (double)t * __longlong_as_double((long long)skeys[j]);
-            if (perm_out != nullptr) perm_out[j] = p;
+            sn += tv[q];
+            ss += (double)tv[q] * __longlong_as_double((long long)kv[q]);
+            if (perm_out != nullptr) {
+                const int32_t pj = perm[j];
+                perm_out[j] = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
+            }
         }
         tn[q] = sn;
         ts[q] = ss;
@@ -556,12 +586,22 @@ __global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
     }
     pn += xn - sn;
     ps += xs - ss;
+    if (full) {
+        longlong2 *np = reinterpret_cast<longlong2 *>(Nsum + base);
+        double2 *sp = reinterpret_cast<double2 *>(Ssum + base);
 #pragma unroll
-    for (int q = 0; q < kScanIPT; ++q) {
-        const int64_t j = base + q;
-        if (j < n) {
-            Nsum[j] = pn + tn[q];
-            Ssum[j] = ps + ts[q];
+        for (int h = 0; h < kScanIPT / 2; ++h) {
+            np[h] = make_longlong2(pn + tn[2 * h], pn + tn[2 * h + 1]);
+            sp[h] = make_double2(ps + ts[2 * h], ps + ts[2 * h + 1]);
+        }
+    } else {
+#pragma unroll
+        for (int q = 0; q < kScanIPT; ++q) {
+            const int64_t j = base + q;
+            if (j < n) {
+                Nsum[j] = pn + tn[q];
+                Ssum[j] = ps + ts[q];
+            }
         }
     }
 }
@@ -666,12 +706,15 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
     int cur = 0;
     hipError_t err = launch_sort_keys(w, T, n, ws, &cur, status, stream);
     if (err != hipSuccess) return err;
+    // the other payload buffer is free once the sort is done: it takes the
+    // context sizes in sorted order
+    int32_t *Tsorted = ws.vals[cur ^ 1];
     hipLaunchKernelGGL(scan_reduce_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
-                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS);
+                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, Tsorted);
     hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(kScanThreads), 0, stream, ws.blkN,
                        ws.blkS, ws.nblocks_scan);
     hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
-                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
+                       ws.keys[cur], ws.vals[cur], Tsorted, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
                        perm_out);
     hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
                        ws.keys[cur], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
