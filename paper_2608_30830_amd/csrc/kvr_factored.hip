@@ -237,6 +237,29 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
                 int32_t qs[kFScanPer];
                 unsigned long long tn = 0ull;
                 double ts = 0.0;
+                // a full run of kFScanPer positions starts on a multiple of 4
+                // (pass starts are multiples of 2^15): one 16-byte load each
+                // of Ts and qslot and two of sw instead of an element each
+                int32_t tv[kFScanPer], qv[kFScanPer];
+                double wv4[kFScanPer];
+                if (kl + kFScanPer <= nk) {
+                    static_assert(kFScanPer == 4, "the vector loads below read 4 positions");
+                    const int4 t4 = *reinterpret_cast<const int4 *>(Ts + k0 + kl);
+                    const int4 q4 = *reinterpret_cast<const int4 *>(qslot + k0 + kl);
+                    const double2 w0 = reinterpret_cast<const double2 *>(sw + k0 + kl)[0];
+                    const double2 w1 = reinterpret_cast<const double2 *>(sw + k0 + kl)[1];
+                    tv[0] = t4.x; tv[1] = t4.y; tv[2] = t4.z; tv[3] = t4.w;
+                    qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
+                    wv4[0] = w0.x; wv4[1] = w0.y; wv4[2] = w1.x; wv4[3] = w1.y;
+                } else {
+#pragma unroll
+                    for (int q = 0; q < kFScanPer; ++q) {
+                        const int64_t k = kl + q;
+                        tv[q] = (k < nk) ? Ts[k0 + k] : 0;
+                        qv[q] = (k < nk) ? qslot[k0 + k] : -1;
+                        wv4[q] = (k < nk) ? sw[k0 + k] : 0.0;
+                    }
+                }
 #pragma unroll
                 for (int q = 0; q < kFScanPer; ++q) {
                     const int64_t k = kl + q;
@@ -244,10 +267,10 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
                     uint32_t c = 0u;
                     if (in) c = wide ? lh[k] : (lh[k >> 1] >> (16 * (int)(k & 1))) & 0xffffu;
                     const unsigned long long cwq =
-                        in ? (unsigned long long)c * (unsigned long long)Ts[k0 + k] : 0ull;
+                        in ? (unsigned long long)c * (unsigned long long)tv[q] : 0ull;
                     cw[q] = cwq;
-                    sv[q] = in ? (double)cwq * sw[k0 + k] : 0.0;
-                    qs[q] = in ? qslot[k0 + k] : -1;
+                    sv[q] = in ? (double)cwq * wv4[q] : 0.0;
+                    qs[q] = in ? qv[q] : -1;
                     tn += cwq;
                     ts += sv[q];
                 }
