@@ -190,22 +190,31 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
             __syncthreads();
             long long inr = 0;                              // draws counted in this range
             for (int64_t j = threadIdx.x; j < m; j += kFUnroll * B) {
+                // the kFUnroll draws are loaded unconditionally (a position past
+                // the row re-reads its last draw and is dropped) and checked with
+                // selects and one branch for all, so the index loads, and then
+                // the rank gathers, are in flight together
                 int32_t ii[kFUnroll];
+                bool live[kFUnroll];
 #pragma unroll
                 for (int u = 0; u < kFUnroll; ++u) {
-                    ii[u] = -1;                             // past the row: no draw
-                    if (j + u * B < m) {
-                        int32_t v = idx[r * m + j + u * B];
-                        if (v < 0 || (int64_t)v >= n) {
-                            flag_domain(status);
-                            v = 0;
-                        }
-                        ii[u] = v;
-                    }
+                    live[u] = j + u * B < m;
+                    ii[u] = idx[r * m + (live[u] ? j + u * B : m - 1)];
                 }
+                bool bad = false;
+#pragma unroll
+                for (int u = 0; u < kFUnroll; ++u) {
+                    const bool out = ii[u] < 0 || (int64_t)ii[u] >= n;
+                    bad = bad || (live[u] && out);
+                    ii[u] = out ? 0 : ii[u];                // a bad draw counts as sample 0
+                }
+                if (bad) flag_domain(status);
                 int64_t kk[kFUnroll];
 #pragma unroll
-                for (int u = 0; u < kFUnroll; ++u) kk[u] = (ii[u] >= 0) ? (int64_t)rank[ii[u]] - k0 : -1;
+                for (int u = 0; u < kFUnroll; ++u) {
+                    kk[u] = (int64_t)rank[ii[u]] - k0;
+                    if (!live[u]) kk[u] = -1;                // past the row: no draw
+                }
 #pragma unroll
                 for (int u = 0; u < kFUnroll; ++u) {
                     if (kk[u] >= 0 && kk[u] < nk) {

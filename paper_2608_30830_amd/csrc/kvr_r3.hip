@@ -102,26 +102,34 @@ __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
         for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) lh[x] = 0ull;
         __syncthreads();
         for (int64_t j = j0 + threadIdx.x; j < j1; j += kR3Unroll * B) {
-            int64_t i[kR3Unroll];
+            // the kR3Unroll draws are loaded unconditionally (a position past
+            // the split re-reads the split's last one and is dropped below)
+            // and checked with selects and one branch for all, so the index
+            // loads, and then the gathers, are in flight together
+            int32_t raw[kR3Unroll];
+            bool inr[kR3Unroll];
 #pragma unroll
             for (int u = 0; u < kR3Unroll; ++u) {
                 const int64_t jj = j + u * B;
-                i[u] = -1;                              // past the split: no draw
-                if (jj < j1) {
-                    i[u] = jj;
-                    if (idx != nullptr) {
-                        int32_t ii = idx[r * m + jj];
-                        if (ii < 0 || (int64_t)ii >= n) {
-                            flag_domain(status);
-                            ii = 0;
-                        }
-                        i[u] = ii;
-                    }
-                }
+                inr[u] = jj < j1;
+                const int64_t jc = inr[u] ? jj : j1 - 1;
+                raw[u] = (idx != nullptr) ? idx[r * m + jc] : (int32_t)jc;
             }
+            bool bad = false;
+            int32_t ic[kR3Unroll];
+#pragma unroll
+            for (int u = 0; u < kR3Unroll; ++u) {
+                const bool out = raw[u] < 0 || (int64_t)raw[u] >= n;
+                bad = bad || (inr[u] && out);
+                ic[u] = out ? 0 : raw[u];               // a bad draw counts as sample 0
+            }
+            if (bad) flag_domain(status);
             int2 bt[kR3Unroll];
 #pragma unroll
-            for (int u = 0; u < kR3Unroll; ++u) bt[u] = (i[u] >= 0) ? binT[i[u]] : make_int2(0, 0);
+            for (int u = 0; u < kR3Unroll; ++u) {
+                bt[u] = binT[ic[u]];
+                if (!inr[u]) bt[u] = make_int2(0, 0);   // bin 0 is never counted
+            }
 #pragma unroll
             for (int u = 0; u < kR3Unroll; ++u) {
                 const int64_t b = (int64_t)bt[u].x - 1 - b0;   // bin 0 gives b < 0
