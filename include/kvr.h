@@ -19,8 +19,9 @@
  *       a2(lambda) = max(0, lambda - lambda_crit) * b3 / C2,
  *       lambda_crit = C2 / W_ref            (Little's law saturation),
  *   then pays beta_2 = T*b2 at resume if w <= e (restore from host), or
- *   beta_3 = T*b3 if the copy was discarded at e (recompute).  t2 = +inf is
- *   host-retain.  The cost of a policy (t1_a, t2_k, lambda_l) is the mean of
+ *   beta_3 = T*b3 if the copy was discarded at e (recompute); the copy made
+ *   at offload is free unless kvr_prices.offload_per_token charges it (see
+ *   there).  t2 = +inf is host-retain.  The cost of a policy (t1_a, t2_k, lambda_l) is the mean of
  *   the per-request cost over the sample, in GPU-s per request (the unit of
  *   Table 6).
  *
@@ -70,7 +71,7 @@ enum {
     KVR_E_NULL = -1,       /* a required pointer is NULL                          */
     KVR_E_SIZE = -2,       /* a count is out of range, or a product overflows     */
     KVR_E_GRID = -3,       /* timer/load grid invalid (see kvr_policy_grid)       */
-    KVR_E_PRICE = -4,      /* a price, C2 or W_ref is not finite and > 0          */
+    KVR_E_PRICE = -4,      /* a price, C2 or W_ref not finite and > 0 (offload >= 0) */
     KVR_E_WORKSPACE = -5,  /* workspace too small or not 256-byte aligned         */
     KVR_E_DOMAIN = -6,     /* device-detected bad sample or index (status word)   */
     KVR_E_HIP = -7,        /* a HIP runtime call failed                           */
