@@ -36,7 +36,10 @@ constexpr int kFScanPer = 4;            // consecutive positions per thread in t
 constexpr int kFUnroll = 4;             // draws per thread and step, fetched together
 constexpr int kFLoads = 32;             // loads per policy-kernel block (16 when L <= 16)
 constexpr int kFPolThreads = 256;
-constexpr int kFPU = 2;                 // policies per thread and step in the policy kernel
+// Policies per thread and step in the policy kernel: 4 with 32-load tiles (two
+// policies' dependent gathers more in flight, at the same three waves per
+// SIMD), 2 with 16-load tiles (where 4 would cost a wave).
+template <int FL> constexpr int kFPU = FL == 16 ? 2 : 4;
 
 // Per sorted position k: the sorted wait and the context size there (below
 // 1 counts as 1; sort_prep_kernel has flagged it); per base sample: its
@@ -373,15 +376,15 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
         bc[l] = INFINITY;
         bf[l] = -1;
     }
-    // kFPU policies per thread and step: their slots, then their prefix
+    // kFPU<FL> policies per thread and step: their slots, then their prefix
     // values, are fetched together before any is used.  P < 2^24, so policy
     // indices are split in 32-bit arithmetic.
     const uint32_t B = blockDim.x, K2 = (uint32_t)tb.K2, P32 = (uint32_t)P;
-    for (uint32_t f0 = threadIdx.x; f0 < P32; f0 += kFPU * B) {
-        int32_t p1[kFPU], pe[kFPU];
-        double t1[kFPU], e[kFPU];
+    for (uint32_t f0 = threadIdx.x; f0 < P32; f0 += kFPU<FL> * B) {
+        int32_t p1[kFPU<FL>], pe[kFPU<FL>];
+        double t1[kFPU<FL>], e[kFPU<FL>];
 #pragma unroll
-        for (int u = 0; u < kFPU; ++u) {
+        for (int u = 0; u < kFPU<FL>; ++u) {
             const uint32_t f = (f0 + u * B < P32) ? f0 + u * B : f0;   // a repeat of f0 is skipped below
             const uint32_t a = f / K2, k = f - a * K2;
             t1[u] = tb.t1[a];
@@ -389,16 +392,16 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
             p1[u] = u1[a];
             pe[u] = ue[f];
         }
-        double n1[kFPU], ne[kFPU], s1[kFPU], se[kFPU];
+        double n1[kFPU<FL>], ne[kFPU<FL>], s1[kFPU<FL>], se[kFPU<FL>];
 #pragma unroll
-        for (int u = 0; u < kFPU; ++u) {
+        for (int u = 0; u < kFPU<FL>; ++u) {
             n1[u] = (double)nrow[p1[u]];
             ne[u] = (double)nrow[pe[u]];
             s1[u] = srow[p1[u]];
             se[u] = srow[pe[u]];
         }
 #pragma unroll
-        for (int u = 0; u < kFPU; ++u) {
+        for (int u = 0; u < kFPU<FL>; ++u) {
             const uint32_t f = f0 + u * B;
             if (f >= P32) break;
             const double hbm = s1[u] + t1[u] * (tot - n1[u]);
