@@ -322,12 +322,16 @@ int kvr_crossover_statistic(const double *d_wait_s, int64_t n, const kvr_prices 
                             void *hip_stream);
 
 /*
- * Instrumentation for benchmarks.  After this call, every kvr_cost_grid and
- * kvr_bootstrap call made from the same host thread records ev_begin (a
- * hipEvent_t) on its stream right before its main kernel -- the brute-force
- * grid kernel, or the first kernel of the sorted path -- and ev_end right
- * after the last kernel of that stage, so hipEventElapsedTime(ev_begin,
- * ev_end) is that stage's device time.  kvr_set_profile_events(NULL, NULL)
+ * Instrumentation for benchmarks.  After this call, every kvr_cost_grid,
+ * kvr_bootstrap, kvr_bootstrap_factored, kvr_capacity_replay and
+ * kvr_controller_select call made from the same host thread records ev_begin
+ * (a hipEvent_t) on its stream right before its main stage and ev_end right
+ * after it, so hipEventElapsedTime(ev_begin, ev_end) is that stage's device
+ * time.  The stage is the brute-force grid kernel alone (kvr_cost_grid with
+ * KVR_BRUTE, kvr_bootstrap), the whole sorted path from its first kernel
+ * (KVR_SORTED), the whole factored path (kvr_bootstrap_factored), the replay
+ * (kvr_capacity_replay), or the replay, count and final kernels
+ * (kvr_controller_select).  kvr_set_profile_events(NULL, NULL)
  * stops it.  These two handles, kept per host thread, are the only state the
  * library holds between calls; the events stay owned by the caller.
  * Returns KVR_E_NULL if exactly one of the two is NULL.
