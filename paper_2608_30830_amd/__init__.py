@@ -176,6 +176,17 @@ def _need_shape(t, shape, name):
         raise ValueError(f"{name} must have shape {tuple(shape)}, not {tuple(t.shape)}")
 
 
+def _on_stream(stream, *tensors) -> None:
+    """Tie buffers allocated here to a caller's stream: torch's caching
+    allocator then does not hand their memory out again before the work queued
+    on that stream has finished (the wrappers return before it has)."""
+    if stream is None:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(stream)
+
+
 def _workspace(nbytes: int, ws=None):
     torch = _torch()
     if ws is not None:
@@ -210,6 +221,7 @@ def kvr_cost_grid(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid, meth
     _check(lib.kvr_cost_grid(_ptr(wait_s), _ptr(ctx_tokens), n, ctypes.byref(prices),
                              ctypes.byref(grid.c), method, _ptr(cost), _ptr(perm), _ptr(ws),
                              ctypes.byref(have), st), "kvr_cost_grid")
+    _on_stream(stream, ws, cost, perm)
     if check:
         _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_cost_grid(device)")
     return (cost, perm) if want_perm else cost
@@ -229,6 +241,7 @@ def kvr_select_policy(cost, last_t2_is_inf: bool, stream=None) -> Tuple:
     _check(load_library().kvr_select_policy(_ptr(cost), batch, L, K1, K2, int(bool(last_t2_is_inf)),
                                             _ptr(best), _ptr(bc), _ptr(br), _stream_ptr(stream)),
            "kvr_select_policy")
+    _on_stream(stream, best, bc, br)
     shape = tuple(lead) + (L,)
     return best.reshape(shape), bc.reshape(shape), br.reshape(shape)
 
@@ -270,6 +283,7 @@ class BootstrapCall:
                        ctypes.byref(self.prices), ctypes.byref(self.grid.c), _ptr(self.best),
                        _ptr(self.best_cost), _ptr(self.cost), _ptr(self.ws),
                        ctypes.byref(self.ws_bytes), _stream_ptr(stream)), self.name)
+        _on_stream(stream, self.ws, self.best, self.best_cost, self.cost)
 
     def status(self, stream=None) -> int:
         return self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream))
@@ -328,6 +342,7 @@ def kvr_capacity_replay(arrival_s, wait_s, prices: kvr_prices, t2: Sequence[floa
                                    ctypes.byref(prices), t2c, K, _ptr(cost), _ptr(rest),
                                    _ptr(adm), _ptr(ws), ctypes.byref(have), st),
            "kvr_capacity_replay")
+    _on_stream(stream, ws, cost, rest, adm)
     if check:
         _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_capacity_replay(device)")
     return cost, rest, adm
@@ -369,6 +384,7 @@ class ControllerCall:
                                               _ptr(self.out), _ptr(self.ws), ctypes.byref(have),
                                               _stream_ptr(stream)),
                "kvr_controller_select")
+        _on_stream(stream, self.ws, self.out)
 
     def result(self, stream=None) -> kvr_controller_out:
         _check(self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream)),
@@ -404,6 +420,7 @@ def kvr_crossover_statistic(wait_s, prices: kvr_prices, stream=None, check: bool
     _check(lib.kvr_crossover_statistic(_ptr(wait_s), n, ctypes.byref(prices), _ptr(count),
                                        _ptr(frac), _ptr(ws), ctypes.byref(have), st),
            "kvr_crossover_statistic")
+    _on_stream(stream, ws, count, frac)
     if check:
         _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_crossover_statistic(device)")
     return count, frac
