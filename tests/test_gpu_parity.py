@@ -401,9 +401,16 @@ def test_binding_rejects_mismatched_arguments(kvr):
     assert tuple(cost.shape) == (3, 1, 9)
 
 
-def test_profile_events_bracket_the_grid_kernel(kvr):
-    """kvr_set_profile_events: the library records the caller's events around
-    its main kernel on the call's stream."""
+PROFILED_CALLS = ["bootstrap", "bootstrap_factored", "cost_grid_brute", "cost_grid_sorted",
+                  "capacity_replay", "controller_select"]
+
+
+@pytest.mark.parametrize("entry", PROFILED_CALLS)
+def test_profile_events_bracket_the_main_stage(kvr, entry):
+    """kvr_set_profile_events: every entry point that documents it records the
+    caller's two events around its main stage on the call's stream (fresh,
+    never-recorded events, so a call that skips them fails the elapsed-time
+    query)."""
     import ctypes
     import torch
     hip = ctypes.CDLL("libamdhip64.so")
@@ -416,11 +423,23 @@ def test_profile_events_bracket_the_grid_kernel(kvr):
         assert hip.hipEventCreate(ctypes.byref(e)) == 0
     wl = workloads.random_case(304, 20000, 2, 80, 8, resamples=8)
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
-    args = (_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()), _dev(wl.idx, _i32()),
-            _lib_prices(kvr, wl), g)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    pr = _lib_prices(kvr, wl)
+    if entry in ("capacity_replay", "controller_select"):
+        rc = workloads.replay_case("mixture", 0.5, reps=2, n=1000, seed=5)
+        arr, rw = _dev(rc.arrival_s, _f64()), _dev(rc.wait_s, _f64())
+    calls = {
+        "bootstrap": lambda: kvr.kvr_bootstrap(w, T, _dev(wl.idx, _i32()), pr, g),
+        "bootstrap_factored": lambda: kvr.kvr_bootstrap(w, T, _dev(wl.idx, _i32()), pr, g,
+                                                        factored=True),
+        "cost_grid_brute": lambda: kvr.kvr_cost_grid(w, T, pr, g, kvr.KVR_BRUTE),
+        "cost_grid_sorted": lambda: kvr.kvr_cost_grid(w, T, pr, g, kvr.KVR_SORTED),
+        "capacity_replay": lambda: kvr.kvr_capacity_replay(arr, rw, pr, [60.0, float("inf")]),
+        "controller_select": lambda: kvr.kvr_controller_select(arr, rw, pr, 0.5),
+    }
     kvr.kvr_set_profile_events(evs[0].value, evs[1].value)
     try:
-        kvr.kvr_bootstrap(*args)
+        calls[entry]()
     finally:
         kvr.kvr_set_profile_events(None, None)
     torch.cuda.synchronize()
