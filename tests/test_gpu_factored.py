@@ -50,13 +50,22 @@ def test_factored_random(kvr, oracle_mod, case):
     assert np.array_equal(_np(bc2), _np(bc))
 
 
-def _rows_agree(got, got_cost, want, want_cost, label):
+def _rows_agree(got, got_cost, want, want_cost, label, ref_row):
     """Where two selections differ, the two picks' best costs must agree to
-    rounding (a near tie); returns how many selections differ."""
+    rounding, and under the oracle's closed form of that row (ref_row(r):
+    cost[L, K1, K2]) both picks must lie within TIE_RTOL of the best (a near
+    tie); returns how many selections differ."""
     differ = np.argwhere(got != want)
+    rows = {}
     for r, l in differ:
         a, b = got_cost[r, l], want_cost[r, l]
         assert abs(a - b) <= (TIE_RTOL + RTOL) * abs(b), (label, r, l, a, b)
+        if r not in rows:
+            rows[r] = ref_row(r)
+        ref_l = rows[r][l].ravel()
+        lo = ref_l.min()
+        for pick in (got[r, l], want[r, l]):
+            assert ref_l[pick] - lo <= TIE_RTOL * abs(lo), (label, r, l, pick)
     print(f"[near-tie] {label}: {len(differ)} of {got.size} selections differ")
     return len(differ)
 
@@ -70,12 +79,16 @@ def test_factored_bench_workloads(kvr, oracle_mod, name):
     cb, cbc = oracle_mod.closed_form_bootstrap(wl.wait_s, wl.ctx_tokens, wl.idx, pr, wl.t1,
                                                wl.t2, wl.lam)
     assert_costs(fbc, cbc)
-    _rows_agree(fb, fbc, cb, cbc, f"{name} factored vs oracle closed form")
+
+    def ref_row(r):
+        return oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                           idx_row=wl.idx[r])
+    _rows_agree(fb, fbc, cb, cbc, f"{name} factored vs oracle closed form", ref_row)
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
     bb, bbc = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
                                 _dev(wl.idx, _i32()), _lib_prices(kvr, wl), g)
     assert_costs(fbc, _np(bbc))
-    _rows_agree(fb, fbc, _np(bb), _np(bbc), f"{name} factored vs brute")
+    _rows_agree(fb, fbc, _np(bb), _np(bbc), f"{name} factored vs brute", ref_row)
     # sampled rows against the double loop, element by element
     for r in (0, wl.n_resamples - 1):
         ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,

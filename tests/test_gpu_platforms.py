@@ -3,7 +3,8 @@ rows of one base sample, priced with each Table 3 vector (H100 NVL, A100 SXM,
 L40S; beta_2 = 0.02, C2 = 425).  The bootstrap entry point (every policy of
 every row, fused selection and the full cost tensor) and the SORTED path per
 family against the oracle's closed form: costs within 1e-9 relative, the
-selected policy identical up to rounding-level near ties."""
+selected policy identical up to rounding-level near ties; sampled host-timer
+columns of both against the oracle's double loop."""
 import numpy as np
 import pytest
 
@@ -48,6 +49,10 @@ def test_platform_bootstrap_rows(kvr, oracle_mod, case, platform):
         rb, rbc, _ = oracle_mod.select(ref, case.t2)
         assert_selection(ref, _np(best)[r], rb)
         assert_costs(_np(bc)[r], rbc)
+        cols = np.array([0, 64, 150, case.t2.size - 2, case.t2.size - 1])
+        loop = oracle_mod.cost_grid(case.wait_s, case.ctx_tokens, pr, case.t1, case.t2[cols],
+                                    case.lam, idx_row=case.idx[r])
+        assert_costs(_np(cost)[r][:, :, cols], loop)
 
 
 @pytest.mark.parametrize("platform", sorted(workloads.PLATFORM_PRICES))
@@ -62,3 +67,7 @@ def test_platform_sorted_per_family(kvr, oracle_mod, case, platform):
         ref = oracle_mod.closed_form_grid(w, T, pr, case.t1, case.t2, case.lam)
         assert_costs(_np(cost), ref)
         assert np.array_equal(_np(perm), oracle_mod.stable_order(w))
+        # and sampled host-timer columns against the double loop
+        cols = np.array([0, 37, 101, 180, case.t2.size - 2, case.t2.size - 1])
+        loop = oracle_mod.cost_grid(w, T, pr, case.t1, case.t2[cols], case.lam)
+        assert_costs(_np(cost)[:, :, cols], loop)
