@@ -322,14 +322,45 @@ int kvr_crossover_statistic(const double *d_wait_s, int64_t n, const kvr_prices 
                             void *hip_stream);
 
 /*
+ * For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): kvr_cost_grid
+ * without a workspace argument.  The workspace is a file-scope device array of
+ * KVR_NOALLOC_SCRATCH_BYTES inside the library, one copy per GPU, held from
+ * the library's load until the process ends; the call allocates and frees
+ * nothing.  Arguments, checks, layouts and results are those of kvr_cost_grid,
+ * with these differences:
+ *   - The workspace kvr_cost_grid would need (its d_ws == NULL size) must fit
+ *     KVR_NOALLOC_SCRATCH_BYTES, else KVR_E_SIZE and nothing is launched.  To
+ *     fit, KVR_BRUTE may sum a sample in fewer splits than kvr_cost_grid does;
+ *     costs then agree with kvr_cost_grid's to rounding (the splits are added
+ *     in another grouping), and are bit-identical whenever kvr_cost_grid's own
+ *     workspace fits.  About 1.6 million waits fit KVR_SORTED.
+ *   - d_status      device, int32 [1] or NULL: written at the end of the
+ *                   call's work on hip_stream with KVR_OK or KVR_E_DOMAIN (the
+ *                   device-detected errors that kvr_workspace_status reports
+ *                   for kvr_cost_grid).
+ *   - Every call on one GPU uses that GPU's single copy of the array: calls
+ *     queued on one stream are ordered, but calls that overlap in time on one
+ *     GPU (different streams, different host threads) race and give
+ *     meaningless results.  The array keeps the last call's contents; the
+ *     kernels clear whatever must start at zero.
+ *   - hip_stream must belong to a device of index < 64.
+ */
+#define KVR_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int kvr_cost_grid_noalloc(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                          const kvr_prices *p, const kvr_policy_grid *g, int32_t method,
+                          double *d_cost, int32_t *d_perm, int32_t *d_status, void *hip_stream);
+
+/*
  * Instrumentation for benchmarks.  After this call, every kvr_cost_grid,
- * kvr_bootstrap, kvr_bootstrap_factored, kvr_capacity_replay and
- * kvr_controller_select call made from the same host thread records ev_begin
- * (a hipEvent_t) on its stream right before its main stage and ev_end right
- * after it, so hipEventElapsedTime(ev_begin, ev_end) is that stage's device
- * time.  The stage is the brute-force grid kernel alone (kvr_cost_grid with
- * KVR_BRUTE, kvr_bootstrap), the whole sorted path from its first kernel
- * (KVR_SORTED), the whole factored path (kvr_bootstrap_factored), the replay
+ * kvr_cost_grid_noalloc, kvr_bootstrap, kvr_bootstrap_factored,
+ * kvr_capacity_replay and kvr_controller_select call made from the same host
+ * thread records ev_begin (a hipEvent_t) on its stream right before its main
+ * stage and ev_end right after it, so hipEventElapsedTime(ev_begin, ev_end) is
+ * that stage's device time.  The stage is the brute-force grid kernel alone
+ * (kvr_cost_grid and kvr_cost_grid_noalloc with KVR_BRUTE, kvr_bootstrap), the
+ * whole sorted path from its first kernel (KVR_SORTED), the whole factored
+ * path (kvr_bootstrap_factored), the replay
  * (kvr_capacity_replay), or the replay, count and final kernels
  * (kvr_controller_select).  kvr_set_profile_events(NULL, NULL)
  * stops it.  These two handles, kept per host thread, are the only state the

@@ -29,7 +29,8 @@ KVR_SORTED = 1
 KVR_RETAIN = 0
 KVR_EXPIRE = 1
 
-EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_select_policy", "kvr_bootstrap",
+EXPORTS = ("kvr_prices_from_platform", "kvr_cost_grid", "kvr_cost_grid_noalloc",
+           "kvr_select_policy", "kvr_bootstrap",
            "kvr_bootstrap_factored", "kvr_eq3_timer", "kvr_capacity_replay",
            "kvr_controller_select", "kvr_crossover_statistic", "kvr_workspace_status",
            "kvr_set_profile_events", "kvr_status_string")
@@ -82,6 +83,9 @@ def load_library(path: str = LIB_PATH):
     lib.kvr_cost_grid.argtypes = [P, P, I64, ctypes.POINTER(kvr_prices),
                                   ctypes.POINTER(kvr_policy_grid), I32, P, P, P, SZ, P]
     lib.kvr_cost_grid.restype = ctypes.c_int
+    lib.kvr_cost_grid_noalloc.argtypes = [P, P, I64, ctypes.POINTER(kvr_prices),
+                                          ctypes.POINTER(kvr_policy_grid), I32, P, P, P, P]
+    lib.kvr_cost_grid_noalloc.restype = ctypes.c_int
     lib.kvr_select_policy.argtypes = [P, I64, I32, I32, I32, I32, P, P, P, P]
     lib.kvr_select_policy.restype = ctypes.c_int
     lib.kvr_bootstrap.argtypes = [P, P, I64, P, I64, I64, ctypes.POINTER(kvr_prices),
@@ -225,6 +229,43 @@ def kvr_cost_grid(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid, meth
     if check:
         _check(lib.kvr_workspace_status(_ptr(ws), st), "kvr_cost_grid(device)")
     return (cost, perm) if want_perm else cost
+
+
+NOALLOC_SCRATCH_BYTES = 64 << 20   # KVR_NOALLOC_SCRATCH_BYTES
+
+
+def kvr_cost_grid_noalloc(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid,
+                          method: int = KVR_BRUTE, cost=None, perm=None, status=None,
+                          stream=None):
+    """kvr_cost_grid with the library's static device scratch as workspace: the
+    library allocates nothing.  ``cost`` ([n_lam, n_t1, n_t2] float64), ``perm``
+    ([n] int32, KVR_SORTED only) and ``status`` ([1] int32: KVR_OK or
+    KVR_E_DOMAIN once the stream reaches the end of the call) are caller tensors
+    (allocated here when None); returns (cost, perm, status) without
+    synchronising."""
+    torch = _torch()
+    _need(wait_s, torch.float64, "wait_s")
+    _need(ctx_tokens, torch.int32, "ctx_tokens")
+    n = wait_s.numel()
+    _need_shape(ctx_tokens, wait_s.shape, "ctx_tokens")
+    if cost is None:
+        cost = torch.empty((grid.n_lam, grid.n_t1, grid.n_t2), dtype=torch.float64, device="cuda")
+    _need(cost, torch.float64, "cost")
+    _need_shape(cost, (grid.n_lam, grid.n_t1, grid.n_t2), "cost")
+    if perm is not None:
+        _need(perm, torch.int32, "perm")
+        _need_shape(perm, (n,), "perm")
+    if status is None:
+        status = torch.empty(1, dtype=torch.int32, device="cuda")
+    _need(status, torch.int32, "status")
+    _need_shape(status, (1,), "status")
+    _check(load_library().kvr_cost_grid_noalloc(_ptr(wait_s), _ptr(ctx_tokens), n,
+                                                ctypes.byref(prices), ctypes.byref(grid.c),
+                                                method, _ptr(cost), _ptr(perm), _ptr(status),
+                                                _stream_ptr(stream)),
+           "kvr_cost_grid_noalloc")
+    _on_stream(stream, cost, perm, status)
+    return cost, perm, status
 
 
 def kvr_select_policy(cost, last_t2_is_inf: bool, stream=None) -> Tuple:

@@ -31,8 +31,11 @@ int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 // is no split (the selection is fused into the grid kernel).  Otherwise the
 // samples are cut into splits of >= 2,048 samples, or of >= 512 samples when
 // that is what it takes to give every resident slot a wave; never more than
-// 16 rounds of waves, and never more than 1 GiB of split partials.
-int64_t choose_splits(int64_t base_waves, int64_t m, int64_t partial_doubles_per_split)
+// 16 rounds of waves, and never more than part_cap bytes (1 GiB unless the
+// caller's workspace is bounded) of split partials.
+constexpr int64_t kPartCapBytes = int64_t(1) << 30;
+int64_t choose_splits(int64_t base_waves, int64_t m, int64_t partial_doubles_per_split,
+                      int64_t part_cap)
 {
     constexpr int64_t kSlots = 4096, kFull = 32768, kMaxRounds = 16;
     if (base_waves >= kFull) return 1;
@@ -40,7 +43,7 @@ int64_t choose_splits(int64_t base_waves, int64_t m, int64_t partial_doubles_per
     if (base_waves * ns < kSlots)
         ns = std::max<int64_t>(1, std::min<int64_t>(m / 512, cdiv(kSlots, base_waves)));
     ns = std::min<int64_t>(ns, cdiv(kMaxRounds * kSlots, base_waves));
-    const int64_t mem_cap = std::max<int64_t>(1, (int64_t(1) << 30) / 8 / partial_doubles_per_split);
+    const int64_t mem_cap = std::max<int64_t>(1, part_cap / 8 / partial_doubles_per_split);
     return std::max<int64_t>(1, std::min<int64_t>(ns, mem_cap));
 }
 
@@ -134,7 +137,7 @@ int choose_tile(int32_t L)
 }
 
 BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, bool bootstrap,
-                     bool want_cost)
+                     bool want_cost, int64_t part_cap = kPartCapBytes)
 {
     const int32_t K1 = g.n_t1, K2 = g.n_t2, L = g.n_lam;
     BrutePlan bp{};
@@ -152,7 +155,7 @@ BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, 
     else gp.mode = kvr::kModeRows2;
     gp.ngroups = (gp.mode == kvr::kModePerLane) ? R * gp.nblk : cdiv(R * P, kvr::kWave);
     const int64_t base_waves = gp.ngroups * gp.ntiles;
-    const int64_t target = choose_splits(base_waves, m, R * gp.ntiles * gp.LT * P);
+    const int64_t target = choose_splits(base_waves, m, R * gp.ntiles * gp.LT * P, part_cap);
     const int64_t split_len = cdiv(cdiv(m, target), kvr::kChunk) * kvr::kChunk;
     const int64_t nsplit = cdiv(m, split_len);
     gp.nsplit = (int)nsplit;
@@ -296,9 +299,16 @@ int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
     return KVR_OK;
 }
 
-int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
-                  const kvr_prices *p, const kvr_policy_grid *g, int32_t method, double *d_cost,
-                  int32_t *d_perm, void *d_ws, size_t *ws_bytes, void *hip_stream)
+}  // extern "C"
+
+// kvr_cost_grid with an optional bound on the workspace: with fit_bytes > 0
+// the brute-force plan takes fewer sample splits when its split partials would
+// otherwise push the workspace beyond fit_bytes (same result up to the order
+// in which the splits are summed).
+int kvr::cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                         const kvr_prices *p, const kvr_policy_grid *g, int32_t method,
+                         double *d_cost, int32_t *d_perm, void *d_ws, size_t *ws_bytes,
+                         size_t fit_bytes, void *hip_stream)
 {
     if (!ws_bytes) return KVR_E_NULL;
     int rc;
@@ -314,6 +324,11 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     int32_t Lpad = g->n_lam;
     if (method == KVR_BRUTE) {
         bp = plan_brute(1, n, n, *g, false, true);
+        if (fit_bytes > 0 && bp.total > fit_bytes && !bp.fused) {
+            const size_t part = bp.total - bp.off_part;   // the partials are carved last
+            if (bp.total - part < fit_bytes)
+                bp = plan_brute(1, n, n, *g, false, true, (int64_t)(fit_bytes - (bp.total - part)));
+        }
         if (bp.max_blocks > INT32_MAX) return KVR_E_SIZE;
         need = bp.total;
     } else {
@@ -357,6 +372,16 @@ int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     KVR_TRY(kvr::launch_sorted_path(d_wait_s, d_ctx_tokens, n, tb, pr, sws, d_cost, d_perm, status, s));
     KVR_MARK(g_prof_end, s);
     return KVR_OK;
+}
+
+extern "C" {
+
+int kvr_cost_grid(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                  const kvr_prices *p, const kvr_policy_grid *g, int32_t method, double *d_cost,
+                  int32_t *d_perm, void *d_ws, size_t *ws_bytes, void *hip_stream)
+{
+    return kvr::cost_grid_entry(d_wait_s, d_ctx_tokens, n, p, g, method, d_cost, d_perm, d_ws,
+                                ws_bytes, 0, hip_stream);
 }
 
 int kvr_select_policy(const double *d_cost, int64_t batch, int32_t n_lam, int32_t n_t1,

@@ -32,6 +32,17 @@ hipError_t launch_clear_status(int *status, hipStream_t stream)
     return hipGetLastError();
 }
 
+__global__ void export_status_kernel(const int *status, int32_t *out)
+{
+    if (threadIdx.x == 0) out[0] = status[0] == 0 ? KVR_OK : KVR_E_DOMAIN;
+}
+
+hipError_t launch_export_status(const int *status, int32_t *out, hipStream_t stream)
+{
+    hipLaunchKernelGGL(export_status_kernel, dim3(1), dim3(64), 0, stream, status, out);
+    return hipGetLastError();
+}
+
 // Clears the status word and stores up to three host tables in one launch
 // when they fit one payload together.
 struct StagePlan {

@@ -70,8 +70,18 @@ struct R3Ws {
     int64_t split_len;
 };
 
+// kvr_cost_grid (same arguments, checks and results) with an optional bound on
+// the workspace: fit_bytes > 0 makes the brute-force plan take fewer sample
+// splits where its split partials would push the workspace beyond fit_bytes.
+int cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n,
+                    const kvr_prices *p, const kvr_policy_grid *g, int32_t method,
+                    double *d_cost, int32_t *d_perm, void *d_ws, size_t *ws_bytes,
+                    size_t fit_bytes, void *hip_stream);
+
 // ---- launches (all asynchronous on `stream`) --------------------------------
 hipError_t launch_clear_status(int *status, hipStream_t stream);
+// out[0] = KVR_OK or KVR_E_DOMAIN from a workspace status word.
+hipError_t launch_export_status(const int *status, int32_t *out, hipStream_t stream);
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
 hipError_t launch_stage(int *status, double *const dst[3], const double *const src[3],
                         const int64_t cnt[3], hipStream_t stream);

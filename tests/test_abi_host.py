@@ -403,3 +403,42 @@ def test_product_path_has_no_cpu_fallback():
     src = open(os.path.join(ROOT, "paper_2608_30830_amd", "__init__.py")).read()
     assert "oracle" not in src
     assert "numpy" not in src
+
+
+def _noalloc_rc(lib, grid, n, method=kvr.KVR_SORTED, prices=None, perm=None, cost=FAKE):
+    pr = prices if prices is not None else _prices()
+    return lib.kvr_cost_grid_noalloc(FAKE, FAKE, n, ctypes.byref(pr), ctypes.byref(grid.c),
+                                     method, cost, perm, None, None)
+
+
+def test_noalloc_rejects_on_the_host(lib):
+    """kvr_cost_grid_noalloc: the checks of kvr_cost_grid, and a workspace that
+    would not fit the static scratch is KVR_E_SIZE, all before any device
+    work (FAKE pointers are never touched)."""
+    g = kvr.PolicyGrid([0.0], [10.0, 100.0, math.inf], [0.1, 0.9])
+    bad = _prices()
+    bad.b3_per_token = -1.0
+    assert _noalloc_rc(lib, g, 100, prices=bad) == kvr.KVR_E_PRICE
+    assert _noalloc_rc(lib, g, 0) == kvr.KVR_E_SIZE
+    assert _noalloc_rc(lib, g, 100, method=7) == kvr.KVR_E_METHOD
+    assert _noalloc_rc(lib, g, 100, method=kvr.KVR_BRUTE, perm=FAKE) == kvr.KVR_E_METHOD
+    assert _noalloc_rc(lib, g, 100, cost=None) == kvr.KVR_E_NULL
+    assert lib.kvr_cost_grid_noalloc(FAKE, FAKE, 100, None, ctypes.byref(g.c), 0, FAKE, None,
+                                     None, None) == kvr.KVR_E_NULL
+    # the sorted path needs about 40 bytes per wait: 2^21 waits exceed 64 MiB
+    need = ctypes.c_size_t(0)
+    pr = _prices()
+    for n in (1 << 21, (1 << 31) - 1):
+        assert lib.kvr_cost_grid(None, None, n, ctypes.byref(pr), ctypes.byref(g.c),
+                                 kvr.KVR_SORTED, None, None, None, ctypes.byref(need),
+                                 None) == kvr.KVR_OK
+        assert need.value > kvr.NOALLOC_SCRATCH_BYTES
+        assert _noalloc_rc(lib, g, n) == kvr.KVR_E_SIZE
+    # brute force with more waits than the deadline bins of 64 MiB can hold
+    assert _noalloc_rc(lib, g, 1 << 24, method=kvr.KVR_BRUTE) == kvr.KVR_E_SIZE
+
+
+def test_noalloc_scratch_size_matches_header(lib):
+    text = open(HEADER).read()
+    m = re.search(r"#define KVR_NOALLOC_SCRATCH_BYTES \(\(size_t\)(\d+) << (\d+)\)", text)
+    assert m and int(m.group(1)) << int(m.group(2)) == kvr.NOALLOC_SCRATCH_BYTES
