@@ -20,6 +20,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "kvr_oracle.c")
+# KVR_ORACLE_LIBRARY names another build of the oracle (e.g. one compiled with
+# sanitizers), loaded as it is, without rebuilding.
+_LIB_OVERRIDE = os.environ.get("KVR_ORACLE_LIBRARY")
 _LIB = os.path.join(_HERE, "_build", "liboracle.so")
 _lib = None
 
@@ -73,8 +76,11 @@ def compile_library(src: str, out: str) -> None:
 def _load():
     global _lib
     if _lib is None:
-        build()
-        _lib = _configure(ctypes.CDLL(_LIB))
+        if _LIB_OVERRIDE:
+            _lib = _configure(ctypes.CDLL(_LIB_OVERRIDE))
+        else:
+            build()
+            _lib = _configure(ctypes.CDLL(_LIB))
     return _lib
 
 

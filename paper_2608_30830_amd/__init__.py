@@ -13,7 +13,9 @@ import os
 from typing import Optional, Sequence, Tuple
 
 _PKG = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_PKG, "_build", "libkvr.so")
+# KVR_LIBRARY names another build of the same library (e.g. one whose host
+# code is compiled with sanitizers); by default the in-tree build is loaded.
+LIB_PATH = os.environ.get("KVR_LIBRARY") or os.path.join(_PKG, "_build", "libkvr.so")
 
 KVR_OK = 0
 KVR_E_NULL = -1
