@@ -117,8 +117,11 @@ def main() -> int:
     ap.add_argument("--resamples", type=int, default=None,
                     help="truncate the bootstrap batch (for quick local runs)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--cpu-rows", type=int, default=2,
-                    help="bootstrap rows the CPU oracle evaluates for cpu_baseline")
+    ap.add_argument("--cpu-rows", type=int, default=16,
+                    help="bootstrap rows (evenly spaced, r = q * R / rows) the CPU oracle "
+                         "evaluates for cpu_baseline")
+    ap.add_argument("--cpu-draws", default="512,8192",
+                    help="draws per row for the 1-thread and the all-thread oracle legs")
     ap.add_argument("--paths", action="store_true",
                     help="also time the other entry points on their workloads")
     ap.add_argument("--table", action="store_true",
@@ -173,6 +176,9 @@ def main() -> int:
     idx = torch.as_tensor(wl.idx, dtype=torch.int32).to(dev)
     call = kvr.BootstrapCall(w, T, idx, prices, grid)
     evals = wl.evaluations
+    inputs = {"wait_s_sha256": sha256_of(wl.wait_s), "ctx_tokens_sha256": sha256_of(wl.ctx_tokens),
+              "idx_sha256": sha256_of(wl.idx)}
+    hbm_copy = copy_rate(torch)
 
     log(f"[bench] warmup {args.warmup} step(s)")
     for _ in range(args.warmup):
@@ -184,7 +190,9 @@ def main() -> int:
 
     log(f"[bench] timing {args.steps} step(s)")
     ev = HipEvents(2 * args.steps)
+    clock = ClockSampler()
     torch.cuda.synchronize()
+    clock.start()
     t0 = time.perf_counter()
     for i in range(args.steps):
         kvr.kvr_set_profile_events(ev.ev[2 * i].value, ev.ev[2 * i + 1].value)
@@ -192,6 +200,7 @@ def main() -> int:
     kvr.kvr_set_profile_events(None, None)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
+    clock.stop()
     st = call.status()
     if st != kvr.KVR_OK:
         raise kvr.KvrError(st, "timed steps")
@@ -224,13 +233,19 @@ def main() -> int:
                      "traffic": counter_traffic(args.workload, wl.n_resamples),
                      "kernel": "grid_kernel<32,1>", "kernel_ms": kernel_ms,
                      "flops_per_launch": 2.0 * evals},
+        "inputs": inputs,
+        "gpu_sclk_mhz": clock.summary(),
+        "hbm_copy": hbm_copy,
     }
 
     if args.paths:
         out["paths"] = time_paths(kvr, workloads, torch)
 
     if not args.no_cpu_baseline:
-        out["cpu_baseline"] = cpu_baseline(wl, args.cpu_rows)
+        draws = [int(x) for x in args.cpu_draws.split(",")]
+        out["cpu_baseline"], out["parity"] = cpu_leg(wl, args.cpu_rows, draws,
+                                                     call.best.cpu().numpy(),
+                                                     call.best_cost.cpu().numpy())
 
     print(json.dumps(out), flush=True)
     return 0
@@ -424,21 +439,158 @@ def time_controller(kvr, workloads, torch, pr, reps: int):
     return res
 
 
-def cpu_baseline(wl, rows: int):
-    """The oracle double loop on the first ``rows`` bootstrap rows, all policies
-    and loads; scaled to evaluations per second."""
+def sha256_of(arr) -> str:
+    import numpy as np
+    return hashlib.sha256(np.ascontiguousarray(arr).tobytes()).hexdigest()
+
+
+def copy_rate(torch):
+    """A plain 2 GiB device-to-device copy (median of 5, torch events): the
+    practical HBM ceiling of this machine, read + write bytes per second."""
+    n = 1 << 28
+    x = torch.empty(n, dtype=torch.float64, device="cuda")
+    y = torch.empty_like(x)
+    ms = _median_ms(torch, lambda: y.copy_(x), 5)
+    del x, y
+    torch.cuda.empty_cache()
+    return {"bytes": 2 * 8 * n, "ms": ms, "tbps": 2 * 8 * n / (ms * 1e-3) / 1e12,
+            "frac_of_peak": 2 * 8 * n / (ms * 1e-3) / (HBM_PEAK_TBS * 1e12)}
+
+
+class ClockSampler:
+    """Samples the GPU's current shader clock (the starred level of the
+    driver's pp_dpm_sclk table) every 0.25 s while the timed steps run."""
+
+    def __init__(self):
+        import glob
+        files = sorted(glob.glob("/sys/class/drm/card*/device/pp_dpm_sclk"))
+        self.path = files[0] if files else None
+        self.samples = []
+        self._stop = None
+
+    def _read(self):
+        try:
+            with open(self.path) as fh:
+                for line in fh:
+                    if "*" in line:
+                        return float(line.split(":")[1].strip().split("Mhz")[0].split("MHz")[0])
+        except (OSError, ValueError, IndexError):
+            return None
+        return None
+
+    def start(self):
+        if self.path is None:
+            return
+        import threading
+        self._stop = threading.Event()
+
+        def loop():
+            while not self._stop.wait(0.25):
+                v = self._read()
+                if v is not None:
+                    self.samples.append(v)
+        self._thread = threading.Thread(target=loop, daemon=True)
+        self._thread.start()
+
+    def stop(self):
+        if self._stop is not None:
+            self._stop.set()
+            self._thread.join()
+
+    def summary(self):
+        if not self.samples:
+            return None
+        s = sorted(self.samples)
+        return {"samples": len(s), "min": s[0], "median": s[len(s) // 2], "max": s[-1],
+                "source": "pp_dpm_sclk, every 0.25 s during the timed steps"}
+
+
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_leg(wl, rows: int, draws, gpu_best, gpu_best_cost):
+    """The cpu_baseline leg.  (1) The oracle's double loop, as it stands, on a
+    bounded sample of the same workload: ``rows`` evenly spaced bootstrap rows
+    (r = q * R / rows), each cut to its first draws (draws[0] on one thread,
+    draws[1] on every thread), every policy and load; the rate is extrapolated
+    linearly in evaluations to the whole workload.  (2) A parity sample of the
+    timed call: the GPU's selections and best costs on the same rows (full
+    length) against the oracle's closed form."""
+    import numpy as np
     import oracle
     pr = oracle.workload_prices(wl)
-    log(f"[bench] cpu baseline: oracle on {rows} row(s) with {oracle.num_threads()} threads")
-    t0 = time.perf_counter()
-    for r in range(rows):
-        oracle.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam, idx_row=wl.idx[r])
-    dt = time.perf_counter() - t0
-    ev = rows * wl.m * wl.t1.size * wl.t2.size * wl.lam.size
-    return {"value": ev / dt, "unit": "evaluations/s", "cores": oracle.num_threads(),
-            "kind": "oracle", "seconds": dt,
-            "sample": f"{rows} of {wl.n_resamples} bootstrap rows, every policy and load "
-                      f"({ev:.3e} evaluations)"}
+    R = wl.n_resamples
+    sel = sorted({(q * R) // rows for q in range(rows)}) if wl.idx is not None else [None]
+    per_draw = wl.t1.size * wl.t2.size * wl.lam.size
+    all_threads = oracle.num_threads()
+    legs = {}
+    for threads, cut in ((1, draws[0]), (all_threads, draws[1])):
+        cut = min(cut, wl.m)
+        oracle.set_num_threads(threads)
+        log(f"[bench] cpu baseline: oracle on {len(sel)} row(s) x {cut} draws, {threads} thread(s)")
+        t0 = time.perf_counter()
+        for r in sel:
+            if r is None:
+                oracle.cost_grid(wl.wait_s[:cut], wl.ctx_tokens[:cut], pr, wl.t1, wl.t2, wl.lam)
+            else:
+                oracle.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                 idx_row=wl.idx[r][:cut])
+        dt = time.perf_counter() - t0
+        ev = len(sel) * cut * per_draw
+        legs[threads] = {"value": ev / dt, "cores": threads, "seconds": dt, "evaluations": ev,
+                         "draws_per_row": cut,
+                         "whole_workload_seconds": wl.evaluations / (ev / dt)}
+    oracle.set_num_threads(all_threads)
+    rows_txt = (f"rows r = q * {R // rows} (q = 0..{len(sel) - 1}) of {R}" if wl.idx is not None
+                else "a prefix of the sample")
+    base = dict(legs[all_threads])
+    base.update({
+        "unit": "evaluations/s", "kind": "oracle",
+        "sample": f"{rows_txt}, first {legs[all_threads]['draws_per_row']} draws of each "
+                  f"(all threads) / first {legs[1]['draws_per_row']} (one thread), every "
+                  f"policy and load",
+        "single_thread": legs[1], "all_threads": legs[all_threads],
+        "extrapolated": True,
+        "extrapolation": "linear in evaluations: whole-workload seconds = evaluations per step "
+                         "/ measured rate",
+        "cpu_model": cpu_model(), "os_cpu_count": os.cpu_count(),
+        "affinity_cpus": len(os.sched_getaffinity(0)),
+    })
+    # parity sample of the timed call on the same rows, full length
+    parity = {"reference": "oracle closed form (sorted prefix sums), full rows",
+              "rows": [r for r in sel if r is not None]}
+    if wl.idx is not None:
+        mism, near, err, gap = 0, 0, 0.0, float("inf")
+        for r in sel:
+            ref = oracle.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                          idx_row=wl.idx[r])
+            rb, rbc, _ = oracle.select(ref, wl.t2)
+            err = max(err, float(np.max(np.abs(gpu_best_cost[r] - rbc) / np.abs(rbc))))
+            flat = ref.reshape(ref.shape[0], -1)
+            for l in range(flat.shape[0]):
+                if gpu_best[r, l] != rb[l]:
+                    c_gpu, c_ref = flat[l, gpu_best[r, l]], flat[l, rb[l]]
+                    if abs(c_gpu - c_ref) <= 1e-11 * abs(c_ref):
+                        near += 1
+                    else:
+                        mism += 1
+                row = np.sort(flat[l])
+                higher = row[row > row[0]]
+                if higher.size and row[0] != 0:
+                    gap = min(gap, float((higher[0] - row[0]) / abs(row[0])))
+        parity.update({"index_mismatches": mism, "near_tie_picks": near,
+                       "max_rel_err_best_cost": err, "min_runner_up_gap": gap})
+        log(f"[bench] parity on {len(sel)} rows: {mism} mismatches, {near} near ties, "
+            f"max rel err {err:.2e}, smallest runner-up gap {gap:.2e}")
+    return base, parity
 
 
 def _median_ms(torch, run, reps=5):

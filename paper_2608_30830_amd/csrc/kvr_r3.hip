@@ -9,9 +9,11 @@
 // w > e_p holds exactly when c(w) > lb_p (every deadline below e_p is below
 // w, and so is e_p; conversely w <= e_p leaves no deadline below w that is
 // not below e_p).  So with hist[b] = sum of T over draws whose wait has
-// c(w) = b, R3(e_p) = sum_{b > lb_p} hist[b], a suffix sum.  Each t1 row of
-// deadlines is non-decreasing in t2 (t2 ascending, rounding monotone), so
-// c(x) is a sum of one binary search per row; no sort is needed.  A finite
+// c(w) = b, R3(e_p) = sum_{b > lb_p} hist[b], a suffix sum.  The deadlines
+// are non-decreasing along each t1 row (t2 ascending) and along each t2
+// column (t1 ascending), rounding being monotone, so c(x) is a sum of one
+// binary search per row or per column, whichever are fewer: at most
+// min(K1, K2) <= 4,096 searches per item, and no sort is needed.  A finite
 // wait has c(w) <= F, the number of finite deadlines, and bin 0 never enters
 // a suffix that is read (lb_p + 1 >= 1), so only bins 1..F are kept, stored
 // at b - 1: S[r][x] = R3 of any policy with lb_p = x, and R3 = 0 when
@@ -33,15 +35,28 @@ constexpr int kR3Unroll = 4;           // draws per thread and step, fetched tog
 __device__ int32_t deadlines_below(const Tables &tb, double x)
 {
     int32_t c = 0;
-    for (int a = 0; a < tb.K1; ++a) {
-        const double t1 = tb.t1[a];
-        int lo = 0, hi = tb.K2;   // first k with t1 + t2[k] >= x
-        while (lo < hi) {
-            const int mid = (lo + hi) >> 1;
-            if (t1 + tb.t2[mid] < x) lo = mid + 1;
-            else hi = mid;
+    if (tb.K1 <= tb.K2) {
+        for (int a = 0; a < tb.K1; ++a) {
+            const double t1 = tb.t1[a];
+            int lo = 0, hi = tb.K2;   // first k with t1 + t2[k] >= x
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (t1 + tb.t2[mid] < x) lo = mid + 1;
+                else hi = mid;
+            }
+            c += lo;
         }
-        c += lo;
+    } else {
+        for (int k = 0; k < tb.K2; ++k) {
+            const double t2 = tb.t2[k];
+            int lo = 0, hi = tb.K1;   // first a with t1[a] + t2 >= x
+            while (lo < hi) {
+                const int mid = (lo + hi) >> 1;
+                if (tb.t1[mid] + t2 < x) lo = mid + 1;
+                else hi = mid;
+            }
+            c += lo;
+        }
     }
     return c;
 }

@@ -38,3 +38,24 @@ def test_grid_hash_covers_the_kernel_sources():
     for rel in bench.GRID_SOURCES:
         assert os.path.exists(os.path.join(ROOT, rel)), rel
     assert "paper_2608_30830_amd/csrc/kvr_grid.hip" in bench.GRID_SOURCES
+
+
+def test_cpu_leg_reports_both_legs_and_a_parity_sample():
+    """cpu_baseline: a one-thread and an all-thread leg on evenly spaced rows,
+    extrapolated linearly, with the CPU model; the parity sample compares the
+    selections handed to it (here the oracle's own) with the closed form."""
+    import oracle
+    import workloads
+    wl = workloads.make("twotier-4096x64k", resamples=32)
+    pr = oracle.workload_prices(wl)
+    best, bc = oracle.closed_form_bootstrap(wl.wait_s, wl.ctx_tokens, wl.idx, pr, wl.t1, wl.t2,
+                                            wl.lam)
+    base, parity = bench.cpu_leg(wl, 16, [4, 16], best, bc)
+    assert base["kind"] == "oracle" and base["extrapolated"] is True
+    assert base["single_thread"]["cores"] == 1 and base["single_thread"]["draws_per_row"] == 4
+    assert base["cores"] == oracle.num_threads() and base["all_threads"]["draws_per_row"] == 16
+    assert base["value"] == base["all_threads"]["value"] > 0
+    assert base["all_threads"]["evaluations"] == 16 * 16 * 64 * 257 * 32
+    assert base["cpu_model"] and base["os_cpu_count"] >= 1
+    assert parity["rows"] == list(range(0, 32, 2))
+    assert parity["index_mismatches"] == 0 and parity["max_rel_err_best_cost"] == 0.0

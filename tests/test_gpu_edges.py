@@ -218,3 +218,40 @@ def test_twotier_full_cost_tensors(kvr, oracle_mod):
         assert_costs(_np(bc)[r], rbc)
         print(f"[twotier] row {r}: max rel err {H.rel_err(host[r], ref).max():.2e}, "
               f"{n} near-tie picks, smallest runner-up gap {H.min_runner_up_gap(ref):.2e}")
+
+
+def test_tall_grid_many_t1_timers(kvr, oracle_mod):
+    """2^20 GPU-tier timers x {300 s, inf}: the deadline count behind the
+    recompute share searches along the short axis (two columns), so the call
+    stays short; BRUTE, SORTED and a two-row bootstrap against the double loop."""
+    import time
+    import torch
+    wl = workloads.random_case(421, 500, 1, 2, 1, resamples=2, ties=True)
+    wl.t1 = np.concatenate([[0.0], np.geomspace(1e-3, 5000.0, (1 << 20) - 1)])
+    assert np.all(np.diff(wl.t1) > 0)
+    wl.t2 = np.array([300.0, np.inf])
+    wl.lam = np.array([0.9])
+    pr = oracle_mod.workload_prices(wl)
+    g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+    lp = _lib_prices(kvr, wl)
+    w, T = _dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32())
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    rb = oracle_mod.select(ref, wl.t2)[0]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    brute = kvr.kvr_cost_grid(w, T, lp, g, method=kvr.KVR_BRUTE)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    sorted_cost = kvr.kvr_cost_grid(w, T, lp, g, method=kvr.KVR_SORTED)
+    for c in (brute, sorted_cost):
+        assert_costs(_np(c), ref)
+        assert_selection(ref, _np(kvr.kvr_select_policy(c, g.last_inf)[0]), rb)
+    best, bc = kvr.kvr_bootstrap(w, T, _dev(wl.idx, _i32()), lp, g)
+    for r in range(2):
+        rr = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                  idx_row=wl.idx[r])
+        rsel, rbc, _ = oracle_mod.select(rr, wl.t2)
+        assert_selection(rr, _np(best)[r], rsel)
+        assert_costs(_np(bc)[r], rbc)
+    print(f"[tall] 2^21 policies, 500 waits: brute call {elapsed * 1e3:.1f} ms")
+    assert elapsed < 5.0
