@@ -76,27 +76,79 @@ void sort_ws_carve(void *base, int64_t n, SortWs &ws)
     ws.blkS = (double *)take(sizeof(double) * ws.nblocks_scan);
 }
 
-// Keys from waits (domain-checked on the bits), identity payload.
-__global__ void __launch_bounds__(256) sort_prep_kernel(const double *__restrict__ w,
-                                                        const int32_t *__restrict__ T, int64_t n,
-                                                        uint64_t *__restrict__ keys,
-                                                        int32_t *__restrict__ vals, int *status)
+// Sort tiles are numbered so that each XCD takes a contiguous range of them:
+// neighbouring tiles share the cache lines of the digit-major histogram and of
+// its scanned offsets, and then share them in one L2.
+__device__ __forceinline__ int sort_tile(int nblocks)
 {
-    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i >= n) return;
-    uint64_t b = (uint64_t)__double_as_longlong(w[i]);
-    if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
-    if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
-        flag_domain(status);
-        b = 0;
+    return (int)xcd_logical_block(blockIdx.x, nblocks);
+}
+
+// Keys from waits (domain-checked on the bits), the payload (the context size
+// when the caller needs only the prefix sums, else the base index), and the
+// tile histograms of the first digit pass, so that pass reads no keys again.
+// Tiles are those of the digit passes (256 * KPT keys); digit-major histogram
+// hist[d * nblocks + tile].
+template <int KPT>
+__global__ void __launch_bounds__(kSortThreads) sort_prep_kernel(
+    const double *__restrict__ w, const int32_t *__restrict__ T, int64_t n, int payload_T,
+    uint64_t *__restrict__ keys, int32_t *__restrict__ vals, uint32_t *__restrict__ hist,
+    int nblocks, int *status)
+{
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int tile = sort_tile(nblocks);
+    const int64_t base = (int64_t)tile * (kSortThreads * KPT);
+    bool bad = false;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+        const int64_t i = base + q * kSortThreads + threadIdx.x;
+        if (i < n) {
+            uint64_t b = (uint64_t)__double_as_longlong(w[i]);
+            int32_t t = T[i];
+            if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
+            if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
+                bad = true;
+                b = 0;
+            }
+            if (t < 1) {
+                bad = true;
+                t = 1;
+            }
+            keys[i] = b;
+            vals[i] = payload_T ? t : (int32_t)i;
+            atomicAdd(&h[b & 255u], 1u);
+        }
     }
-    if (T[i] < 1) flag_domain(status);
-    keys[i] = b;
-    vals[i] = (int32_t)i;
+    if (bad) flag_domain(status);
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * nblocks + tile] = h[threadIdx.x];
+}
+
+__device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+}
+
+// Lanes of the wave whose (valid) digit equals this lane's: a ballot per bit.
+__device__ __forceinline__ uint64_t digit_peers(uint32_t d, bool valid)
+{
+    uint64_t peers = __ballot(valid);
+#pragma unroll
+    for (int b = 0; b < 8; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t m = __ballot(bit);
+        peers &= bit ? m : ~m;
+    }
+    return peers;
 }
 
 // Per-tile digit histogram (tiles of 256 * KPT keys), digit-major:
-// hist[d * nblocks + tile].
+// hist[d * nblocks + tile].  A wave whose keys all hold one digit (the high
+// bytes of waits spread over a few binades) adds its count through one lane
+// instead of 64 atomics on one LDS word; otherwise each lane adds its own.
 template <int KPT>
 __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t *__restrict__ keys,
                                                                  int64_t n, int shift,
@@ -106,13 +158,29 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t 
     __shared__ uint32_t h[256];
     h[threadIdx.x] = 0;
     __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * (kSortThreads * KPT);
+    const int tile = sort_tile(nblocks);
+    const int64_t base = (int64_t)tile * (kSortThreads * KPT);
+    uint64_t key[KPT];
+#pragma unroll
     for (int q = 0; q < KPT; ++q) {
         const int64_t i = base + q * kSortThreads + threadIdx.x;
-        if (i < n) atomicAdd(&h[(keys[i] >> shift) & 255u], 1u);
+        key[q] = i < n ? keys[i] : 0;
+    }
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+        const bool valid = base + q * kSortThreads + threadIdx.x < n;
+        const uint32_t d = (uint32_t)(key[q] >> shift) & 255u;
+        const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+        const uint64_t vmask = __ballot(valid);
+        if (__ballot(valid && d == d0) == vmask) {   // uniform over the wave
+            if (lane == 0 && vmask != 0) atomicAdd(&h[d0], (uint32_t)__popcll(vmask));
+        } else if (valid) {
+            atomicAdd(&h[d], 1u);
+        }
     }
     __syncthreads();
-    hist[(int64_t)threadIdx.x * nblocks + blockIdx.x] = h[threadIdx.x];
+    hist[(int64_t)threadIdx.x * nblocks + tile] = h[threadIdx.x];
 }
 
 // Exclusive scan, within one block of 256 threads, of one value per thread;
@@ -135,28 +203,70 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *t
     return before + x - v;
 }
 
-// One block per digit: exclusive scan of that digit's per-tile counts over the
-// tiles (in place) and the digit's total count.
-__global__ void __launch_bounds__(256) digit_scan_kernel(uint32_t *__restrict__ hist, int nblocks,
-                                                         uint32_t *__restrict__ totals)
+// Exclusive scan over the 1,024 threads of a block of one value per thread
+// (a fixed order: shuffles within each wave, then the wave totals in order);
+// *total receives the block's sum.
+template <typename V>
+__device__ __forceinline__ V block1024_exclusive_scan(V v, V *total)
 {
-    uint32_t *row = hist + (int64_t)blockIdx.x * nblocks;
-    uint32_t carry = 0;
-    for (int base = 0; base < nblocks; base += 256) {
-        const int i = base + threadIdx.x;
-        const uint32_t v = (i < nblocks) ? row[i] : 0u;
-        uint32_t tot;
-        const uint32_t pre = block_exclusive_scan(v, &tot);
-        if (i < nblocks) row[i] = carry + pre;
-        carry += tot;
+    __shared__ V wsum[1024 / kWave];
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    V x = v;
+    for (int off = 1; off < kWave; off <<= 1) {
+        const V y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
     }
-    if (threadIdx.x == 0) totals[blockIdx.x] = carry;
+    if (lane == kWave - 1) wsum[wave] = x;
+    __syncthreads();
+    V before = 0, all = 0;
+    for (int q = 0; q < 1024 / kWave; ++q) {
+        if (q < wave) before += wsum[q];
+        all += wsum[q];
+    }
+    *total = all;
+    __syncthreads();
+    return before + (x - v);
 }
 
-__device__ __forceinline__ uint32_t lanes_below(uint64_t mask)
+// One block of 1,024 threads per digit: exclusive scan of that digit's
+// per-tile counts over the tiles (in place) and the digit's total.  Each
+// thread takes a run of consecutive tiles, so the row is scanned in one round.
+constexpr int kRunRegs = 8;   // runs up to this length stay in registers (8,192 tiles)
+
+__global__ void __launch_bounds__(1024) digit_scan_kernel(uint32_t *__restrict__ hist, int nblocks,
+                                                          uint32_t *__restrict__ totals)
 {
-    return __builtin_amdgcn_mbcnt_hi((uint32_t)(mask >> 32),
-                                     __builtin_amdgcn_mbcnt_lo((uint32_t)mask, 0u));
+    uint32_t *row = hist + (int64_t)blockIdx.x * nblocks;
+    const int per = (nblocks + 1023) / 1024;
+    const int64_t t0 = (int64_t)threadIdx.x * per;
+    int64_t t1 = t0 + per;
+    if (t1 > nblocks) t1 = nblocks;
+    uint32_t all;
+    if (per <= kRunRegs) {   // uniform
+        uint32_t c[kRunRegs];
+        uint32_t sum = 0;
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) {
+            c[i] = (t0 + i < t1) ? row[t0 + i] : 0u;
+            sum += c[i];
+        }
+        uint32_t run = block1024_exclusive_scan(sum, &all);
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) {
+            if (t0 + i < t1) row[t0 + i] = run;
+            run += c[i];
+        }
+    } else {
+        uint32_t sum = 0;
+        for (int64_t t = t0; t < t1; ++t) sum += row[t];
+        uint32_t run = block1024_exclusive_scan(sum, &all);
+        for (int64_t t = t0; t < t1; ++t) {
+            const uint32_t c = row[t];
+            row[t] = run;
+            run += c;
+        }
+    }
+    if (threadIdx.x == 0) totals[blockIdx.x] = all;
 }
 
 // Stable ranking scatter of one digit pass.  The destination of a key is
@@ -170,58 +280,70 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
     uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
 {
-    __shared__ uint32_t wcnt[4][256];
-    __shared__ uint32_t wofs[4][256];
-    __shared__ uint32_t dbase[256];
-    __shared__ uint32_t tstart[256];                 // first tile position of each digit
+    // 16-bit counters and 32-bit bases keep a block at 29 KiB of LDS (five
+    // resident blocks per CU): a wave holds at most 64 * KPT keys, a tile 2,048,
+    // and a destination fits 32 bits (n < 2^31)
+    __shared__ uint16_t wcnt[4][256];
+    __shared__ uint16_t wofs[4][256];
+    __shared__ int32_t gbase[256];                   // destination of digit d's first tile key
     constexpr int kTile = kSortThreads * KPT, kWaveK = kWave * KPT;
     __shared__ uint64_t lkey[kTile];
     __shared__ int32_t lval[kTile];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
+    const int tile = sort_tile(nblocks);
+    // this tile's offset within digit threadIdx.x, loaded early (its latency
+    // overlaps the ranking below)
+    const uint32_t my_off = offs[(int64_t)threadIdx.x * nblocks + tile];
 #pragma unroll
     for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
+    uint32_t dbase;
     {
         uint32_t all;
-        dbase[threadIdx.x] = block_exclusive_scan(totals[threadIdx.x], &all);
+        dbase = block_exclusive_scan(totals[threadIdx.x], &all);
     }
     __syncthreads();
 
-    const int64_t base = (int64_t)blockIdx.x * kTile + (int64_t)wave * kWaveK;
+    const int64_t base = (int64_t)tile * kTile + (int64_t)wave * kWaveK;
     uint64_t key[KPT];
     int32_t val[KPT];
     uint32_t local[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) {
+    for (int j = 0; j < KPT; ++j) {   // every load of the wave in flight before ranking
         const int64_t i = base + j * kWave + lane;
-        const bool valid = i < n;
-        key[j] = valid ? keys_in[i] : 0;
-        val[j] = valid ? vals_in[i] : 0;
-        const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
-        uint64_t peers = __ballot(valid);
+        key[j] = i < n ? keys_in[i] : 0;
+        val[j] = i < n ? vals_in[i] : 0;
+    }
 #pragma unroll
-        for (int b = 0; b < 8; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t m = __ballot(bit);
-            peers &= bit ? m : ~m;
-        }
+    for (int j = 0; j < KPT; ++j) {
+        const bool valid = base + j * kWave + lane < n;
+        const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
+        const uint64_t peers = digit_peers(d, valid);
         const uint32_t rank = lanes_below(peers);
         const uint32_t before = wcnt[wave][d];
         local[j] = before + rank;
         __builtin_amdgcn_wave_barrier();
-        if (valid && rank == 0) wcnt[wave][d] = before + (uint32_t)__popcll(peers);
+        if (valid && rank == 0) wcnt[wave][d] = (uint16_t)(before + (uint32_t)__popcll(peers));
         __builtin_amdgcn_wave_barrier();
     }
     __syncthreads();
     {
         const int d = threadIdx.x;
-        uint32_t run = 0;
+        uint32_t cnt[4], run = 0;
 #pragma unroll
         for (int q = 0; q < 4; ++q) {
-            wofs[q][d] = run;
-            run += wcnt[q][d];
+            cnt[q] = wcnt[q][d];
+            run += cnt[q];
         }
         uint32_t all;
-        tstart[d] = block_exclusive_scan(run, &all);   // run = this tile's count of digit d
+        const uint32_t tstart = block_exclusive_scan(run, &all);   // run = this tile's count of digit d
+        // wofs holds tile positions: digit d's run starts at tstart
+        uint32_t at = tstart;
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            wofs[q][d] = (uint16_t)at;
+            at += cnt[q];
+        }
+        gbase[d] = (int32_t)((int64_t)dbase + my_off - tstart);
     }
     __syncthreads();
     // tile positions are dense: the valid keys of the tile fill [0, nvalid)
@@ -230,7 +352,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
         const int64_t i = base + j * kWave + lane;
         if (i < n) {
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
-            const uint32_t pos = tstart[d] + wofs[wave][d] + local[j];
+            const uint32_t pos = wofs[wave][d] + local[j];
             if (pos < (uint32_t)kTile) {           // always true; never write outside
                 lkey[pos] = key[j];
                 lval[pos] = val[j];
@@ -238,7 +360,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
         }
     }
     __syncthreads();
-    const int64_t tile0 = (int64_t)blockIdx.x * kTile;
+    const int64_t tile0 = (int64_t)tile * kTile;
     const int64_t left = n - tile0;
     const int nvalid = left < kTile ? (int)left : kTile;
 #pragma unroll
@@ -246,9 +368,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
         const int pos = q * kSortThreads + (int)threadIdx.x;
         if (pos < nvalid) {
             const uint64_t k = lkey[pos];
-            const uint32_t d = (uint32_t)(k >> shift) & 255u;
-            const int64_t dest = (int64_t)dbase[d] + offs[(int64_t)d * nblocks + blockIdx.x] +
-                                 (pos - (int64_t)tstart[d]);
+            const int64_t dest = (int64_t)gbase[(k >> shift) & 255u] + pos;
             if (dest >= 0 && dest < n) {  // always true when the histograms agree
                 keys_out[dest] = k;
                 vals_out[dest] = lval[pos];
@@ -303,13 +423,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
             key[j] = valid ? lk[cur][i] : 0;
             val[j] = valid ? lv[cur][i] : 0;
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
-            uint64_t peers = __ballot(valid);
-#pragma unroll
-            for (int b = 0; b < 8; ++b) {
-                const bool bit = (d >> b) & 1u;
-                const uint64_t m = __ballot(bit);
-                peers &= bit ? m : ~m;
-            }
+            const uint64_t peers = digit_peers(d, valid);
             const uint32_t rank = lanes_below(peers);
             const uint32_t before = wcnt[wave][d];
             local[j] = before + rank;
@@ -410,7 +524,11 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
     }
 }
 
-// Per scan tile: sums of T and T*w over the sorted order.
+// Per scan tile: sums of T and T*w over the sorted order.  GATHER: the sort's
+// payload is the base index (perm) and the context sizes are gathered through
+// it once, into Tsorted; otherwise the payload already is the context size in
+// sorted order (Tsorted) and is only read.
+template <bool GATHER>
 __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
     const int32_t *__restrict__ T, int64_t n, int64_t *__restrict__ blkN,
@@ -426,10 +544,15 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     for (int q = 0; q < kScanIPT; ++q) {
         const int64_t j = base + (int64_t)q * kScanThreads;
         if (j < n) {
-            const int32_t pj = perm[j];
-            const int32_t pi = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
-            const int32_t t = T[pi] < 1 ? 1 : T[pi];
-            Tsorted[j] = t;   // the gather is done once; the final pass streams it
+            int32_t t;
+            if (GATHER) {
+                const int32_t pj = perm[j];
+                const int32_t pi = (pj >= 0 && pj < n) ? pj : 0;  // perm is a permutation of [0, n)
+                t = T[pi] < 1 ? 1 : T[pi];
+                Tsorted[j] = t;   // the gather is done once; the final pass streams it
+            } else {
+                t = Tsorted[j];   // clamped to >= 1 when the keys were prepared
+            }
             sn += t;
             ss += (double)t * __longlong_as_double((long long)skeys[j]);
         }
@@ -457,54 +580,58 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     }
 }
 
-// Exclusive scan of the tile sums in place (one block of kScanThreads, in
-// rounds of kScanThreads tiles; a fixed order, so the result is reproducible).
-__global__ void __launch_bounds__(kScanThreads) scan_blocks_kernel(int64_t *blkN, double *blkS,
-                                                                   int nb)
+// Exclusive scan of the tile sums in place, one block of 1,024 threads, each
+// thread a run of consecutive tiles added in order, then the run totals across
+// the block in a fixed order (reproducible).
+__global__ void __launch_bounds__(1024) scan_blocks_kernel(int64_t *blkN, double *blkS, int nb)
 {
-    __shared__ int64_t wn[kScanThreads / kWave];
-    __shared__ double wsm[kScanThreads / kWave];
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    int64_t carryN = 0;
-    double carryS = 0.0;
-    for (int base = 0; base < nb; base += kScanThreads) {
-        const int i = base + (int)threadIdx.x;
-        int64_t xn = i < nb ? blkN[i] : 0;
-        double xs = i < nb ? blkS[i] : 0.0;
-        for (int off = 1; off < kWave; off <<= 1) {   // inclusive scan within the wave
-            const int64_t yn = __shfl_up(xn, off, kWave);
-            const double ys = __shfl_up(xs, off, kWave);
-            if (lane >= off) {
-                xn += yn;
-                xs += ys;
+    const int per = (nb + 1023) / 1024;
+    const int64_t t0 = (int64_t)threadIdx.x * per;
+    int64_t t1 = t0 + per;
+    if (t1 > nb) t1 = nb;
+    int64_t alln;
+    double alls;
+    if (per <= kRunRegs) {   // uniform
+        int64_t cn[kRunRegs];
+        double cs[kRunRegs];
+        int64_t sn = 0;
+        double ss = 0.0;
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) {
+            const bool in = t0 + i < t1;
+            cn[i] = in ? blkN[t0 + i] : 0;
+            cs[i] = in ? blkS[t0 + i] : 0.0;
+            sn += cn[i];
+            ss += cs[i];
+        }
+        int64_t pn = block1024_exclusive_scan(sn, &alln);
+        double ps = block1024_exclusive_scan(ss, &alls);
+#pragma unroll
+        for (int i = 0; i < kRunRegs; ++i) {
+            if (t0 + i < t1) {
+                blkN[t0 + i] = pn;
+                blkS[t0 + i] = ps;
             }
+            pn += cn[i];
+            ps += cs[i];
         }
-        int64_t en = __shfl_up(xn, 1, kWave);            // exclusive within the wave
-        double es = __shfl_up(xs, 1, kWave);
-        if (lane == 0) {
-            en = 0;
-            es = 0.0;
-        }
-        if (lane == kWave - 1) {
-            wn[wave] = xn;
-            wsm[wave] = xs;
-        }
-        __syncthreads();
-        int64_t pn = carryN;
-        double ps = carryS;
-        for (int q = 0; q < wave; ++q) {
-            pn += wn[q];
-            ps += wsm[q];
-        }
-        if (i < nb) {
-            blkN[i] = pn + en;
-            blkS[i] = ps + es;
-        }
-        for (int q = 0; q < kScanThreads / kWave; ++q) {
-            carryN += wn[q];
-            carryS += wsm[q];
-        }
-        __syncthreads();
+        return;
+    }
+    int64_t sn = 0;
+    double ss = 0.0;
+    for (int64_t t = t0; t < t1; ++t) {
+        sn += blkN[t];
+        ss += blkS[t];
+    }
+    int64_t pn = block1024_exclusive_scan(sn, &alln);
+    double ps = block1024_exclusive_scan(ss, &alls);
+    for (int64_t t = t0; t < t1; ++t) {
+        const int64_t cn = blkN[t];
+        const double cs = blkS[t];
+        blkN[t] = pn;
+        blkS[t] = ps;
+        pn += cn;
+        ps += cs;
     }
 }
 
@@ -619,7 +746,52 @@ __device__ __forceinline__ int64_t upper_bound_keys(const uint64_t *__restrict__
     return lo;
 }
 
-// One thread per policy (a, k): closed form for every load.
+// Number of sorted waits <= x found by one wave in steps of a 64-ary search:
+// the lanes compare 64 evenly spaced keys of the open range [lo, hi) (keys
+// before lo are <= x, keys from hi on are > x; sorted keys make the lanes
+// with key <= x a prefix), which shrinks 65-fold per step; the last <= 64
+// keys are compared directly.  Every lane returns the count.
+__device__ __forceinline__ int64_t wave_upper_bound(const uint64_t *__restrict__ skeys, int64_t n,
+                                                    double x)
+{
+    const int lane = threadIdx.x % kWave;
+    int64_t lo = 0, hi = n;
+    while (hi - lo > kWave) {
+        const int64_t len = hi - lo;
+        const int64_t pos = lo + ((int64_t)(lane + 1) * len) / (kWave + 1);   // strictly increasing
+        const bool le = __longlong_as_double((long long)skeys[pos]) <= x;
+        const int k = __popcll(__ballot(le));
+        const int64_t below = __shfl(pos, k > 0 ? k - 1 : 0, kWave);
+        const int64_t above = __shfl(pos, k < kWave ? k : kWave - 1, kWave);
+        if (k > 0) lo = below + 1;
+        if (k < kWave) hi = above;
+    }
+    const int64_t pos = lo + lane;
+    const bool le = pos < hi && __longlong_as_double((long long)skeys[pos]) <= x;
+    return lo + __popcll(__ballot(le));
+}
+
+// The closed form of policy f for every load, from its two positions (counts of
+// sorted waits <= t1 and <= e); loads l0, l0 + lstep, ... are written.
+__device__ __forceinline__ void closed_form_policy(const int64_t *__restrict__ Nsum,
+                                                   const double *__restrict__ Ssum, int64_t n,
+                                                   const Tables &tb, const PriceDev &pr, int64_t f,
+                                                   double t1, double e, int64_t p1, int64_t pe,
+                                                   int l0, int lstep, double *__restrict__ cost)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t tot = Nsum[n - 1];
+    const int64_t n1 = p1 ? Nsum[p1 - 1] : 0, ne = pe ? Nsum[pe - 1] : 0;
+    const double s1 = p1 ? Ssum[p1 - 1] : 0.0, se = pe ? Ssum[pe - 1] : 0.0;
+    const double hbm = s1 + t1 * (double)(tot - n1);
+    double hold = (se - s1) - t1 * (double)(ne - n1);
+    if (!isinf(e)) hold += (e - t1) * (double)(tot - ne);
+    const double fixed = pr.a1 * hbm + pr.b2 * (double)(ne - n1) + pr.b3 * (double)(tot - ne);
+    const double nd = (double)n;
+    for (int l = l0; l < tb.L; l += lstep) cost[(int64_t)l * P + f] = (fixed + tb.a2[l] * hold) / nd;
+}
+
+// One thread per policy (a, k): closed form for every load (many policies).
 __global__ void __launch_bounds__(256) closed_form_kernel(const uint64_t *__restrict__ skeys,
                                                           const int64_t *__restrict__ Nsum,
                                                           const double *__restrict__ Ssum, int64_t n,
@@ -632,93 +804,126 @@ __global__ void __launch_bounds__(256) closed_form_kernel(const uint64_t *__rest
     const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
     const double t1 = tb.t1[a];
     const double e = t1 + tb.t2[k];
-    const int64_t p1 = upper_bound_keys(skeys, n, t1);
-    const int64_t pe = upper_bound_keys(skeys, n, e);
-    const int64_t tot = Nsum[n - 1];
-    const int64_t n1 = p1 ? Nsum[p1 - 1] : 0, ne = pe ? Nsum[pe - 1] : 0;
-    const double s1 = p1 ? Ssum[p1 - 1] : 0.0, se = pe ? Ssum[pe - 1] : 0.0;
-    const double hbm = s1 + t1 * (double)(tot - n1);
-    double hold = (se - s1) - t1 * (double)(ne - n1);
-    if (!isinf(e)) hold += (e - t1) * (double)(tot - ne);
-    const double fixed = pr.a1 * hbm + pr.b2 * (double)(ne - n1) + pr.b3 * (double)(tot - ne);
-    const double nd = (double)n;
-    for (int l = 0; l < tb.L; ++l) cost[(int64_t)l * P + f] = (fixed + tb.a2[l] * hold) / nd;
+    closed_form_policy(Nsum, Ssum, n, tb, pr, f, t1, e, upper_bound_keys(skeys, n, t1),
+                       upper_bound_keys(skeys, n, e), 0, 1, cost);
+}
+
+// One wave per policy (few policies): the two positions by 64-ary searches,
+// whose few dependent steps replace a binary search's ~log2(n), then the
+// lanes share the loads.
+__global__ void __launch_bounds__(256) closed_form_wave_kernel(const uint64_t *__restrict__ skeys,
+                                                               const int64_t *__restrict__ Nsum,
+                                                               const double *__restrict__ Ssum,
+                                                               int64_t n, Tables tb, PriceDev pr,
+                                                               double *__restrict__ cost)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t f = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (f >= P) return;   // uniform per wave
+    const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
+    const double t1 = tb.t1[a];
+    const double e = t1 + tb.t2[k];
+    const int64_t p1 = wave_upper_bound(skeys, n, t1);
+    const int64_t pe = wave_upper_bound(skeys, n, e);
+    closed_form_policy(Nsum, Ssum, n, tb, pr, f, t1, e, p1, pe, (int)(threadIdx.x % kWave), kWave,
+                       cost);
+}
+
+// Policies up to which a wave per policy pays (its searches are short chains
+// of dependent loads; many policies already fill the chip with one thread each).
+constexpr int64_t kWavePolicies = 16384;
+
+static hipError_t launch_closed_form(const uint64_t *skeys, const SortWs &ws, int64_t n,
+                                     const Tables &tb, const PriceDev &pr, double *cost_out,
+                                     hipStream_t stream)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    if (P <= kWavePolicies)
+        hipLaunchKernelGGL(closed_form_wave_kernel, dim3((unsigned)cdiv(P, 256 / kWave)), dim3(256),
+                           0, stream, skeys, ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
+    else
+        hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
+                           skeys, ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
+    return hipGetLastError();
+}
+
+template <int KPT>
+static hipError_t launch_digit_passes(const double *w, const int32_t *T, int64_t n, SortWs &ws,
+                                      int payload_T, int *status, hipStream_t stream)
+{
+    hipLaunchKernelGGL(sort_prep_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream, w,
+                       T, n, payload_T, ws.keys[0], ws.vals[0], ws.hist, ws.nblocks, status);
+    hipError_t err = hipGetLastError();
+    int cur = 0;
+    for (int pass = 0; pass < 8 && err == hipSuccess; ++pass) {
+        const int shift = 8 * pass;
+        if (pass > 0)   // the first pass's histograms come from sort_prep_kernel
+            hipLaunchKernelGGL(sort_hist_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0,
+                               stream, ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+        hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(1024), 0, stream, ws.hist,
+                           ws.nblocks, ws.counts);
+        hipLaunchKernelGGL(sort_scatter_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0,
+                           stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
+                           ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        err = hipGetLastError();
+        cur ^= 1;
+    }
+    return err;
+}
+
+// Eight passes leave the result in buffer 0.
+static hipError_t launch_sort(const double *w, const int32_t *T, int64_t n, SortWs &ws,
+                              int payload_T, int *status, hipStream_t stream)
+{
+    switch (ws.kpt) {
+    case 8: return launch_digit_passes<8>(w, T, n, ws, payload_T, status, stream);
+    case 4: return launch_digit_passes<4>(w, T, n, ws, payload_T, status, stream);
+    default: return launch_digit_passes<2>(w, T, n, ws, payload_T, status, stream);
+    }
 }
 
 hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs &ws, int *cur_out,
                             int *status, hipStream_t stream)
 {
-    hipError_t err;
+    *cur_out = 0;
     if (n <= kSortTile) {   // one block
         hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
                            ws.keys[0], ws.vals[0], nullptr, nullptr, nullptr, status);
-        *cur_out = 0;
         return hipGetLastError();
     }
-    hipLaunchKernelGGL(sort_prep_kernel, dim3((unsigned)cdiv(n, 256)), dim3(256), 0, stream, w, T,
-                       n, ws.keys[0], ws.vals[0], status);
-    if ((err = hipGetLastError()) != hipSuccess) return err;
-    int cur = 0;
-    for (int pass = 0; pass < 8; ++pass) {
-        const int shift = 8 * pass;
-        if (ws.kpt == 8)
-            hipLaunchKernelGGL(sort_hist_kernel<8>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
-        else if (ws.kpt == 4)
-            hipLaunchKernelGGL(sort_hist_kernel<4>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
-        else
-            hipLaunchKernelGGL(sort_hist_kernel<2>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream,
-                               ws.keys[cur], n, shift, ws.hist, ws.nblocks);
-        hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(256), 0, stream, ws.hist, ws.nblocks,
-                           ws.counts);
-        if (ws.kpt == 8)
-            hipLaunchKernelGGL(sort_scatter_kernel<8>, dim3(ws.nblocks), dim3(kSortThreads), 0,
-                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
-                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
-        else if (ws.kpt == 4)
-            hipLaunchKernelGGL(sort_scatter_kernel<4>, dim3(ws.nblocks), dim3(kSortThreads), 0,
-                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
-                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
-        else
-            hipLaunchKernelGGL(sort_scatter_kernel<2>, dim3(ws.nblocks), dim3(kSortThreads), 0,
-                               stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
-                               ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
-        if ((err = hipGetLastError()) != hipSuccess) return err;
-        cur ^= 1;
-    }
-    *cur_out = cur;
-    return hipSuccess;
+    return launch_sort(w, T, n, ws, 0, status, stream);
 }
 
 hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, const Tables &tb,
                               const PriceDev &pr, SortWs &ws, double *cost_out,
                               int32_t *perm_out, int *status, hipStream_t stream)
 {
-    const int64_t P = (int64_t)tb.K1 * tb.K2;
     if (n <= kSortTile) {   // sort and prefix arrays in one block
         hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
                            ws.keys[0], ws.vals[0], ws.Nsum, ws.Ssum, perm_out, status);
-        hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
-                           ws.keys[0], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
-        return hipGetLastError();
+        const hipError_t err = hipGetLastError();
+        if (err != hipSuccess) return err;
+        return launch_closed_form(ws.keys[0], ws, n, tb, pr, cost_out, stream);
     }
-    int cur = 0;
-    hipError_t err = launch_sort_keys(w, T, n, ws, &cur, status, stream);
+    // without a requested order the payload is the context size itself, so the
+    // scans read it in sorted order instead of gathering it through the order
+    const bool want_perm = perm_out != nullptr;
+    hipError_t err = launch_sort(w, T, n, ws, want_perm ? 0 : 1, status, stream);
     if (err != hipSuccess) return err;
-    // the other payload buffer is free once the sort is done: it takes the
-    // context sizes in sorted order
-    int32_t *Tsorted = ws.vals[cur ^ 1];
-    hipLaunchKernelGGL(scan_reduce_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
-                       ws.keys[cur], ws.vals[cur], T, n, ws.blkN, ws.blkS, Tsorted);
-    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(kScanThreads), 0, stream, ws.blkN,
-                       ws.blkS, ws.nblocks_scan);
+    int32_t *Tsorted = want_perm ? ws.vals[1] : ws.vals[0];   // buffer 1 is free after the sort
+    if (want_perm)
+        hipLaunchKernelGGL(scan_reduce_kernel<true>, dim3(ws.nblocks_scan), dim3(kScanThreads), 0,
+                           stream, ws.keys[0], ws.vals[0], T, n, ws.blkN, ws.blkS, Tsorted);
+    else
+        hipLaunchKernelGGL(scan_reduce_kernel<false>, dim3(ws.nblocks_scan), dim3(kScanThreads), 0,
+                           stream, ws.keys[0], nullptr, T, n, ws.blkN, ws.blkS, Tsorted);
+    hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(1024), 0, stream, ws.blkN, ws.blkS,
+                       ws.nblocks_scan);
     hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
-                       ws.keys[cur], ws.vals[cur], Tsorted, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
+                       ws.keys[0], ws.vals[0], Tsorted, n, ws.blkN, ws.blkS, ws.Nsum, ws.Ssum,
                        perm_out);
-    hipLaunchKernelGGL(closed_form_kernel, dim3((unsigned)cdiv(P, 256)), dim3(256), 0, stream,
-                       ws.keys[cur], ws.Nsum, ws.Ssum, n, tb, pr, cost_out);
-    return hipGetLastError();
+    if ((err = hipGetLastError()) != hipSuccess) return err;
+    return launch_closed_form(ws.keys[0], ws, n, tb, pr, cost_out, stream);
 }
 
 }  // namespace kvr
