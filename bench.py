@@ -131,7 +131,7 @@ def main() -> int:
                     help="time only the admission replay and the controller, then exit")
     ap.add_argument("--replay-reps", type=int, default=8192)
     ap.add_argument("--sort-scale", action="store_true",
-                    help="time the SORTED path on 2^20, 2^22 and 2^24 waits, then exit")
+                    help="time the SORTED path on 2^20, 2^22, 2^23 and 2^24 waits, then exit")
     ap.add_argument("--copy-calibration", action="store_true")
     args = ap.parse_args()
 
@@ -301,18 +301,19 @@ def time_paths(kvr, workloads, torch):
     return res
 
 
-# Algorithmic bytes per key of the SORTED path: eight digit passes, each an
-# 8-byte histogram read, a 12-byte scatter read (key and payload) and a 12-byte
-# write; key preparation (12 B read, 12 B written); the prefix scans (12 B read
-# twice, 16 B written).
-SORT_BYTES_PER_KEY = 8 * (8 + 12 + 12) + 24 + 40
+# Algorithmic bytes per key of the SORTED path (no order requested): key
+# preparation, which also counts the first digit (12 B read: wait and context
+# size; 12 B written: key and payload); seven histogram reads of the keys for
+# the other digits (8 B each); eight scatters (12 B read, 12 B written each);
+# the prefix scans (12 B read twice, 16 B written).
+SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 40
 
 
 def time_sort_scale(kvr, workloads, torch):
-    """Median milliseconds per SORTED kvr_cost_grid call at 2^20, 2^22 and
-    2^24 waits and the algorithmic bytes per second that implies."""
+    """Median milliseconds per SORTED kvr_cost_grid call at 2^20, 2^22, 2^23
+    and 2^24 waits and the algorithmic bytes per second that implies."""
     res = {}
-    for lg in (20, 22, 24):
+    for lg in (20, 22, 23, 24):
         wl = workloads.sort_scale_case(lg)
         pf = wl.platform
         pr = kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],

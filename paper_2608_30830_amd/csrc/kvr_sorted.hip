@@ -32,11 +32,18 @@ static inline int64_t cdiv(int64_t a, int64_t b) { return (a + b - 1) / b; }
 static inline size_t align256(size_t x) { return (x + 255) & ~(size_t)255; }
 
 // Keys per thread of the multi-block sort: the largest tile (256 * kpt keys,
-// kpt = 2, 4 or 8) that still gives about one block per CU, since below that
-// each pass is bound by the length of a block's chain (measured on MI355X:
-// 65,536 keys 0.150 ms with kpt = 2 against 0.203 ms with 8; 2^20 keys
-// 0.31 ms with 8 against 0.41 ms with 2).
-static int sort_kpt(int64_t n) { return n >= (int64_t(1) << 19) ? 8 : n >= (int64_t(1) << 18) ? 4 : 2; }
+// kpt = 2, 4, 8 or 16) that still gives about one block per CU, since below
+// that each pass is bound by the length of a block's chain (measured on
+// MI355X: 65,536 keys 0.150 ms with kpt = 2 against 0.203 ms with 8; 2^20
+// keys 0.31 ms with 8 against 0.41 ms with 2).  Longer tiles also give each
+// digit longer runs of consecutive destinations: at 2^24 keys a scatter pass
+// writes exactly its 24 algorithmic bytes per key with 4,096-key tiles (103 us)
+// and 12-37 % more with 2,048-key tiles (129-134 us); at 2^22 keys the shorter
+// tiles still win (23.4 against 29.4 us), having twice the blocks.
+static int sort_kpt(int64_t n)
+{
+    return n >= (int64_t(1) << 23) ? 16 : n >= (int64_t(1) << 19) ? 8 : n >= (int64_t(1) << 18) ? 4 : 2;
+}
 
 size_t sort_ws_bytes(int64_t n)
 {
@@ -146,9 +153,10 @@ __device__ __forceinline__ uint64_t digit_peers(uint32_t d, bool valid)
 }
 
 // Per-tile digit histogram (tiles of 256 * KPT keys), digit-major:
-// hist[d * nblocks + tile].  A wave whose keys all hold one digit (the high
-// bytes of waits spread over a few binades) adds its count through one lane
-// instead of 64 atomics on one LDS word; otherwise each lane adds its own.
+// hist[d * nblocks + tile].  The keys of a wave that share the first lane's
+// digit add their count through that lane, the others one by one: when most
+// keys hold one digit (the high bytes of waits spread over a few binades)
+// this replaces up to 64 atomics on one LDS word by one.
 template <int KPT>
 __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t *__restrict__ keys,
                                                                  int64_t n, int shift,
@@ -172,12 +180,9 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t 
         const bool valid = base + q * kSortThreads + threadIdx.x < n;
         const uint32_t d = (uint32_t)(key[q] >> shift) & 255u;
         const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
-        const uint64_t vmask = __ballot(valid);
-        if (__ballot(valid && d == d0) == vmask) {   // uniform over the wave
-            if (lane == 0 && vmask != 0) atomicAdd(&h[d0], (uint32_t)__popcll(vmask));
-        } else if (valid) {
-            atomicAdd(&h[d], 1u);
-        }
+        const uint64_t same = __ballot(valid && d == d0);
+        if (lane == 0 && same != 0) atomicAdd(&h[d0], (uint32_t)__popcll(same));
+        else if (valid && d != d0) atomicAdd(&h[d], 1u);
     }
     __syncthreads();
     hist[(int64_t)threadIdx.x * nblocks + tile] = h[threadIdx.x];
@@ -242,20 +247,25 @@ __global__ void __launch_bounds__(1024) digit_scan_kernel(uint32_t *__restrict__
     int64_t t1 = t0 + per;
     if (t1 > nblocks) t1 = nblocks;
     uint32_t all;
-    if (per <= kRunRegs) {   // uniform
+    if (per <= kRunRegs) {   // uniform: the row passes through LDS with coalesced accesses
+        __shared__ uint32_t lrow[1024 * kRunRegs];
+        for (int t = threadIdx.x; t < nblocks; t += 1024) lrow[t] = row[t];
+        __syncthreads();
         uint32_t c[kRunRegs];
         uint32_t sum = 0;
 #pragma unroll
         for (int i = 0; i < kRunRegs; ++i) {
-            c[i] = (t0 + i < t1) ? row[t0 + i] : 0u;
+            c[i] = (t0 + i < t1) ? lrow[t0 + i] : 0u;
             sum += c[i];
         }
         uint32_t run = block1024_exclusive_scan(sum, &all);
 #pragma unroll
         for (int i = 0; i < kRunRegs; ++i) {
-            if (t0 + i < t1) row[t0 + i] = run;
+            if (t0 + i < t1) lrow[t0 + i] = run;
             run += c[i];
         }
+        __syncthreads();
+        for (int t = threadIdx.x; t < nblocks; t += 1024) row[t] = lrow[t];
     } else {
         uint32_t sum = 0;
         for (int64_t t = t0; t < t1; ++t) sum += row[t];
@@ -281,7 +291,8 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
 {
     // 16-bit counters and 32-bit bases keep a block at 29 KiB of LDS (five
-    // resident blocks per CU): a wave holds at most 64 * KPT keys, a tile 2,048,
+    // resident blocks per CU at 2,048-key tiles): a wave holds at most 64 * KPT
+    // keys, a tile at most 4,096,
     // and a destination fits 32 bits (n < 2^31)
     __shared__ uint16_t wcnt[4][256];
     __shared__ uint16_t wofs[4][256];
@@ -876,6 +887,7 @@ static hipError_t launch_sort(const double *w, const int32_t *T, int64_t n, Sort
                               int payload_T, int *status, hipStream_t stream)
 {
     switch (ws.kpt) {
+    case 16: return launch_digit_passes<16>(w, T, n, ws, payload_T, status, stream);
     case 8: return launch_digit_passes<8>(w, T, n, ws, payload_T, status, stream);
     case 4: return launch_digit_passes<4>(w, T, n, ws, payload_T, status, stream);
     default: return launch_digit_passes<2>(w, T, n, ws, payload_T, status, stream);
