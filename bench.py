@@ -275,12 +275,8 @@ def time_paths(kvr, workloads, torch):
             run = call.launch
             key = f"{name}/{'factored' if method else 'bootstrap'}"
         else:
-            out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
-                              device="cuda")
-            kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out)
-
-            def run(w=w, T=T, pr=pr, g=g, method=method, out=out):
-                kvr.kvr_cost_grid(w, T, pr, g, method=method, out=out, check=False)
+            call = kvr.CostGridCall(w, T, pr, g, method=method)
+            run = call.launch
             key = f"{name}/{'sorted' if method == kvr.KVR_SORTED else 'brute'}"
         run()
         torch.cuda.synchronize()
@@ -322,15 +318,14 @@ def time_sort_scale(kvr, workloads, torch):
         g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
-        out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
-                          device="cuda")
-        kvr.kvr_cost_grid(w, T, pr, g, method=kvr.KVR_SORTED, out=out)
+        call = kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED)
+        call.launch()
         torch.cuda.synchronize()
         times = []
         for _ in range(9):
             a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
             a.record()
-            kvr.kvr_cost_grid(w, T, pr, g, method=kvr.KVR_SORTED, out=out, check=False)
+            call.launch()
             b.record()
             torch.cuda.synchronize()
             times.append(a.elapsed_time(b))
@@ -629,12 +624,9 @@ def results_table(kvr, workloads, torch, cpu_evals=2.0e9):
         T = torch.as_tensor(wl.ctx_tokens).cuda()
         reps = 3 if name.startswith("twotier") else 5
         if wl.idx is None:
-            out = torch.empty((wl.lam.size, wl.t1.size, wl.t2.size), dtype=torch.float64,
-                              device="cuda")
-            brute = _median_ms(torch, lambda: kvr.kvr_cost_grid(w, T, pr, g, out=out,
-                                                                check=False), reps)
-            closed = _median_ms(torch, lambda: kvr.kvr_cost_grid(
-                w, T, pr, g, method=kvr.KVR_SORTED, out=out, check=False), reps)
+            brute = _median_ms(torch, kvr.CostGridCall(w, T, pr, g).launch, reps)
+            closed = _median_ms(torch, kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED).launch,
+                                reps)
             closed_name = "sorted"
         else:
             idx = torch.as_tensor(wl.idx).cuda()

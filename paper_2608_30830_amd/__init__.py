@@ -202,6 +202,43 @@ def _workspace(nbytes: int, ws=None):
     return torch.empty(max(nbytes, 256), dtype=torch.uint8, device="cuda")
 
 
+class CostGridCall:
+    """A prepared kvr_cost_grid call: workspace and outputs allocated once, so
+    that ``launch()`` only enqueues the library's kernels (as a serving loop
+    or a benchmark would call it)."""
+
+    def __init__(self, wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid,
+                 method: int = KVR_BRUTE, want_perm: bool = False):
+        torch = _torch()
+        _need(wait_s, torch.float64, "wait_s")
+        _need(ctx_tokens, torch.int32, "ctx_tokens")
+        _need_shape(ctx_tokens, wait_s.shape, "ctx_tokens")
+        self.lib = load_library()
+        self.wait_s, self.ctx, self.prices, self.grid, self.method = wait_s, ctx_tokens, prices, \
+            grid, method
+        self.n = wait_s.numel()
+        need = ctypes.c_size_t(0)
+        _check(self.lib.kvr_cost_grid(None, None, self.n, ctypes.byref(prices), ctypes.byref(grid.c),
+                                      method, None, None, None, ctypes.byref(need), None),
+               "kvr_cost_grid(size)")
+        self.ws = _workspace(need.value)
+        self.ws_bytes = ctypes.c_size_t(self.ws.numel())
+        self.cost = torch.empty((grid.n_lam, grid.n_t1, grid.n_t2), dtype=torch.float64,
+                                device="cuda")
+        self.perm = torch.empty(self.n, dtype=torch.int32, device="cuda") if want_perm else None
+
+    def launch(self, stream=None) -> None:
+        _check(self.lib.kvr_cost_grid(_ptr(self.wait_s), _ptr(self.ctx), self.n,
+                                      ctypes.byref(self.prices), ctypes.byref(self.grid.c),
+                                      self.method, _ptr(self.cost), _ptr(self.perm), _ptr(self.ws),
+                                      ctypes.byref(self.ws_bytes), _stream_ptr(stream)),
+               "kvr_cost_grid")
+        _on_stream(stream, self.ws, self.cost, self.perm)
+
+    def status(self, stream=None) -> int:
+        return self.lib.kvr_workspace_status(_ptr(self.ws), _stream_ptr(stream))
+
+
 def kvr_cost_grid(wait_s, ctx_tokens, prices: kvr_prices, grid: PolicyGrid, method: int = KVR_BRUTE,
                   want_perm: bool = False, out=None, workspace=None, stream=None,
                   check: bool = True):

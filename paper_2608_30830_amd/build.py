@@ -15,7 +15,7 @@ HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["kvr_api.cpp", "kvr_grid.hip", "kvr_aux.hip", "kvr_sorted.hip", "kvr_replay.hip",
            "kvr_controller.hip", "kvr_r3.hip",
-           "kvr_factored.hip", "kvr_noalloc.hip"]
+           "kvr_factored.hip", "kvr_noalloc.hip", "kvr_small.hip"]
 COMMON = ["--offload-arch=gfx950", "-O3", "-std=c++17", "-fPIC",
           # no packed-fp32 instruction selection anywhere
           "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

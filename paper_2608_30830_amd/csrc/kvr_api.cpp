@@ -160,6 +160,7 @@ BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, 
     const int64_t nsplit = cdiv(m, split_len);
     gp.nsplit = (int)nsplit;
     gp.split_len = split_len;
+    gp.wpb = 1;
     bp.fused = (nsplit == 1);
 
     size_t off = kStatusBytes;
@@ -222,6 +223,59 @@ kvr::R3Ws r3_view(void *ws, const BrutePlan &bp)
     v.nsplit = bp.r3_nsplit;
     v.split_len = bp.r3_split_len;
     return v;
+}
+
+// Workspace of the four-launch brute force for one small sample
+// (kvr::small_path_fits): after bp's tables, the pre-pass blocks' rows of the
+// recompute histogram over the F finite deadlines, each policy's deadline
+// bin, the per-block X/G partials and the grid kernel's split partials
+// (always written, even for one split).
+struct SmallPlan {
+    size_t off_hist, off_lb, off_xgp, off_part, total;
+    size_t part_bytes;
+};
+
+bool small_plan_applies(const BrutePlan &bp, const kvr_policy_grid &g, int64_t n)
+{
+    return kvr::small_path_fits(g.n_t1, g.n_t2, bp.r3_bins, n);
+}
+
+// Splits of the small-sample path: blocks of kSmallWaves waves add their
+// splits in LDS, so splits can be as short as one staged chunk; about 4,096
+// waves (four per SIMD) in all.
+void small_splits(BrutePlan &bp, int64_t m, int64_t part_cap)
+{
+    kvr::GridPlan &gp = bp.gp;
+    const int64_t base_waves = gp.ngroups * gp.ntiles;
+    int64_t ns = std::max<int64_t>(1, std::min<int64_t>(4096 / base_waves, cdiv(m, kvr::kChunk)));
+    const int64_t per_group = gp.ntiles * gp.LT * (int64_t)gp.nblk * kvr::kWave;   // doubles per split group
+    const int64_t cap_groups = std::max<int64_t>(1, part_cap / 8 / std::max<int64_t>(1, per_group));
+    ns = std::min<int64_t>(ns, cap_groups * kvr::kSmallWaves);
+    gp.split_len = cdiv(cdiv(m, ns), kvr::kChunk) * kvr::kChunk;
+    gp.nsplit = (int)cdiv(m, gp.split_len);
+    gp.wpb = kvr::kSmallWaves;
+    bp.fused = false;
+}
+
+SmallPlan plan_small(const BrutePlan &bp, int64_t n, const kvr_policy_grid &g)
+{
+    SmallPlan sp{};
+    const int64_t P = (int64_t)g.n_t1 * g.n_t2;
+    size_t off = bp.off_a2 + align256(sizeof(double) * bp.Lpad);
+    auto take = [&](size_t bytes) {
+        size_t o = off;
+        off += align256(bytes);
+        return o;
+    };
+    sp.off_hist = take(sizeof(uint64_t) * std::max<int64_t>(1, bp.r3_bins) *
+                       kvr::small_sample_blocks(n));
+    sp.off_lb = take(sizeof(int32_t) * P);
+    sp.off_xgp = take(sizeof(double) * 2 * g.n_t1 * kvr::small_sample_blocks(n));
+    const int64_t nsg = cdiv(bp.gp.nsplit, bp.gp.wpb);
+    sp.part_bytes = sizeof(double) * (size_t)nsg * bp.gp.ntiles * bp.gp.LT * P;
+    sp.off_part = take(sp.part_bytes);
+    sp.total = off;
+    return sp;
 }
 
 int hip_ok(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_E_HIP; }
@@ -320,17 +374,31 @@ int kvr::cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, in
 
     size_t need;
     BrutePlan bp{};
+    SmallPlan sp{};
+    bool small = false;
     size_t off_t1 = kStatusBytes, off_t2 = 0, off_a2 = 0, off_sort = 0;
     int32_t Lpad = g->n_lam;
     if (method == KVR_BRUTE) {
         bp = plan_brute(1, n, n, *g, false, true);
-        if (fit_bytes > 0 && bp.total > fit_bytes && !bp.fused) {
-            const size_t part = bp.total - bp.off_part;   // the partials are carved last
-            if (bp.total - part < fit_bytes)
-                bp = plan_brute(1, n, n, *g, false, true, (int64_t)(fit_bytes - (bp.total - part)));
+        small = small_plan_applies(bp, *g, n);
+        if (small) {
+            small_splits(bp, n, kPartCapBytes);
+            sp = plan_small(bp, n, *g);
+        }
+        need = small ? sp.total : bp.total;
+        // the split partials are carved last: fewer splits when they alone
+        // push the workspace past fit_bytes
+        const size_t part = small ? sp.part_bytes : (bp.fused ? 0 : bp.total - bp.off_part);
+        if (fit_bytes > 0 && need > fit_bytes && part > 0 && need - part < fit_bytes) {
+            const int64_t cap = (int64_t)(fit_bytes - (need - part));
+            bp = plan_brute(1, n, n, *g, false, true, cap);
+            if (small) {
+                small_splits(bp, n, cap);
+                sp = plan_small(bp, n, *g);
+            }
+            need = small ? sp.total : bp.total;
         }
         if (bp.max_blocks > INT32_MAX) return KVR_E_SIZE;
-        need = bp.total;
     } else {
         off_t2 = off_t1 + align256(sizeof(double) * g->n_t1);
         off_a2 = off_t2 + align256(sizeof(double) * g->n_t2);
@@ -348,6 +416,24 @@ int kvr::cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, in
     int *status = static_cast<int *>(d_ws);
     const PriceDev pr = device_prices(p);
     Tables tb{};
+    if (method == KVR_BRUTE && small) {
+        unsigned long long *hist = at<unsigned long long>(d_ws, sp.off_hist);
+        if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
+            return rc;
+        int32_t *lb = at<int32_t>(d_ws, sp.off_lb);
+        double *xgp = at<double>(d_ws, sp.off_xgp), *part = at<double>(d_ws, sp.off_part);
+        KVR_TRY(kvr::launch_small_prep(d_wait_s, d_ctx_tokens, n, tb, bp.r3_bins, hist, lb, xgp,
+                                       status, s));
+        SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
+        kvr::R3Ws none{};
+        KVR_MARK(g_prof_begin, s);
+        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, nullptr, nullptr, none, nullptr, nullptr, part,
+                                 status, s));
+        KVR_MARK(g_prof_end, s);
+        KVR_TRY(kvr::launch_small_finalize(bp.gp, tb, pr, n, bp.r3_bins, hist, lb, xgp, part, d_cost,
+                                           s));
+        return KVR_OK;
+    }
     if (method == KVR_BRUTE) {
         if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
             return rc;

@@ -11,6 +11,7 @@ namespace kvr {
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kChunk = 128;        // samples staged in LDS per buffer (grid kernel)
 constexpr int kStatusDomain = 1;   // value of the workspace status word on a domain error
+constexpr int kSmallWaves = 8;     // waves per grid block on the small-sample path
 
 // Where a call's samples come from: the base arrays, optionally through
 // bootstrap index rows idx[R][m].
@@ -44,6 +45,8 @@ struct GridPlan {
     int ntiles;          // ceil(L / LT)
     int nblk;            // groups per resample, kModePerLane: ceil(K1*K2 / 64)
     int nsplit;          // sample splits per resample
+    int wpb;             // waves per block (1, or kSmallWaves: consecutive splits
+                         // of one group, added in LDS before one partial is written)
     int mode;            // kModePerLane, kModeRows1 or kModeRows2
     int64_t ngroups;     // 64-lane groups: R*nblk (per lane) or ceil(R*K1*K2 / 64)
     int64_t split_len;   // samples per split (multiple of kChunk)
@@ -131,6 +134,19 @@ hipError_t launch_controller_final(const int64_t *restored, const int64_t *admit
                                    int64_t reps, int64_t n_requests, const void *count_ws,
                                    double t2, double t_star, double b2, double b3,
                                    kvr_controller_out *out, hipStream_t stream);
+
+// Brute-force grid of one sample with few t1 timers and deadlines in four
+// launches (kvr_small.hip): stage, pre-pass, grid kernel with split partials,
+// finalize.
+bool small_path_fits(int K1, int K2, int64_t nbins, int64_t n);
+int small_sample_blocks(int64_t n);
+hipError_t launch_small_prep(const double *w, const int32_t *T, int64_t n, const Tables &tb,
+                             int64_t nbins, unsigned long long *hist, int32_t *lb, double *xgp,
+                             int *status, hipStream_t stream);
+hipError_t launch_small_finalize(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
+                                 int64_t m, int64_t nbins, const unsigned long long *hist,
+                                 const int32_t *lb, const double *xgp, const double *partials,
+                                 double *cost_out, hipStream_t stream);
 
 // Sorted path.
 struct SortWs {

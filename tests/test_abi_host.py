@@ -435,7 +435,11 @@ def test_noalloc_rejects_on_the_host(lib):
         assert need.value > kvr.NOALLOC_SCRATCH_BYTES
         assert _noalloc_rc(lib, g, n) == kvr.KVR_E_SIZE
     # brute force with more waits than the deadline bins of 64 MiB can hold
-    assert _noalloc_rc(lib, g, 1 << 24, method=kvr.KVR_BRUTE) == kvr.KVR_E_SIZE
+    # (nine GPU-tier timers: the general plan, which keeps a bin per wait; a
+    # grid of at most eight t1 timers needs no per-wait storage)
+    g9 = kvr.PolicyGrid([0.0] + [float(2 ** i) for i in range(8)], [10.0, 100.0, math.inf],
+                        [0.1, 0.9])
+    assert _noalloc_rc(lib, g9, 1 << 24, method=kvr.KVR_BRUTE) == kvr.KVR_E_SIZE
 
 
 def test_noalloc_scratch_size_matches_header(lib):

@@ -90,6 +90,9 @@ RANDOM_CASES = [  # seed, n, K1, K2, L, ties  (ragged n, K2 below/at/above one w
     (106, 3001, 1, 130, 40, False),
     (107, 2500, 4, 70, 9, True),
     (108, 300, 5, 2, 4, True),
+    # eight t1 rows and ~4,000 finite deadlines over 16 pre-pass blocks: the
+    # largest grid of the four-launch path for one sample
+    (109, 16000, 8, 500, 5, True),
 ]
 
 
@@ -294,16 +297,23 @@ def test_bootstrap_twotier_4096_full(kvr, oracle_mod):
     _boot_full(kvr, oracle_mod, "twotier-4096x64k", sample_rows=[0, 4095])
 
 
-def test_identity_rows_equal_cost_grid(kvr):
-    """A bootstrap row drawing every sample once in order is the plain grid."""
-    wl = workloads.random_case(301, 5000, 2, 66, 6)
+@pytest.mark.parametrize("k1", [2, 9])
+def test_identity_rows_equal_cost_grid(kvr, k1):
+    """A bootstrap row drawing every sample once in order is the plain grid:
+    bit for bit where both calls run the same kernels in the same order (nine
+    GPU-tier timers), within 1e-12 where the plain grid of one small sample
+    adds its splits in blocks (two timers, the four-launch path)."""
+    wl = workloads.random_case(301, 5000, k1, 66, 6)
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
     idx = np.tile(np.arange(wl.n, dtype=np.int32), (3, 1))
     best, bc, cost = kvr.kvr_bootstrap(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
                                        _dev(idx, _i32()), _lib_prices(kvr, wl), g, want_cost=True)
     plain, _, _ = run_grid(kvr, wl, "brute")
     for r in range(3):
-        assert np.array_equal(_np(cost)[r], plain)
+        if k1 > 8:
+            assert np.array_equal(_np(cost)[r], plain)
+        else:
+            assert_costs(_np(cost)[r], plain, rtol=1e-12)
 
 
 def test_deterministic(kvr):
