@@ -130,6 +130,8 @@ def main() -> int:
     ap.add_argument("--replay-only", action="store_true",
                     help="time only the admission replay and the controller, then exit")
     ap.add_argument("--replay-reps", type=int, default=8192)
+    ap.add_argument("--factored-only", action="store_true",
+                    help="time only kvr_bootstrap_factored on the bootstrap workloads, then exit")
     ap.add_argument("--sort-scale", action="store_true",
                     help="time the SORTED path on 2^20, 2^22, 2^23 and 2^24 waits, then exit")
     ap.add_argument("--copy-calibration", action="store_true")
@@ -154,6 +156,10 @@ def main() -> int:
 
     if args.sort_scale:
         print(json.dumps({"sort_scale": time_sort_scale(kvr, workloads, torch)}), flush=True)
+        return 0
+
+    if args.factored_only:
+        print(json.dumps({"paths": time_factored(kvr, workloads, torch)}), flush=True)
         return 0
 
     if args.replay_only:
@@ -227,7 +233,10 @@ def main() -> int:
         "config": {"workload": args.workload, "samples": wl.n, "resamples": wl.n_resamples,
                    "resample_len": wl.m, "t1_timers": int(wl.t1.size),
                    "t2_timers": int(wl.t2.size), "loads": int(wl.lam.size),
-                   "evaluations_per_step": evals, "method": "brute-force grid, fused selection"},
+                   "evaluations_per_step": evals, "method": "brute-force grid: one fp64 FMA per (draw, policy, load) for "
+                             "the load-dependent holding term; load-independent terms per "
+                             "(draw, t1) and recompute counts per (draw, deadline) through "
+                             "deadline bins; selection fused"},
         "roofline": {"bound": "alu", "achieved": achieved, "peak": FP64_PEAK_TFLOPS,
                      "unit": "TFLOP/s", "frac": achieved / FP64_PEAK_TFLOPS,
                      "traffic": counter_traffic(args.workload, wl.n_resamples),
@@ -303,6 +312,27 @@ def time_paths(kvr, workloads, torch):
 # the other digits (8 B each); eight scatters (12 B read, 12 B written each);
 # the prefix scans (12 B read twice, 16 B written).
 SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 40
+
+
+def time_factored(kvr, workloads, torch):
+    """kvr_bootstrap_factored on boot-1024x64k and twotier-4096x64k (median of
+    seven calls, inputs resident)."""
+    res = {}
+    for name in ("boot-1024x64k", "twotier-4096x64k"):
+        wl = workloads.make(name)
+        pf = wl.platform
+        pr = kvr.kvr_prices_from_platform(wl.kv_bytes_per_token, pf["hbm_usable_bytes"],
+                                          pf["host_link_bytes_per_s"],
+                                          pf["prefill_tokens_per_s"])
+        g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
+        call = kvr.BootstrapCall(torch.as_tensor(wl.wait_s).cuda(),
+                                 torch.as_tensor(wl.ctx_tokens).cuda(),
+                                 torch.as_tensor(wl.idx).cuda(), pr, g, factored=True)
+        ms = _median_ms(torch, call.launch, 7)
+        key = f"{name}/factored"
+        res[key] = {"ms": ms}
+        log(f"[bench] path {key}: {ms:.3f} ms")
+    return res
 
 
 def time_sort_scale(kvr, workloads, torch):

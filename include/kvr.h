@@ -141,7 +141,11 @@ int kvr_prices_from_platform(double kv_bytes_per_token, double hbm_usable_bytes,
  *   d_wait_s[n]     device, float64: suspension (approval) waits, seconds.
  *   d_ctx_tokens[n] device, int32: context tokens per request (T >= 1).
  *   p, g            host: prices and policy grid (validated on the host).
- *   method          KVR_BRUTE: every (sample, policy, load) evaluated;
+ *   method          KVR_BRUTE: the load-dependent holding term of every
+ *                   (sample, policy, load) evaluated, one fp64 FMA each; the
+ *                   load-independent terms are summed once per (sample, t1)
+ *                   (HBM residency, offload) and, for the recompute branch,
+ *                   counted once per (sample, deadline) through deadline bins;
  *                   KVR_SORTED: stable radix sort of the waits, prefix sums
  *                   of T and T*w, closed form per policy.
  *   d_cost          device, float64 [n_lam][n_t1][n_t2]: mean GPU-s per
@@ -175,8 +179,10 @@ int kvr_select_policy(const double *d_cost, int64_t batch, int32_t n_lam, int32_
                       void *hip_stream);
 
 /*
- * Bootstrap calibration: the brute-force grid over every resample, with the
- * selection fused per resample.
+ * Bootstrap calibration: the brute-force grid (as KVR_BRUTE of kvr_cost_grid:
+ * every (draw, policy, load) holding term evaluated, the load-independent
+ * terms summed per (draw, t1) and binned per (draw, deadline)) over every
+ * resample, with the selection fused per resample.
  *   d_wait_s[n], d_ctx_tokens[n]  device: the base sample (as kvr_cost_grid).
  *   d_idx           device, int32 [n_resamples][m]: with-replacement draws,
  *                   each in [0, n).  The caller draws them (seeded).

@@ -252,8 +252,9 @@ hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *
 }
 
 // ---------------------------------------------------- split reduce, finalize --
-// Partials are laid out [split][resample][tile][value][policy] with LT load
-// accumulators and the recompute weight R3 as values.  Stage 1: one thread per
+// Partials are laid out [split][resample][tile][value][policy] with the LT
+// load accumulators as values (R3 comes from the deadline bins of
+// kvr_r3.hip, X and G from xg_kernel).  Stage 1: one thread per
 // element of split 0 sums it over the splits, in split order, in place.
 __global__ void __launch_bounds__(256) reduce_splits_kernel(int64_t nsplit, int64_t slice,
                                                             double *__restrict__ partials)
