@@ -12,6 +12,9 @@
   count that lets a wave straddle two resamples, and a grid of at least 32,768
   base waves.  Its picks must equal the selection rule (cost ascending, exact
   ties to the larger flat index) applied to the GPU's own cost tensor, exactly.
+* Load tiles of 16, 8 and 4 loads on grids whose 64-lane groups straddle t1
+  rows or resamples, fused and split, through kvr_bootstrap and kvr_cost_grid
+  (above the small-sample path), against the oracle's double loop.
 * The full two-tier cost tensor (64 x 257 x 32 policies and loads) of fixed
   rows of the 4,096-row bench workload, from the bench's own launch, against
   the oracle's double loop element by element.
@@ -173,6 +176,49 @@ def test_fused_argmin_tie_rule(kvr, oracle_mod, name):
     tied = _check_fused(kvr, oracle_mod, wl, rows_vs_oracle=range(R))
     print(f"[ties] {name}: {tied} (resample, load) minima shared by several policies")
     assert tied > 0
+
+
+def _lane_layout_cases():
+    # (seed, n, K1, K2, L, R, m): loads L <= 16 take tiles of 16, 8 or 4 loads
+    return {
+        "lt16-straddle": (420, 1000, 1, 257, 12, 5, 1000),   # groups straddle resamples
+        "lt8-straddle": (417, 900, 3, 300, 7, 4, 1000),      # and t1 rows
+        "lt4-straddle": (418, 800, 5, 256, 3, 3, 900),
+        "lt4-rows": (419, 700, 2, 250, 4, 2, 1023),          # 500 policies per resample
+    }
+
+
+@pytest.mark.parametrize("split", [False, True], ids=["fused", "split"])
+@pytest.mark.parametrize("name", sorted(_lane_layout_cases()))
+def test_lane_layouts(kvr, oracle_mod, name, split):
+    """Tiles of fewer than 32 loads with the selection fused into the grid
+    kernel (one split) or over split partials (20,000 draws per resample):
+    every cost against the oracle's double loop, the picks against the
+    selection rule on the GPU's own costs, exactly."""
+    seed, n, k1, k2, L, R, m = _lane_layout_cases()[name]
+    if split:
+        m = 20000
+    wl = _tie_heavy(workloads.random_case(seed, n, k1, k2, L, resamples=R, m=m, ties=True), 900.0)
+    tied = _check_fused(kvr, oracle_mod, wl, rows_vs_oracle=range(R))
+    print(f"[ties] {name} {'split' if split else 'fused'}: {tied} shared minima")
+
+
+@pytest.mark.parametrize("shape", [(421, 300000, 2, 256, 4), (422, 280000, 1, 257, 16),
+                                   (423, 270000, 3, 300, 7)],
+                         ids=["lt4", "lt16", "lt8"])
+def test_lane_layouts_cost_grid(kvr, oracle_mod, shape):
+    """kvr_cost_grid BRUTE on samples above the small-sample path (one
+    resample, split partials) with tiles of 4, 16 and 8 loads: every cost
+    against the oracle's double loop, and the selection."""
+    seed, n, k1, k2, L = shape
+    wl = workloads.random_case(seed, n, k1, k2, L, ties=True)
+    cost, _, g = __import__("tests.test_gpu_parity", fromlist=["run_grid"]).run_grid(kvr, wl, "brute")
+    pr = oracle_mod.workload_prices(wl)
+    ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam)
+    assert_costs(cost, ref)
+    rb, _, _ = oracle_mod.select(ref, wl.t2)
+    hb, _, _ = oracle_mod.select(cost, wl.t2)
+    assert_selection(ref, hb, rb)
 
 
 def test_fused_argmin_32k_waves(kvr, oracle_mod):

@@ -180,3 +180,53 @@ def test_factored_degenerate_inputs(kvr, oracle_mod, name):
         rb, rbc, _ = oracle_mod.select(ref, wl.t2)
         assert_selection(ref, _np(best)[r], rb)
         assert_costs(_np(bc)[r], rbc)
+
+
+def _tie_case(name, k1):
+    rng = np.random.Generator(np.random.PCG64(700 + k1))
+    if name == "all-zero":
+        # every policy costs exactly 0
+        w = np.zeros(3000)
+        t2 = np.concatenate([np.geomspace(1.0, 1e5, 300), [np.inf]])
+    else:
+        # loads at or below lambda_crit (no holding price) and about three
+        # deadlines per gap between waits: the policies of one t1 row whose
+        # deadlines share a gap cost exactly the same
+        w = np.geomspace(1.0, 1e4, 500)
+        t2 = np.concatenate([np.geomspace(1.0, 1e5, 2000), [np.inf]])
+    T = rng.integers(1, 5000, w.size).astype(np.int32)
+    t1 = np.array([0.0, 5.0, 50.0, 400.0, 900.0, 3000.0, 7000.0])[:k1]
+    lam = np.array([0.05, 0.1, 425.0 / 1800.0])
+    idx = np.stack([np.arange(w.size, dtype=np.int32),
+                    rng.integers(0, w.size, w.size, dtype=np.int32)])
+    return workloads.Workload(name, w, T, t1, t2, lam, float(workloads.KV_128K), idx=idx)
+
+
+@pytest.mark.parametrize("name", ["all-zero", "gap-ties"])
+@pytest.mark.parametrize("k1", [1, 7])
+def test_factored_exact_tie_rule(kvr, oracle_mod, name, k1):
+    """Exact ties with one and with several t1 rows (all-zero waits: every
+    policy ties; gap ties: the policies of a t1 row whose deadlines share a
+    gap between waits tie below lambda_crit): every selection is the largest
+    flat index among the policies whose cost equals the minimum, on the GPU's
+    own cost tensor, and equals the oracle's."""
+    wl = _tie_case(name, k1)
+    best, bc, cost = _factored(kvr, wl, want_cost=True)
+    best, bc, cost = _np(best), _np(bc), _np(cost)
+    R, L = best.shape
+    nties = 0
+    for r in range(R):
+        for l in range(L):
+            c = cost[r, l].ravel()
+            at_min = np.flatnonzero(c == c.min())
+            nties += at_min.size > 1
+            assert best[r, l] == at_min[-1], (r, l, best[r, l], at_min[-8:])
+            assert bc[r, l] == c.min()
+    assert nties >= R * L // 2, nties
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(R):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        assert_costs(cost[r], ref)
+        rb, _, _ = oracle_mod.select(ref, wl.t2)
+        assert np.array_equal(best[r], rb), (r, best[r], rb)
