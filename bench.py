@@ -287,17 +287,7 @@ def time_paths(kvr, workloads, torch):
             call = kvr.CostGridCall(w, T, pr, g, method=method)
             run = call.launch
             key = f"{name}/{'sorted' if method == kvr.KVR_SORTED else 'brute'}"
-        run()
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(7):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            run()
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = sorted(times)[len(times) // 2]
+        ms = _median_ms(torch, run, 7)
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
@@ -310,8 +300,9 @@ def time_paths(kvr, workloads, torch):
 # preparation, which also counts the first digit (12 B read: wait and context
 # size; 12 B written: key and payload); seven histogram reads of the keys for
 # the other digits (8 B each); eight scatters (12 B read, 12 B written each);
-# the prefix scans (12 B read twice, 16 B written).
-SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 40
+# the tile and 64-key chunk sums (12 B read, 16 B written per 64 keys).  The
+# closed form then reads N and S at its query positions only.
+SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 12 + 16 / 64
 
 
 def time_factored(kvr, workloads, torch):
@@ -349,17 +340,7 @@ def time_sort_scale(kvr, workloads, torch):
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
         call = kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED)
-        call.launch()
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(9):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            call.launch()
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = sorted(times)[len(times) // 2]
+        ms = _median_ms(torch, call.launch, 9)
         bps = SORT_BYTES_PER_KEY * wl.n / (ms * 1e-3)
         res[wl.name] = {"ms": ms, "keys_per_s": wl.n / (ms * 1e-3), "algorithmic_bytes_per_s": bps,
                         "hbm_frac": bps / (HBM_PEAK_TBS * 1e12)}
@@ -380,17 +361,7 @@ def time_platforms(kvr, workloads, torch):
         pr = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, 425.0, 1800.0)
         pr.a1_per_token, pr.b2_per_token, pr.b3_per_token = a1, b2, b3
         call = kvr.BootstrapCall(w, T, idx, pr, g)
-        call.launch()
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(7):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            call.launch()
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = sorted(times)[len(times) // 2]
+        ms = _median_ms(torch, call.launch, 7)
         key = f"{wl.name}-{name}/bootstrap"
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
@@ -411,17 +382,8 @@ def time_replay(kvr, workloads, torch, reps: int = 8192):
         t2 = [kvr.kvr_eq3_timer(pr, 2 * lc), float("inf"), 600.0, 1800.0, 3600.0]
         arr = torch.as_tensor(rc.arrival_s).cuda()
         w = torch.as_tensor(rc.wait_s).cuda()
-        kvr.kvr_capacity_replay(arr, w, pr, t2)
-        torch.cuda.synchronize()
-        times = []
-        for _ in range(5):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            kvr.kvr_capacity_replay(arr, w, pr, t2, check=False)
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = sorted(times)[len(times) // 2]
+        kvr.kvr_capacity_replay(arr, w, pr, t2)   # checked once
+        ms = _median_ms(torch, lambda: kvr.kvr_capacity_replay(arr, w, pr, t2, check=False), 5)
         events = reps * len(t2) * rc.n
         key = f"replay-{family}-2x/{reps}x{rc.n}"
         res[key] = {"ms": ms, "replayed_requests": events,
@@ -445,15 +407,7 @@ def time_controller(kvr, workloads, torch, pr, reps: int):
         call = kvr.ControllerCall(arr, w, pr, 2 * lc)
         call.launch()
         out = call.result()
-        times = []
-        for _ in range(5):
-            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-            a.record()
-            call.launch()
-            b.record()
-            torch.cuda.synchronize()
-            times.append(a.elapsed_time(b))
-        ms = sorted(times)[len(times) // 2]
+        ms = _median_ms(torch, call.launch, 5)
         events = reps * 2 * rc.n
         key = f"controller-{family}-2x/{reps}x{rc.n}"
         res[key] = {"ms": ms, "replayed_requests": events,
@@ -619,9 +573,20 @@ def cpu_leg(wl, rows: int, draws, gpu_best, gpu_best_cost):
     return base, parity
 
 
-def _median_ms(torch, run, reps=5):
+def _warm(torch, run, ms=100.0):
+    """Runs ``run`` back to back for about ``ms`` of wall time, so that the
+    timed calls that follow see the clock a busy GPU runs at (a few short
+    calls after an idle spell are timed while the clock is still rising)."""
+    t0 = time.perf_counter()
     run()
     torch.cuda.synchronize()
+    while (time.perf_counter() - t0) * 1e3 < ms:
+        run()
+        torch.cuda.synchronize()
+
+
+def _median_ms(torch, run, reps=5):
+    _warm(torch, run)
     times = []
     for _ in range(reps):
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)

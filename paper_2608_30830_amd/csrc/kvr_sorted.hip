@@ -538,22 +538,29 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
 // Per scan tile: sums of T and T*w over the sorted order.  GATHER: the sort's
 // payload is the base index (perm) and the context sizes are gathered through
 // it once, into Tsorted; otherwise the payload already is the context size in
-// sorted order (Tsorted) and is only read.
-template <bool GATHER>
+// sorted order (Tsorted) and is only read.  CHUNKS: the sums of every run of 64
+// sorted positions are also written (chunkN, chunkS; run c of tile b is
+// c = 32 b + 4 q + wave, the positions of row q that a wave holds), so that N
+// and S at a few query positions can be formed without the full prefix arrays.
+template <bool GATHER, bool CHUNKS>
 __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
     const uint64_t *__restrict__ skeys, const int32_t *__restrict__ perm,
     const int32_t *__restrict__ T, int64_t n, int64_t *__restrict__ blkN,
-    double *__restrict__ blkS, int32_t *__restrict__ Tsorted)
+    double *__restrict__ blkS, int32_t *__restrict__ Tsorted, int64_t *__restrict__ chunkN,
+    double *__restrict__ chunkS)
 {
     // striped over the tile (element q*256 + t of it), so that every load and
     // store of a wave covers consecutive positions; the tile's total is summed
     // in this fixed order
     const int64_t base = (int64_t)blockIdx.x * kScanTile + threadIdx.x;
+    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     int64_t sn = 0;
     double ss = 0.0;
 #pragma unroll
     for (int q = 0; q < kScanIPT; ++q) {
         const int64_t j = base + (int64_t)q * kScanThreads;
+        int64_t en = 0;
+        double es = 0.0;
         if (j < n) {
             int32_t t;
             if (GATHER) {
@@ -564,16 +571,29 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
             } else {
                 t = Tsorted[j];   // clamped to >= 1 when the keys were prepared
             }
-            sn += t;
-            ss += (double)t * __longlong_as_double((long long)skeys[j]);
+            en = t;
+            es = (double)t * __longlong_as_double((long long)skeys[j]);
         }
+        if (CHUNKS) {   // this wave's 64 positions of row q, then into the wave's total
+            en = wave_sum(en);
+            es = wave_sum(es);
+            const int64_t c = ((int64_t)blockIdx.x * kScanIPT + q) * (kScanThreads / kWave) + wave;
+            if (lane == 0 && c * kWave < n) {
+                chunkN[c] = en;
+                chunkS[c] = es;
+            }
+        }
+        sn += en;
+        ss += es;
     }
-    // fixed-order tree: butterfly within each wave, then the four waves in order
-    sn = wave_sum(sn);
-    ss = wave_sum(ss);
+    // fixed-order tree: butterfly within each wave (done per chunk with
+    // CHUNKS), then the four waves in order
+    if (!CHUNKS) {
+        sn = wave_sum(sn);
+        ss = wave_sum(ss);
+    }
     __shared__ int64_t rn[kScanThreads / kWave];
     __shared__ double rs[kScanThreads / kWave];
-    const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     if (lane == 0) {
         rn[wave] = sn;
         rs[wave] = ss;
@@ -784,22 +804,70 @@ __device__ __forceinline__ int64_t wave_upper_bound(const uint64_t *__restrict__
 
 // The closed form of policy f for every load, from its two positions (counts of
 // sorted waits <= t1 and <= e); loads l0, l0 + lstep, ... are written.
-__device__ __forceinline__ void closed_form_policy(const int64_t *__restrict__ Nsum,
-                                                   const double *__restrict__ Ssum, int64_t n,
-                                                   const Tables &tb, const PriceDev &pr, int64_t f,
-                                                   double t1, double e, int64_t p1, int64_t pe,
-                                                   int l0, int lstep, double *__restrict__ cost)
+__device__ __forceinline__ void closed_form_values(int64_t tot, int64_t n1, int64_t ne, double s1,
+                                                   double se, int64_t n, const Tables &tb,
+                                                   const PriceDev &pr, int64_t f, double t1,
+                                                   double e, int l0, int lstep,
+                                                   double *__restrict__ cost)
 {
     const int64_t P = (int64_t)tb.K1 * tb.K2;
-    const int64_t tot = Nsum[n - 1];
-    const int64_t n1 = p1 ? Nsum[p1 - 1] : 0, ne = pe ? Nsum[pe - 1] : 0;
-    const double s1 = p1 ? Ssum[p1 - 1] : 0.0, se = pe ? Ssum[pe - 1] : 0.0;
     const double hbm = s1 + t1 * (double)(tot - n1);
     double hold = (se - s1) - t1 * (double)(ne - n1);
     if (!isinf(e)) hold += (e - t1) * (double)(tot - ne);
     const double fixed = pr.a1 * hbm + pr.b2 * (double)(ne - n1) + pr.b3 * (double)(tot - ne);
     const double nd = (double)n;
     for (int l = l0; l < tb.L; l += lstep) cost[(int64_t)l * P + f] = (fixed + tb.a2[l] * hold) / nd;
+}
+
+// The same from the inclusive prefix arrays.
+__device__ __forceinline__ void closed_form_policy(const int64_t *__restrict__ Nsum,
+                                                   const double *__restrict__ Ssum, int64_t n,
+                                                   const Tables &tb, const PriceDev &pr, int64_t f,
+                                                   double t1, double e, int64_t p1, int64_t pe,
+                                                   int l0, int lstep, double *__restrict__ cost)
+{
+    const int64_t tot = Nsum[n - 1];
+    const int64_t n1 = p1 ? Nsum[p1 - 1] : 0, ne = pe ? Nsum[pe - 1] : 0;
+    const double s1 = p1 ? Ssum[p1 - 1] : 0.0, se = pe ? Ssum[pe - 1] : 0.0;
+    closed_form_values(tot, n1, ne, s1, se, n, tb, pr, f, t1, e, l0, lstep, cost);
+}
+
+// N and S over the sorted positions [0, p), by one wave: the tile's exclusive
+// prefix, the 64-position chunk sums of the tile before p and the positions of
+// p's own chunk, each group added across the lanes in a fixed order; every
+// lane returns the same values, and equal p give equal values.
+__device__ __forceinline__ void wave_prefix_at(int64_t p, int nb, const int64_t *__restrict__ blkN,
+                                               const double *__restrict__ blkS,
+                                               const int64_t *__restrict__ chunkN,
+                                               const double *__restrict__ chunkS,
+                                               const uint64_t *__restrict__ skeys,
+                                               const int32_t *__restrict__ Tsorted, int64_t &N,
+                                               double &S)
+{
+    const int lane = threadIdx.x % kWave;
+    int64_t tile = p / kScanTile;
+    if (tile > nb - 1) tile = nb - 1;
+    const int64_t off = p - tile * kScanTile;     // 0 .. kScanTile
+    const int nc = (int)(off / kWave), rem = (int)(off % kWave);
+    int64_t cn = 0, en = 0;
+    double cs = 0.0, es = 0.0;
+    if (lane < nc) {
+        const int64_t c = tile * (kScanTile / kWave) + lane;
+        cn = chunkN[c];
+        cs = chunkS[c];
+    }
+    if (lane < rem) {
+        const int64_t j = tile * kScanTile + (int64_t)nc * kWave + lane;
+        const int32_t t = Tsorted[j];
+        en = t;
+        es = (double)t * __longlong_as_double((long long)skeys[j]);
+    }
+    cn = wave_sum(cn);
+    cs = wave_sum(cs);
+    en = wave_sum(en);
+    es = wave_sum(es);
+    N = blkN[tile] + cn + en;
+    S = (blkS[tile] + cs) + es;
 }
 
 // One thread per policy (a, k): closed form for every load (many policies).
@@ -837,6 +905,32 @@ __global__ void __launch_bounds__(256) closed_form_wave_kernel(const uint64_t *_
     const int64_t p1 = wave_upper_bound(skeys, n, t1);
     const int64_t pe = wave_upper_bound(skeys, n, e);
     closed_form_policy(Nsum, Ssum, n, tb, pr, f, t1, e, p1, pe, (int)(threadIdx.x % kWave), kWave,
+                       cost);
+}
+
+// One wave per policy, N and S at the query positions only (no prefix arrays):
+// the two positions by 64-ary searches, then wave_prefix_at for t1, the
+// deadline and the whole sample.
+__global__ void __launch_bounds__(256) closed_form_query_kernel(
+    const uint64_t *__restrict__ skeys, const int32_t *__restrict__ Tsorted, int64_t n, int nb,
+    const int64_t *__restrict__ blkN, const double *__restrict__ blkS,
+    const int64_t *__restrict__ chunkN, const double *__restrict__ chunkS, Tables tb, PriceDev pr,
+    double *__restrict__ cost)
+{
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    const int64_t f = (int64_t)blockIdx.x * (blockDim.x / kWave) + threadIdx.x / kWave;
+    if (f >= P) return;   // uniform per wave
+    const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
+    const double t1 = tb.t1[a];
+    const double e = t1 + tb.t2[k];
+    const int64_t p1 = wave_upper_bound(skeys, n, t1);
+    const int64_t pe = wave_upper_bound(skeys, n, e);
+    int64_t tot, n1, ne;
+    double sall, s1, se;
+    wave_prefix_at(n, nb, blkN, blkS, chunkN, chunkS, skeys, Tsorted, tot, sall);
+    wave_prefix_at(p1, nb, blkN, blkS, chunkN, chunkS, skeys, Tsorted, n1, s1);
+    wave_prefix_at(pe, nb, blkN, blkS, chunkN, chunkS, skeys, Tsorted, ne, se);
+    closed_form_values(tot, n1, ne, s1, se, n, tb, pr, f, t1, e, (int)(threadIdx.x % kWave), kWave,
                        cost);
 }
 
@@ -923,12 +1017,29 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
     hipError_t err = launch_sort(w, T, n, ws, want_perm ? 0 : 1, status, stream);
     if (err != hipSuccess) return err;
     int32_t *Tsorted = want_perm ? ws.vals[1] : ws.vals[0];   // buffer 1 is free after the sort
+    const int64_t P = (int64_t)tb.K1 * tb.K2;
+    if (!want_perm && P <= kWavePolicies) {
+        // N and S are needed at 2 P + 1 positions only: the tile sums, the
+        // 64-position chunk sums (in the prefix arrays' space) and the tiles'
+        // prefixes, then one wave per policy; no prefix arrays are written
+        hipLaunchKernelGGL((scan_reduce_kernel<false, true>), dim3(ws.nblocks_scan),
+                           dim3(kScanThreads), 0, stream, ws.keys[0], nullptr, T, n, ws.blkN,
+                           ws.blkS, Tsorted, ws.Nsum, ws.Ssum);
+        hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(1024), 0, stream, ws.blkN, ws.blkS,
+                           ws.nblocks_scan);
+        hipLaunchKernelGGL(closed_form_query_kernel, dim3((unsigned)cdiv(P, 256 / kWave)),
+                           dim3(256), 0, stream, ws.keys[0], Tsorted, n, ws.nblocks_scan, ws.blkN,
+                           ws.blkS, ws.Nsum, ws.Ssum, tb, pr, cost_out);
+        return hipGetLastError();
+    }
     if (want_perm)
-        hipLaunchKernelGGL(scan_reduce_kernel<true>, dim3(ws.nblocks_scan), dim3(kScanThreads), 0,
-                           stream, ws.keys[0], ws.vals[0], T, n, ws.blkN, ws.blkS, Tsorted);
+        hipLaunchKernelGGL((scan_reduce_kernel<true, false>), dim3(ws.nblocks_scan),
+                           dim3(kScanThreads), 0, stream, ws.keys[0], ws.vals[0], T, n, ws.blkN,
+                           ws.blkS, Tsorted, nullptr, nullptr);
     else
-        hipLaunchKernelGGL(scan_reduce_kernel<false>, dim3(ws.nblocks_scan), dim3(kScanThreads), 0,
-                           stream, ws.keys[0], nullptr, T, n, ws.blkN, ws.blkS, Tsorted);
+        hipLaunchKernelGGL((scan_reduce_kernel<false, false>), dim3(ws.nblocks_scan),
+                           dim3(kScanThreads), 0, stream, ws.keys[0], nullptr, T, n, ws.blkN,
+                           ws.blkS, Tsorted, nullptr, nullptr);
     hipLaunchKernelGGL(scan_blocks_kernel, dim3(1), dim3(1024), 0, stream, ws.blkN, ws.blkS,
                        ws.nblocks_scan);
     hipLaunchKernelGGL(scan_final_kernel, dim3(ws.nblocks_scan), dim3(kScanThreads), 0, stream,
