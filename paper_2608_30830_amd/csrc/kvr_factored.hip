@@ -19,8 +19,8 @@
 // Once per call: the base waits are radix-sorted; each t1 and each deadline
 // gets its count of waits at or below it (a sorted position, a query), and
 // the distinct query positions are numbered in order (slots).  Per batch of
-// resamples: factored_prefix_kernel (one block per resample: the draws'
-// multiplicities per sorted position in LDS, then, from LDS, a fixed-order
+// resamples: factored_prefix_kernel (one block per resample, two per CU: the
+// draws' multiplicities per sorted position in LDS, then, from LDS, a fixed-order
 // scan of the weights c_k T_k (exact) and c_k T_k w_k over the positions that
 // records N and S only at the query positions), factored_policy_kernel (one
 // block per (resample, tile of 32 or 16 loads): every policy from its two slots,
@@ -31,7 +31,11 @@
 namespace kvr {
 
 constexpr int kFThreads = 1024;
-constexpr int kFLdsWords = 32768;      // 128 KiB of LDS counters
+constexpr int kFPThreads = 512;         // prefix kernel: two blocks (resamples) per CU
+constexpr int kFLdsWords = 16384;       // 64 KiB of LDS counters per block
+constexpr int kFBits = 8;               // bits of a narrow multiplicity counter
+constexpr int kFPerWord = 32 / kFBits;  // narrow counters per LDS word
+constexpr uint32_t kFMask = (1u << kFBits) - 1u;
 constexpr int kFScanPer = 4;            // consecutive positions per thread in the scan
 constexpr int kFUnroll = 4;             // draws per thread and step, fetched together
 constexpr int kFLoads = 32;             // loads per policy-kernel block (16 when L <= 16)
@@ -155,20 +159,22 @@ __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict
 // sum_{j < k} c_j T_j w_j (reproducible) in the query row.  Position n (every
 // wait) closes the row; tot[rb] = N(n).
 //
-// Counters: 16-bit halves of 32-bit LDS words, kFLdsWords * 2 positions per
-// pass.  A half that passes 65535 carries into (or out of) its word, and that
-// only ever lowers the decoded total, so comparing the decoded total with the
-// number of draws in the range (counted exactly) detects it; the resample then
-// restarts with 32-bit counters, kFLdsWords positions per pass.
-__global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
+// Counters: 8-bit quarters of 32-bit LDS words, kFLdsWords * 4 positions per
+// pass (64 KiB, so that two blocks share a CU and one's barriers and gathers
+// overlap the other's).  A quarter that passes 255 carries into (or out of)
+// its word, and that only ever lowers the decoded total (a carry turns 256
+// counts into 1), so comparing the decoded total with the number of draws in
+// the range (counted exactly) detects it; the resample then restarts with
+// 32-bit counters, kFLdsWords positions per pass.
+__global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
     const int32_t *__restrict__ rank, const int32_t *__restrict__ Ts,
     const double *__restrict__ sw, const int32_t *__restrict__ qslot, int64_t nqs,
     unsigned long long *__restrict__ TN, double *__restrict__ TS,
     unsigned long long *__restrict__ tot, int *status)
 {
-    constexpr int nw = kFThreads / kWave;
-    constexpr int kTile = kFThreads * kFScanPer;
+    constexpr int nw = kFPThreads / kWave;
+    constexpr int kTile = kFPThreads * kFScanPer;
     __shared__ uint32_t lh[kFLdsWords];
     __shared__ unsigned long long wn[nw];
     __shared__ double wsd[nw];
@@ -182,13 +188,13 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
     unsigned long long carry_n = 0ull;   // totals of the earlier positions (same in every thread)
     double carry_s = 0.0;
     for (int wide = 0; wide < 2; ++wide) {
-        const int64_t PP = wide ? kFLdsWords : 2 * (int64_t)kFLdsWords;   // positions per pass
+        const int64_t PP = wide ? kFLdsWords : kFPerWord * (int64_t)kFLdsWords;   // positions per pass
         bool overflow = false;
         carry_n = 0ull;
         carry_s = 0.0;
         for (int64_t k0 = 0; k0 < n && !overflow; k0 += PP) {
             const int64_t nk = (n - k0 < PP) ? n - k0 : PP;
-            const int64_t nwords = wide ? nk : (nk + 1) / 2;
+            const int64_t nwords = wide ? nk : (nk + kFPerWord - 1) / kFPerWord;
             for (int64_t x = threadIdx.x; x < nwords; x += B) lh[x] = 0u;
             __syncthreads();
             long long inr = 0;                              // draws counted in this range
@@ -223,7 +229,7 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
                     if (kk[u] >= 0 && kk[u] < nk) {
                         ++inr;
                         if (wide) atomicAdd(&lh[kk[u]], 1u);
-                        else atomicAdd(&lh[kk[u] >> 1], 1u << (16 * (int)(kk[u] & 1)));
+                        else atomicAdd(&lh[kk[u] / kFPerWord], 1u << (kFBits * (int)(kk[u] % kFPerWord)));
                     }
                 }
             }
@@ -231,8 +237,11 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
             if (!wide) {
                 // decoded total minus the draws counted, over the whole block
                 long long d = -inr;
-                for (int64_t x = threadIdx.x; x < nwords; x += B)
-                    d += (long long)(lh[x] & 0xffffu) + (long long)(lh[x] >> 16);
+                for (int64_t x = threadIdx.x; x < nwords; x += B) {
+                    const uint32_t v = lh[x];
+#pragma unroll
+                    for (int h = 0; h < kFPerWord; ++h) d += (long long)((v >> (kFBits * h)) & kFMask);
+                }
                 d = wave_sum(d);
                 if (lane == 0) wchk[wv] = d;
                 __syncthreads();
@@ -250,7 +259,7 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
                 unsigned long long tn = 0ull;
                 double ts = 0.0;
                 // a full run of kFScanPer positions starts on a multiple of 4
-                // (pass starts are multiples of 2^15): one 16-byte load each
+                // (pass starts are multiples of 2^14): one 16-byte load each
                 // of Ts and qslot and two of sw instead of an element each
                 int32_t tv[kFScanPer], qv[kFScanPer];
                 double wv4[kFScanPer];
@@ -277,7 +286,7 @@ __global__ void __launch_bounds__(kFThreads) factored_prefix_kernel(
                     const int64_t k = kl + q;
                     const bool in = k < nk;
                     uint32_t c = 0u;
-                    if (in) c = wide ? lh[k] : (lh[k >> 1] >> (16 * (int)(k & 1))) & 0xffffu;
+                    if (in) c = wide ? lh[k] : (lh[k / kFPerWord] >> (kFBits * (int)(k % kFPerWord))) & kFMask;
                     const unsigned long long cwq =
                         in ? (unsigned long long)c * (unsigned long long)tv[q] : 0ull;
                     cw[q] = cwq;
@@ -490,7 +499,7 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     const int ntl = (tb.L + FL - 1) / FL;
     for (int64_t r0 = 0; r0 < R; r0 += ws.Rb) {
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
-        hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFThreads), 0, stream,
+        hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFPThreads), 0, stream,
                            src.idx, n, m, r0, ws.rank, ws.Ts, ws.sw, ws.qslot, ws.nqs, ws.TN, ws.TS,
                            ws.tot, status);
         if (FL == 16)

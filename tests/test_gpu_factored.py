@@ -130,25 +130,30 @@ def test_factored_domain_errors(kvr):
 
 @pytest.mark.parametrize("n", [1000, 100000])
 def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
-    """Rows that draw one base sample 65,535, 65,536 or 70,000 times (at an even
-    and at an odd sorted position), so that a 16-bit multiplicity counter
-    wraps: the kernel must detect it and recount the row with 32-bit counters.
-    With n = 100,000 the positions take two counting passes."""
+    """Rows that draw one base sample 255 or 256 times (at each of the four
+    sorted positions that share an LDS word), 65,535, 65,536 or 70,000 times,
+    so that an 8-bit multiplicity counter wraps (or just does not): the kernel
+    must detect a wrap and recount the row with 32-bit counters.  With
+    n = 100,000 the positions take two counting passes."""
     m = 70000
-    wl = workloads.random_case(208, n, 1, 9, 3, resamples=6, m=m, ties=True)
+    wl = workloads.random_case(208, n, 1, 9, 3, resamples=10, m=m, ties=True)
     order = np.argsort(wl.wait_s, kind="stable")
-    even, odd = int(order[10]), int(order[11])       # sorted positions 10 and 11
     rng = np.random.Generator(np.random.PCG64(209))
-    idx = rng.integers(0, n, size=(6, m), dtype=np.int32)
-    idx[0, :] = even                                  # 70,000 draws of one sample
-    idx[1, :] = odd
-    idx[2, :65536] = even                             # exactly 65,536
-    idx[3, :65536] = odd
-    idx[4, :65535] = odd                              # the largest count that fits
-    wl.idx = idx                                      # row 5 stays random
+    idx = rng.integers(0, n, size=(10, m), dtype=np.int32)
+    pos = lambda k: int(order[k])                    # the sample at sorted position k
+    idx[0, :] = pos(10)                               # 70,000 draws of one sample
+    idx[1, :] = pos(11)
+    idx[2, :65536] = pos(10)                          # exactly 65,536
+    idx[3, :65536] = pos(11)
+    idx[4, :65535] = pos(11)
+    idx[5, :255] = pos(12)                            # the largest count an 8-bit counter holds
+    idx[6, :256] = pos(13)                            # one more, at each byte of a word
+    idx[7, :256] = pos(14)
+    idx[8, :256] = pos(15)                            # (the top byte carries out of the word)
+    wl.idx = idx                                      # row 9 stays random
     best, bc, cost = _factored(kvr, wl, want_cost=True)
     pr = oracle_mod.workload_prices(wl)
-    for r in range(6):
+    for r in range(10):
         ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
                                    idx_row=idx[r])
         assert_costs(_np(cost)[r], ref)
