@@ -119,7 +119,8 @@ static int xg_tiles_per_block(int K1)
 
 __global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int ng, int parts,
                                                  int64_t part_len, double *X, double *G,
-                                                 double *xgp, int *status)
+                                                 double *xgp, const double2 *__restrict__ wT,
+                                                 int *status)
 {
     const int natiles = (tb.K1 + kAT - 1) / kAT;
     const int ngroups = (natiles + ng - 1) / ng;
@@ -145,10 +146,25 @@ __global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int n
     __shared__ double2 stage[2][kXT];
     auto fetch = [&](int64_t c) {                  // this thread's draw of chunk c
         const int64_t j = j0 + c * kXT + threadIdx.x;
-        if (j < j1) return fetch_sample(src, row_off, j, status);
         Sample z;                                  // padding: adds exact zeros
         z.w = 0.0;
         z.T = 0.0;
+        if (j >= j1) return z;
+        if (wT == nullptr) return fetch_sample(src, row_off, j, status);
+        // the cleaned (w, T) record of the drawn sample: one 16-byte gather
+        // (bad waits and contexts are flagged by the grid kernel's reads)
+        int64_t i = j;
+        if (src.idx) {
+            int32_t ii = src.idx[row_off + j];
+            if (ii < 0 || (int64_t)ii >= src.n) {
+                flag_domain(status);
+                ii = 0;
+            }
+            i = ii;
+        }
+        const double2 v = wT[i];
+        z.w = v.x;
+        z.T = v.y;
         return z;
     };
     Sample pre = nch > 0 ? fetch(0) : Sample{0.0, 0.0};
@@ -235,14 +251,14 @@ int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len)
 }
 
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     double *xgp, int *status, hipStream_t stream)
+                     double *xgp, const double2 *wT, int *status, hipStream_t stream)
 {
     const int ng = xg_tiles_per_block(tb.K1);
     const int ngroups = ((tb.K1 + kAT - 1) / kAT + ng - 1) / ng;
     int64_t part_len = 0;
     const int parts = xg_parts(R, tb.K1, src.m, &part_len);
     hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * ngroups * parts)), dim3(kXT), 0, stream, src,
-                       tb, ng, parts, part_len, X, G, xgp, status);
+                       tb, ng, parts, part_len, X, G, xgp, wT, status);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || parts == 1) return err;
     const int64_t RK1 = R * tb.K1;

@@ -66,6 +66,8 @@ struct ArgminCand {
 // with lb[f] >= nbins (infinite deadlines) have R3 = 0.
 struct R3Ws {
     int2 *binT;               // [n] (deadline bin of the wait, clamped context size)
+    double2 *wT;              // [n] (wait, context size) cleaned as fetch_sample cleans them,
+                              // one 16-byte record per base sample for xg_kernel's gathers
     int32_t *lb;              // [K1*K2] grid deadlines strictly below each policy's
     unsigned long long *S;    // [R][nbins] suffix sums of T over bins 1..nbins
     int64_t nbins;            // F, the number of finite grid deadlines
@@ -93,7 +95,7 @@ hipError_t launch_stage(int *status, double *const dst[3], const double *const s
 // parts (partials in xgp[parts][R][K1][2], summed in part order).
 int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len);
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     double *xgp, int *status, hipStream_t stream);
+                     double *xgp, const double2 *wT, int *status, hipStream_t stream);
 
 int r3_splits(int64_t R, int64_t m, int64_t *split_len);
 hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3Ws &ws,

@@ -30,29 +30,31 @@ constexpr int kR3Threads = 1024;
 constexpr int kR3BinsPerPass = 16384;  // 128 KiB of LDS counters per pass
 constexpr int kR3BinsSmall = 2048;     // 16 KiB: grids with few deadlines
 constexpr int kR3Unroll = 4;           // draws per thread and step, fetched together
+constexpr int kR3LdsTable = 4096;      // timer-table entries staged in LDS (32 KiB)
 
-// Number of grid deadlines fl(t1[a] + t2[k]) strictly below x.
-__device__ int32_t deadlines_below(const Tables &tb, double x)
+// Number of grid deadlines fl(t1[a] + t2[k]) strictly below x, from timer
+// tables t1[K1] and t2[K2] (in LDS when they fit there).
+__device__ int32_t deadlines_below(const double *t1v, int K1, const double *t2v, int K2, double x)
 {
     int32_t c = 0;
-    if (tb.K1 <= tb.K2) {
-        for (int a = 0; a < tb.K1; ++a) {
-            const double t1 = tb.t1[a];
-            int lo = 0, hi = tb.K2;   // first k with t1 + t2[k] >= x
+    if (K1 <= K2) {
+        for (int a = 0; a < K1; ++a) {
+            const double t1 = t1v[a];
+            int lo = 0, hi = K2;   // first k with t1 + t2[k] >= x
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
-                if (t1 + tb.t2[mid] < x) lo = mid + 1;
+                if (t1 + t2v[mid] < x) lo = mid + 1;
                 else hi = mid;
             }
             c += lo;
         }
     } else {
-        for (int k = 0; k < tb.K2; ++k) {
-            const double t2 = tb.t2[k];
-            int lo = 0, hi = tb.K1;   // first a with t1[a] + t2 >= x
+        for (int k = 0; k < K2; ++k) {
+            const double t2 = t2v[k];
+            int lo = 0, hi = K1;   // first a with t1[a] + t2 >= x
             while (lo < hi) {
                 const int mid = (lo + hi) >> 1;
-                if (tb.t1[mid] + t2 < x) lo = mid + 1;
+                if (t1v[mid] + t2 < x) lo = mid + 1;
                 else hi = mid;
             }
             c += lo;
@@ -68,8 +70,20 @@ __device__ int32_t deadlines_below(const Tables &tb, double x)
 __global__ void __launch_bounds__(256) r3_bins_kernel(const double *__restrict__ w,
                                                       const int32_t *__restrict__ T, int64_t n,
                                                       Tables tb, int2 *__restrict__ binT,
-                                                      int32_t *__restrict__ lb)
+                                                      int32_t *__restrict__ lb,
+                                                      double2 *__restrict__ wT)
 {
+    // the timer tables in LDS when both fit (every item searches them)
+    __shared__ double lt[kR3LdsTable];
+    const bool in_lds = tb.K1 + tb.K2 <= kR3LdsTable;   // uniform
+    const double *t1v = tb.t1, *t2v = tb.t2;
+    if (in_lds) {
+        for (int q = threadIdx.x; q < tb.K1 + tb.K2; q += blockDim.x)
+            lt[q] = q < tb.K1 ? tb.t1[q] : tb.t2[q - tb.K1];
+        __syncthreads();
+        t1v = lt;
+        t2v = lt + tb.K1;
+    }
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
     const int64_t P = (int64_t)tb.K1 * tb.K2;
     if (i < n) {
@@ -78,11 +92,12 @@ __global__ void __launch_bounds__(256) r3_bins_kernel(const double *__restrict__
         if (!(bits < 0x7ff0000000000000ull || bits == 0x8000000000000000ull)) x = 0.0;
         int32_t t = T[i];
         if (t < 1) t = 1;
-        binT[i] = make_int2(deadlines_below(tb, x + 0.0), t);
+        binT[i] = make_int2(deadlines_below(t1v, tb.K1, t2v, tb.K2, x + 0.0), t);
+        if (wT != nullptr) wT[i] = make_double2(x + 0.0, (double)t);
     } else if (i - n < P) {
         const int64_t f = i - n;
         const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
-        lb[f] = deadlines_below(tb, tb.t1[a] + tb.t2[k]);
+        lb[f] = deadlines_below(t1v, tb.K1, t2v, tb.K2, t1v[a] + t2v[k]);
     }
 }
 
@@ -215,7 +230,7 @@ hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3
 {
     const int64_t P = (int64_t)tb.K1 * tb.K2;
     hipLaunchKernelGGL(r3_bins_kernel, dim3((unsigned)((src.n + P + 255) / 256)), dim3(256), 0,
-                       stream, src.w, src.T, src.n, tb, ws.binT, ws.lb);
+                       stream, src.w, src.T, src.n, tb, ws.binT, ws.lb, ws.wT);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     if (ws.nbins == 0) return hipSuccess;   // every deadline infinite: R3 = 0
