@@ -25,6 +25,7 @@ constexpr int kSmallPer = kSmallThreads * kSmallSPT;           // samples per bl
 constexpr int kSmallMaxK1 = 8;
 constexpr int kSmallMaxK2 = 4096;
 constexpr int kSmallMaxBins = 4096;
+constexpr int kFinFlight = 16;   // finalize: histogram rows and split partials in flight per thread
 
 int small_sample_blocks(int64_t n) { return (int)((n + kSmallPer - 1) / kSmallPer); }
 
@@ -157,12 +158,12 @@ __global__ void __launch_bounds__(kSmallThreads) small_finalize_kernel(
     for (int64_t i = threadIdx.x; i < nbins; i += kSmallThreads) {
         unsigned long long v = 0ull;
         int b = 0;
-        for (; b + 8 <= nsb; b += 8) {   // eight rows in flight, added in block order
-            unsigned long long u[8];
+        for (; b + kFinFlight <= nsb; b += kFinFlight) {   // rows in flight, added in block order
+            unsigned long long u[kFinFlight];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) u[q] = hist[(int64_t)(b + q) * nbins + i];
+            for (int q = 0; q < kFinFlight; ++q) u[q] = hist[(int64_t)(b + q) * nbins + i];
 #pragma unroll
-            for (int q = 0; q < 8; ++q) v += u[q];
+            for (int q = 0; q < kFinFlight; ++q) v += u[q];
         }
         for (; b < nsb; ++b) v += hist[(int64_t)b * nbins + i];
         S[i] = v;
@@ -170,7 +171,15 @@ __global__ void __launch_bounds__(kSmallThreads) small_finalize_kernel(
     if ((int)threadIdx.x < 2 * tb.K1) {
         const int a = (int)threadIdx.x % tb.K1, which = (int)threadIdx.x / tb.K1;
         double v = 0.0;
-        for (int b = 0; b < nsb; ++b) v += xgp[((int64_t)b * tb.K1 + a) * 2 + which];
+        int b = 0;
+        for (; b + kFinFlight <= nsb; b += kFinFlight) {   // in flight, added in block order
+            double u[kFinFlight];
+#pragma unroll
+            for (int q = 0; q < kFinFlight; ++q) u[q] = xgp[((int64_t)(b + q) * tb.K1 + a) * 2 + which];
+#pragma unroll
+            for (int q = 0; q < kFinFlight; ++q) v += u[q];
+        }
+        for (; b < nsb; ++b) v += xgp[((int64_t)b * tb.K1 + a) * 2 + which];
         xg[a][which] = v;
     }
     __syncthreads();
@@ -212,12 +221,12 @@ __global__ void __launch_bounds__(kSmallThreads) small_finalize_kernel(
     const double *p0 = partials + row * P + f;
     double s = p0[0];
     int64_t q = 1;
-    for (; q + 8 <= nsg; q += 8) {   // eight loads in flight, added in split order
-        double v[8];
+    for (; q + kFinFlight <= nsg; q += kFinFlight) {   // loads in flight, added in split order
+        double v[kFinFlight];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) v[u] = p0[(q + u) * slice];
+        for (int u = 0; u < kFinFlight; ++u) v[u] = p0[(q + u) * slice];
 #pragma unroll
-        for (int u = 0; u < 8; ++u) s += v[u];
+        for (int u = 0; u < kFinFlight; ++u) s += v[u];
     }
     for (; q < nsg; ++q) s += p0[q * slice];
     cost_out[(int64_t)l * P + f] = (base + s) / md;
