@@ -156,8 +156,9 @@ struct SortWs {
     int32_t *vals[2];
     uint32_t *hist;       // [256][nblocks]
     uint32_t *counts;     // [256] digit totals of the current pass
-    int64_t *Nsum;        // [n] inclusive prefix of T (sorted order)
-    double *Ssum;         // [n] inclusive prefix of T*w (sorted order)
+    int64_t *Nsum;        // [n] inclusive prefix of T (sorted order), or the sums of T over
+                          // each run of 64 sorted positions when the closed form queries
+    double *Ssum;         // [n] the same for T*w
     int64_t *blkN;        // [nblocks_scan]
     double *blkS;         // [nblocks_scan]
     int nblocks;          // sort tiles

@@ -16,6 +16,12 @@
 // ranking scatter); no inter-workgroup waiting, so no forward-progress
 // assumption.  Ranking inside a tile is stable: a wave ranks its keys with a
 // ballot match on the digit, in input order.
+//
+// Scans: the closed form needs N and S only at t1, at each deadline and at
+// the whole sample.  Without a requested order they are formed there, from
+// the scan tiles' exclusive prefixes and the sums of every run of 64 sorted
+// positions; with an order requested (or very many policies) the full
+// inclusive prefix arrays are written and read.
 #include "kvr_device.h"
 
 namespace kvr {
