@@ -138,9 +138,9 @@ def main() -> int:
     args = ap.parse_args()
 
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print(json.dumps({"error": "this build runs on one GPU only; --gpus must be 1 "
-                                   "(the bootstrap batch would shard by resample with no "
-                                   "exchange; this build has no multi-GPU path)"}))
+        print(json.dumps({"error": "kvr runs on one GPU only; --gpus must be 1 (the "
+                                   "bootstrap batch would shard by resample with no exchange; "
+                                   "there is no multi-GPU path)"}))
         return 2
     if args.copy_calibration:
         return copy_calibration()
