@@ -112,7 +112,7 @@ struct BrutePlan {
     bool fused;              // nsplit == 1: costs finalised inside the grid kernel
     // workspace offsets
     size_t off_t1, off_t2, off_a2, off_X, off_G, off_xgp, off_cand, off_part, off_cost, total;
-    size_t off_binT, off_wT, off_lb, off_S;
+    size_t off_rec, off_lb, off_S;
     int64_t r3_bins;         // finite grid deadlines (bins kept per resample)
     int r3_nsplit;
     int64_t r3_split_len;
@@ -183,8 +183,7 @@ BrutePlan plan_brute(int64_t R, int64_t n, int64_t m, const kvr_policy_grid &g, 
         for (int32_t k = 0; k < K2; ++k)
             if (std::isfinite((g.t1[a] + 0.0) + g.t2[k])) ++bp.r3_bins;
     bp.r3_nsplit = kvr::r3_splits(R, m, &bp.r3_split_len);
-    bp.off_binT = take(sizeof(int32_t) * 2 * n);
-    bp.off_wT = take(sizeof(double) * 2 * n);
+    bp.off_rec = take(sizeof(kvr::SampleRec) * n);
     bp.off_lb = take(sizeof(int32_t) * P);
     bp.off_S = take(sizeof(uint64_t) * R * bp.r3_bins);
     bp.off_cand = bp.off_part = bp.off_cost = 0;
@@ -217,8 +216,7 @@ template <typename T> T *at(void *ws, size_t off) { return reinterpret_cast<T *>
 kvr::R3Ws r3_view(void *ws, const BrutePlan &bp)
 {
     kvr::R3Ws v{};
-    v.binT = at<int2>(ws, bp.off_binT);
-    v.wT = at<double2>(ws, bp.off_wT);
+    v.rec = at<kvr::SampleRec>(ws, bp.off_rec);
     v.lb = at<int32_t>(ws, bp.off_lb);
     v.S = at<unsigned long long>(ws, bp.off_S);
     v.nbins = bp.r3_bins;
@@ -442,8 +440,10 @@ int kvr::cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, in
         SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
         double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
         const kvr::R3Ws r3 = r3_view(d_ws, bp);
-        KVR_TRY(kvr::launch_r3(src, 1, tb, r3, status, s));   // also the (w, T) records
-        KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, at<double>(d_ws, bp.off_xgp), r3.wT, status, s));
+        const bool fuse = kvr::r3_fuses_xg(g->n_t1, r3.nsplit, r3.nbins);
+        KVR_TRY(kvr::launch_r3(src, 1, tb, r3, fuse ? X : nullptr, fuse ? G : nullptr, status, s));
+        if (!fuse)
+            KVR_TRY(kvr::launch_xg(src, 1, tb, X, G, at<double>(d_ws, bp.off_xgp), r3.rec, status, s));
         double *part = bp.fused ? nullptr : at<double>(d_ws, bp.off_part);
         KVR_MARK(g_prof_begin, s);
         KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, X, G, r3, bp.fused ? d_cost : nullptr,
@@ -517,9 +517,12 @@ int kvr_bootstrap(const double *d_wait_s, const int32_t *d_ctx_tokens, int64_t n
     SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};
     double *X = at<double>(d_ws, bp.off_X), *G = at<double>(d_ws, bp.off_G);
     const kvr::R3Ws r3 = r3_view(d_ws, bp);
-    KVR_TRY(kvr::launch_r3(src, n_resamples, tb, r3, status, s));   // also the (w, T) records
-    KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, at<double>(d_ws, bp.off_xgp), r3.wT, status,
+    const bool fuse = kvr::r3_fuses_xg(g->n_t1, r3.nsplit, r3.nbins);
+    KVR_TRY(kvr::launch_r3(src, n_resamples, tb, r3, fuse ? X : nullptr, fuse ? G : nullptr, status,
                            s));
+    if (!fuse)
+        KVR_TRY(kvr::launch_xg(src, n_resamples, tb, X, G, at<double>(d_ws, bp.off_xgp), r3.rec,
+                               status, s));
     const int64_t P = (int64_t)g->n_t1 * g->n_t2;
     if (bp.fused) {
         kvr::ArgminCand *cand = at<kvr::ArgminCand>(d_ws, bp.off_cand);

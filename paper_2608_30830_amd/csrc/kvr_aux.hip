@@ -119,7 +119,7 @@ static int xg_tiles_per_block(int K1)
 
 __global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int ng, int parts,
                                                  int64_t part_len, double *X, double *G,
-                                                 double *xgp, const double2 *__restrict__ wT,
+                                                 double *xgp, const SampleRec *__restrict__ rec,
                                                  int *status)
 {
     const int natiles = (tb.K1 + kAT - 1) / kAT;
@@ -150,8 +150,8 @@ __global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int n
         z.w = 0.0;
         z.T = 0.0;
         if (j >= j1) return z;
-        if (wT == nullptr) return fetch_sample(src, row_off, j, status);
-        // the cleaned (w, T) record of the drawn sample: one 16-byte gather
+        if (rec == nullptr) return fetch_sample(src, row_off, j, status);
+        // the cleaned record of the drawn sample: one 16-byte gather
         // (bad waits and contexts are flagged by the grid kernel's reads)
         int64_t i = j;
         if (src.idx) {
@@ -162,9 +162,9 @@ __global__ void __launch_bounds__(kXT) xg_kernel(SampleSrc src, Tables tb, int n
             }
             i = ii;
         }
-        const double2 v = wT[i];
-        z.w = v.x;
-        z.T = v.y;
+        const SampleRec v = rec[i];
+        z.w = v.w;
+        z.T = (double)v.T;
         return z;
     };
     Sample pre = nch > 0 ? fetch(0) : Sample{0.0, 0.0};
@@ -251,14 +251,14 @@ int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len)
 }
 
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     double *xgp, const double2 *wT, int *status, hipStream_t stream)
+                     double *xgp, const SampleRec *rec, int *status, hipStream_t stream)
 {
     const int ng = xg_tiles_per_block(tb.K1);
     const int ngroups = ((tb.K1 + kAT - 1) / kAT + ng - 1) / ng;
     int64_t part_len = 0;
     const int parts = xg_parts(R, tb.K1, src.m, &part_len);
     hipLaunchKernelGGL(xg_kernel, dim3((unsigned)(R * ngroups * parts)), dim3(kXT), 0, stream, src,
-                       tb, ng, parts, part_len, X, G, xgp, wT, status);
+                       tb, ng, parts, part_len, X, G, xgp, rec, status);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess || parts == 1) return err;
     const int64_t RK1 = R * tb.K1;

@@ -61,13 +61,21 @@ struct ArgminCand {
     int32_t pad;
 };
 
+// One base sample for the pre-passes over the draws: the number of grid
+// deadlines below its wait, its context size (>= 1) and its wait (finite,
+// >= 0; bad values replaced as fetch_sample replaces them).
+struct SampleRec {
+    int32_t bin;
+    int32_t T;
+    double w;
+};
+
 // Recompute share R3 per (resample, deadline), counted through deadline bins
 // (kvr_r3.hip).  S[r][x] is R3 of every policy f with lb[f] == x; policies
 // with lb[f] >= nbins (infinite deadlines) have R3 = 0.
 struct R3Ws {
-    int2 *binT;               // [n] (deadline bin of the wait, clamped context size)
-    double2 *wT;              // [n] (wait, context size) cleaned as fetch_sample cleans them,
-                              // one 16-byte record per base sample for xg_kernel's gathers
+    SampleRec *rec;           // [n] per base sample: deadline bin, clamped context size and
+                              // wait, cleaned as fetch_sample cleans them (one 16-byte gather)
     int32_t *lb;              // [K1*K2] grid deadlines strictly below each policy's
     unsigned long long *S;    // [R][nbins] suffix sums of T over bins 1..nbins
     int64_t nbins;            // F, the number of finite grid deadlines
@@ -95,11 +103,15 @@ hipError_t launch_stage(int *status, double *const dst[3], const double *const s
 // parts (partials in xgp[parts][R][K1][2], summed in part order).
 int xg_parts(int64_t R, int K1, int64_t m, int64_t *part_len);
 hipError_t launch_xg(const SampleSrc &src, int64_t R, const Tables &tb, double *X, double *G,
-                     double *xgp, const double2 *wT, int *status, hipStream_t stream);
+                     double *xgp, const SampleRec *rec, int *status, hipStream_t stream);
 
 int r3_splits(int64_t R, int64_t m, int64_t *split_len);
+// With X and G given (one t1 timer, one histogram block per resample: see
+// r3_fuses_xg), the histogram pass also forms X and G, and xg_kernel is not
+// needed.
+bool r3_fuses_xg(int K1, int nsplit, int64_t nbins);
 hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3Ws &ws,
-                     int *status, hipStream_t stream);
+                     double *X, double *G, int *status, hipStream_t stream);
 
 hipError_t launch_grid(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                        const GridPlan &plan, const double *X, const double *G, const R3Ws &r3,

@@ -63,15 +63,16 @@ __device__ int32_t deadlines_below(const double *t1v, int K1, const double *t2v,
     return c;
 }
 
-// Items 0..n-1: per base sample, its wait's bin and its (clamped) context
-// size, read as fetch_sample reads them (bad waits count as 0, contexts below
-// 1 as 1; the grid kernel flags both).  Items n..n+P-1: per policy f =
-// a*K2 + k, the number of grid deadlines strictly below its own.
+// Items 0..n-1: per base sample, one 16-byte record of its wait's bin, its
+// (clamped) context size and its wait, read as fetch_sample reads them (bad
+// waits count as 0, contexts below 1 as 1; the grid kernel flags both), so
+// that the passes over the draws gather one record per draw.  Items
+// n..n+P-1: per policy f = a*K2 + k, the number of grid deadlines strictly
+// below its own.
 __global__ void __launch_bounds__(256) r3_bins_kernel(const double *__restrict__ w,
                                                       const int32_t *__restrict__ T, int64_t n,
-                                                      Tables tb, int2 *__restrict__ binT,
-                                                      int32_t *__restrict__ lb,
-                                                      double2 *__restrict__ wT)
+                                                      Tables tb, SampleRec *__restrict__ rec,
+                                                      int32_t *__restrict__ lb)
 {
     // the timer tables in LDS when both fit (every item searches them)
     __shared__ double lt[kR3LdsTable];
@@ -92,8 +93,11 @@ __global__ void __launch_bounds__(256) r3_bins_kernel(const double *__restrict__
         if (!(bits < 0x7ff0000000000000ull || bits == 0x8000000000000000ull)) x = 0.0;
         int32_t t = T[i];
         if (t < 1) t = 1;
-        binT[i] = make_int2(deadlines_below(t1v, tb.K1, t2v, tb.K2, x + 0.0), t);
-        if (wT != nullptr) wT[i] = make_double2(x + 0.0, (double)t);
+        SampleRec v;
+        v.bin = deadlines_below(t1v, tb.K1, t2v, tb.K2, x + 0.0);
+        v.T = t;
+        v.w = x + 0.0;
+        rec[i] = v;
     } else if (i - n < P) {
         const int64_t f = i - n;
         const int a = (int)(f / tb.K2), k = (int)(f % tb.K2);
@@ -113,11 +117,11 @@ __global__ void __launch_bounds__(256) r3_zero_kernel(unsigned long long *__rest
 // (a small PER for grids with few deadlines leaves room for more resident
 // blocks).  A resample with one split owns its row of hist and stores it;
 // several splits add into a zeroed row.
-template <int PER>
+template <int PER, bool XG>
 __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
-    const int32_t *__restrict__ idx, int64_t n, int64_t m, const int2 *__restrict__ binT,
+    const int32_t *__restrict__ idx, int64_t n, int64_t m, const SampleRec *__restrict__ rec,
     int64_t nbins, int nsplit, int64_t split_len, unsigned long long *__restrict__ hist,
-    int *status)
+    const double *__restrict__ t1p, double *__restrict__ X, double *__restrict__ G, int *status)
 {
     __shared__ unsigned long long lh[PER];
     constexpr int64_t per = PER;
@@ -127,6 +131,11 @@ __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
     const int64_t j1 = (j0 + split_len < m) ? j0 + split_len : m;
     const int64_t B = blockDim.x;
     unsigned long long *row = hist + r * nbins;
+    // XG (one t1 timer, one block per resample): X = sum T*min(w, t1) and
+    // G = sum T*[w > t1] over the resample's draws, formed in the first pass
+    // in each thread's draw order, then across the block in a fixed order
+    double xs = 0.0, gs = 0.0;
+    const double t1 = XG ? t1p[0] : 0.0;
     for (int64_t b0 = 0; b0 < nbins; b0 += per) {
         const int64_t nb = (nbins - b0 < per) ? nbins - b0 : per;
         for (int64_t x = threadIdx.x; x < nb; x += blockDim.x) lh[x] = 0ull;
@@ -154,16 +163,27 @@ __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
                 ic[u] = out ? 0 : raw[u];               // a bad draw counts as sample 0
             }
             if (bad) flag_domain(status);
-            int2 bt[kR3Unroll];
+            SampleRec bt[kR3Unroll];
 #pragma unroll
             for (int u = 0; u < kR3Unroll; ++u) {
-                bt[u] = binT[ic[u]];
-                if (!inr[u]) bt[u] = make_int2(0, 0);   // bin 0 is never counted
+                bt[u] = rec[ic[u]];
+                if (!inr[u]) {   // bin 0 is never counted; T = 0 adds nothing to X, G
+                    bt[u].bin = 0;
+                    bt[u].T = 0;
+                }
             }
 #pragma unroll
             for (int u = 0; u < kR3Unroll; ++u) {
-                const int64_t b = (int64_t)bt[u].x - 1 - b0;   // bin 0 gives b < 0
-                if (b >= 0 && b < nb) atomicAdd(&lh[b], (unsigned long long)bt[u].y);
+                const int64_t b = (int64_t)bt[u].bin - 1 - b0;   // bin 0 gives b < 0
+                if (b >= 0 && b < nb) atomicAdd(&lh[b], (unsigned long long)bt[u].T);
+            }
+            if (XG && b0 == 0) {
+#pragma unroll
+                for (int u = 0; u < kR3Unroll; ++u) {
+                    const double T = (double)bt[u].T;
+                    xs = fma(T, fmin(bt[u].w, t1), xs);
+                    gs += (bt[u].w > t1) ? T : 0.0;
+                }
             }
         }
         __syncthreads();
@@ -174,6 +194,31 @@ __global__ void __launch_bounds__(kR3Threads) r3_hist_kernel(
         }
         __syncthreads();
     }
+    if (XG) {   // butterfly within each wave, then the waves in order
+        __shared__ double wx[kR3Threads / kWave], wg[kR3Threads / kWave];
+        xs = wave_sum(xs);
+        gs = wave_sum(gs);
+        const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
+        if (lane == 0) {
+            wx[wv] = xs;
+            wg[wv] = gs;
+        }
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            double a = 0.0, g = 0.0;
+            for (int q = 0; q < kR3Threads / kWave; ++q) {
+                a += wx[q];
+                g += wg[q];
+            }
+            X[r] = a;
+            G[r] = g;
+        }
+    }
+}
+
+bool r3_fuses_xg(int K1, int nsplit, int64_t nbins)
+{
+    return K1 == 1 && nsplit == 1 && nbins > 0;   // with no finite deadline the pass is skipped
 }
 
 // One block per resample: hist row -> suffix sums S[b] = sum_{b' >= b} hist[b'],
@@ -226,11 +271,11 @@ int r3_splits(int64_t R, int64_t m, int64_t *split_len)
 }
 
 hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3Ws &ws,
-                     int *status, hipStream_t stream)
+                     double *X, double *G, int *status, hipStream_t stream)
 {
     const int64_t P = (int64_t)tb.K1 * tb.K2;
     hipLaunchKernelGGL(r3_bins_kernel, dim3((unsigned)((src.n + P + 255) / 256)), dim3(256), 0,
-                       stream, src.w, src.T, src.n, tb, ws.binT, ws.lb, ws.wT);
+                       stream, src.w, src.T, src.n, tb, ws.rec, ws.lb);
     hipError_t err = hipGetLastError();
     if (err != hipSuccess) return err;
     if (ws.nbins == 0) return hipSuccess;   // every deadline infinite: R3 = 0
@@ -240,14 +285,25 @@ hipError_t launch_r3(const SampleSrc &src, int64_t R, const Tables &tb, const R3
                            stream, ws.S, cnt);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
-    if (ws.nbins <= kR3BinsSmall)
-        hipLaunchKernelGGL(r3_hist_kernel<kR3BinsSmall>, dim3((unsigned)(R * ws.nsplit)),
-                           dim3(kR3Threads), 0, stream, src.idx, src.n, src.m, ws.binT, ws.nbins,
-                           ws.nsplit, ws.split_len, ws.S, status);
+    const bool xg = X != nullptr;   // r3_fuses_xg held on the host
+    const double *t1 = tb.t1;
+    const dim3 grid((unsigned)(R * ws.nsplit)), block(kR3Threads);
+    if (ws.nbins <= kR3BinsSmall && xg)
+        hipLaunchKernelGGL((r3_hist_kernel<kR3BinsSmall, true>), grid, block, 0, stream, src.idx,
+                           src.n, src.m, ws.rec, ws.nbins, ws.nsplit, ws.split_len, ws.S, t1, X,
+                           G, status);
+    else if (ws.nbins <= kR3BinsSmall)
+        hipLaunchKernelGGL((r3_hist_kernel<kR3BinsSmall, false>), grid, block, 0, stream, src.idx,
+                           src.n, src.m, ws.rec, ws.nbins, ws.nsplit, ws.split_len, ws.S, t1,
+                           nullptr, nullptr, status);
+    else if (xg)
+        hipLaunchKernelGGL((r3_hist_kernel<kR3BinsPerPass, true>), grid, block, 0, stream, src.idx,
+                           src.n, src.m, ws.rec, ws.nbins, ws.nsplit, ws.split_len, ws.S, t1, X,
+                           G, status);
     else
-        hipLaunchKernelGGL(r3_hist_kernel<kR3BinsPerPass>, dim3((unsigned)(R * ws.nsplit)),
-                           dim3(kR3Threads), 0, stream, src.idx, src.n, src.m, ws.binT, ws.nbins,
-                           ws.nsplit, ws.split_len, ws.S, status);
+        hipLaunchKernelGGL((r3_hist_kernel<kR3BinsPerPass, false>), grid, block, 0, stream,
+                           src.idx, src.n, src.m, ws.rec, ws.nbins, ws.nsplit, ws.split_len, ws.S,
+                           t1, nullptr, nullptr, status);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     hipLaunchKernelGGL(r3_suffix_kernel, dim3((unsigned)R), dim3(kR3Threads), 0, stream, ws.S,
                        ws.nbins);
