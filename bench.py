@@ -287,7 +287,7 @@ def time_paths(kvr, workloads, torch):
             call = kvr.CostGridCall(w, T, pr, g, method=method)
             run = call.launch
             key = f"{name}/{'sorted' if method == kvr.KVR_SORTED else 'brute'}"
-        ms = _median_ms(torch, run, 7)
+        ms = _median_ms(torch, run, 11)
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
         log(f"[bench] path {key}: {ms:.3f} ms")
@@ -307,7 +307,7 @@ SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 12 + 16 / 64
 
 def time_factored(kvr, workloads, torch):
     """kvr_bootstrap_factored on boot-1024x64k and twotier-4096x64k (median of
-    seven calls, inputs resident)."""
+    eleven calls after about 100 ms of calls, inputs resident)."""
     res = {}
     for name in ("boot-1024x64k", "twotier-4096x64k"):
         wl = workloads.make(name)
@@ -319,7 +319,7 @@ def time_factored(kvr, workloads, torch):
         call = kvr.BootstrapCall(torch.as_tensor(wl.wait_s).cuda(),
                                  torch.as_tensor(wl.ctx_tokens).cuda(),
                                  torch.as_tensor(wl.idx).cuda(), pr, g, factored=True)
-        ms = _median_ms(torch, call.launch, 7)
+        ms = _median_ms(torch, call.launch, 11)
         key = f"{name}/factored"
         res[key] = {"ms": ms}
         log(f"[bench] path {key}: {ms:.3f} ms")
@@ -340,7 +340,7 @@ def time_sort_scale(kvr, workloads, torch):
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
         call = kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED)
-        ms = _median_ms(torch, call.launch, 9)
+        ms = _median_ms(torch, call.launch, 11)
         bps = SORT_BYTES_PER_KEY * wl.n / (ms * 1e-3)
         res[wl.name] = {"ms": ms, "keys_per_s": wl.n / (ms * 1e-3), "algorithmic_bytes_per_s": bps,
                         "hbm_frac": bps / (HBM_PEAK_TBS * 1e12)}
@@ -361,7 +361,7 @@ def time_platforms(kvr, workloads, torch):
         pr = kvr.kvr_prices_from_platform(1.0, 1.0, 1.0, 1.0, 1.0, 425.0, 1800.0)
         pr.a1_per_token, pr.b2_per_token, pr.b3_per_token = a1, b2, b3
         call = kvr.BootstrapCall(w, T, idx, pr, g)
-        ms = _median_ms(torch, call.launch, 7)
+        ms = _median_ms(torch, call.launch, 11)
         key = f"{wl.name}-{name}/bootstrap"
         res[key] = {"ms": ms, "evaluations": wl.evaluations,
                     "evaluations_per_s": wl.evaluations / (ms * 1e-3)}
@@ -383,7 +383,7 @@ def time_replay(kvr, workloads, torch, reps: int = 8192):
         arr = torch.as_tensor(rc.arrival_s).cuda()
         w = torch.as_tensor(rc.wait_s).cuda()
         kvr.kvr_capacity_replay(arr, w, pr, t2)   # checked once
-        ms = _median_ms(torch, lambda: kvr.kvr_capacity_replay(arr, w, pr, t2, check=False), 5)
+        ms = _median_ms(torch, lambda: kvr.kvr_capacity_replay(arr, w, pr, t2, check=False), 11)
         events = reps * len(t2) * rc.n
         key = f"replay-{family}-2x/{reps}x{rc.n}"
         res[key] = {"ms": ms, "replayed_requests": events,
@@ -407,7 +407,7 @@ def time_controller(kvr, workloads, torch, pr, reps: int):
         call = kvr.ControllerCall(arr, w, pr, 2 * lc)
         call.launch()
         out = call.result()
-        ms = _median_ms(torch, call.launch, 5)
+        ms = _median_ms(torch, call.launch, 11)
         events = reps * 2 * rc.n
         key = f"controller-{family}-2x/{reps}x{rc.n}"
         res[key] = {"ms": ms, "replayed_requests": events,
@@ -617,7 +617,7 @@ def results_table(kvr, workloads, torch, cpu_evals=2.0e9):
         g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
         w = torch.as_tensor(wl.wait_s).cuda()
         T = torch.as_tensor(wl.ctx_tokens).cuda()
-        reps = 3 if name.startswith("twotier") else 5
+        reps = 3 if name.startswith("twotier") else 11
         if wl.idx is None:
             brute = _median_ms(torch, kvr.CostGridCall(w, T, pr, g).launch, reps)
             closed = _median_ms(torch, kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED).launch,
