@@ -19,8 +19,8 @@
 // Once per call: the base waits are radix-sorted; each t1 and each deadline
 // gets its count of waits at or below it (a sorted position, a query), and
 // the distinct query positions are numbered in order (slots).  Per batch of
-// resamples: factored_prefix_kernel (one block per resample, two per CU: the
-// draws' multiplicities per sorted position in LDS, then, from LDS, a fixed-order
+// resamples: factored_prefix_kernel (one block per resample, four per CU: the
+// draws' multiplicities per base sample in LDS, then, from LDS, a fixed-order
 // scan of the weights c_k T_k (exact) and c_k T_k w_k over the positions that
 // records N and S only at the query positions), factored_policy_kernel (one
 // block per (resample, tile of 32 or 16 loads): every policy from its two slots,
@@ -31,9 +31,9 @@
 namespace kvr {
 
 constexpr int kFThreads = 1024;
-constexpr int kFPThreads = 512;         // prefix kernel: two blocks (resamples) per CU
-constexpr int kFLdsWords = 16384;       // 64 KiB of LDS counters per block
-constexpr int kFBits = 8;               // bits of a narrow multiplicity counter
+constexpr int kFPThreads = 256;         // prefix kernel: four blocks (resamples) per CU
+constexpr int kFLdsWords = 8192;        // 32 KiB of LDS counters per block
+constexpr int kFBits = 4;               // bits of a narrow multiplicity counter
 constexpr int kFPerWord = 32 / kFBits;  // narrow counters per LDS word
 constexpr uint32_t kFMask = (1u << kFBits) - 1u;
 constexpr int kFScanPer = 4;            // consecutive positions per thread in the scan
@@ -112,30 +112,53 @@ __global__ void __launch_bounds__(256) factored_mark_kernel(const int32_t *__res
 }
 
 // One block: numbers the marked positions 0, 1, ... in position order
-// (exclusive count of marks below), unmarked positions stay -1.
+// (exclusive count of marks below), unmarked positions stay -1.  Each wave
+// takes one contiguous segment of the positions, read 64 consecutive
+// positions per lane step with eight steps' loads in flight: it counts its
+// marks, one scan across the waves gives each segment its first number, and
+// a second pass numbers the marks (ballot and lane prefix counts).
 __global__ void __launch_bounds__(kFThreads) factored_slot_kernel(int32_t *__restrict__ qslot,
                                                                   int64_t len)
 {
-    constexpr int nw = kFThreads / kWave;
-    __shared__ int32_t wcount[nw];
+    constexpr int nw = kFThreads / kWave, kIn = 8;
+    __shared__ int32_t wsum[nw];
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
-    int32_t carry = 0;
-    for (int64_t base = 0; base < len; base += kFThreads) {
-        const int64_t p = base + threadIdx.x;
-        const bool marked = p < len && qslot[p] >= 0;
-        const uint64_t bal = __ballot(marked);
-        const int32_t below = (int32_t)__builtin_amdgcn_mbcnt_hi(
-            (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-        if (lane == 0) wcount[wv] = (int32_t)__popcll(bal);
-        __syncthreads();
-        int32_t before = carry, all = 0;
-        for (int q = 0; q < nw; ++q) {
-            if (q < wv) before += wcount[q];
-            all += wcount[q];
+    const int64_t seg = (len + nw - 1) / nw;
+    const int64_t s0 = (int64_t)wv * seg;
+    const int64_t s1 = (s0 + seg < len) ? s0 + seg : len;
+    int32_t cnt = 0;   // this lane's marks (summed over the wave below)
+    for (int64_t b = s0; b < s1; b += kIn * kWave) {
+        int32_t v[kIn];
+#pragma unroll
+        for (int u = 0; u < kIn; ++u) {
+            const int64_t p = b + u * kWave + lane;
+            v[u] = p < s1 ? qslot[p] : -1;
         }
-        if (marked) qslot[p] = before + below;
-        carry += all;
-        __syncthreads();
+#pragma unroll
+        for (int u = 0; u < kIn; ++u) cnt += v[u] >= 0 ? 1 : 0;
+    }
+    cnt = wave_sum(cnt);
+    if (lane == 0) wsum[wv] = cnt;
+    __syncthreads();
+    int32_t next = 0;   // marks in the earlier segments
+    for (int q = 0; q < wv; ++q) next += wsum[q];
+    for (int64_t b = s0; b < s1; b += kIn * kWave) {
+        int32_t v[kIn];
+#pragma unroll
+        for (int u = 0; u < kIn; ++u) {
+            const int64_t p = b + u * kWave + lane;
+            v[u] = p < s1 ? qslot[p] : -1;
+        }
+#pragma unroll
+        for (int u = 0; u < kIn; ++u) {
+            const int64_t p = b + u * kWave + lane;
+            const bool marked = v[u] >= 0;
+            const uint64_t bal = __ballot(marked);
+            const int32_t below = (int32_t)__builtin_amdgcn_mbcnt_hi(
+                (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
+            if (marked) qslot[p] = next + below;
+            next += (int32_t)__popcll(bal);
+        }
     }
 }
 
@@ -159,16 +182,21 @@ __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict
 // sum_{j < k} c_j T_j w_j (reproducible) in the query row.  Position n (every
 // wait) closes the row; tot[rb] = N(n).
 //
-// Counters: 8-bit quarters of 32-bit LDS words, kFLdsWords * 4 positions per
-// pass (64 KiB, so that two blocks share a CU and one's barriers and gathers
-// overlap the other's).  A quarter that passes 255 carries into (or out of)
-// its word, and that only ever lowers the decoded total (a carry turns 256
-// counts into 1), so comparing the decoded total with the number of draws in
-// the range (counted exactly) detects it; the resample then restarts with
-// 32-bit counters, kFLdsWords positions per pass.
+// Counters: kFBits-bit fields of 32-bit LDS words, kFLdsWords * kFPerWord
+// positions per pass (32 KiB, so that four blocks share a CU and one's
+// barriers and loads overlap the others').  When that covers every position
+// the draws are counted by base sample instead (no rank gather per draw) and
+// the scan reads each position's count through the sort order.  A field that
+// passes its maximum carries into (or out of) its word, and that only ever
+// lowers the decoded total (a carry turns 2^kFBits counts into 1), so
+// comparing the decoded total with the number of draws in the range (counted
+// exactly) detects it; the resample then restarts with 32-bit counters by
+// sorted position, kFLdsWords positions per pass.  A bootstrap row's
+// multiplicities are Poisson(1)-like, so 4-bit fields almost never wrap.
 __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
-    const int32_t *__restrict__ rank, const int32_t *__restrict__ Ts,
+    const int32_t *__restrict__ rank, const int32_t *__restrict__ perm,
+    const int32_t *__restrict__ Ts,
     const double *__restrict__ sw, const int32_t *__restrict__ qslot, int64_t nqs,
     unsigned long long *__restrict__ TN, double *__restrict__ TS,
     unsigned long long *__restrict__ tot, int *status)
@@ -195,6 +223,10 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
         for (int64_t k0 = 0; k0 < n && !overflow; k0 += PP) {
             const int64_t nk = (n - k0 < PP) ? n - k0 : PP;
             const int64_t nwords = wide ? nk : (nk + kFPerWord - 1) / kFPerWord;
+            // narrow counters over every position at once (n <= PP): count by
+            // base sample instead of sorted position, so a draw needs no rank
+            // gather; the scan then finds each position's count through perm
+            const bool byidx = !wide && nk == n;
             for (int64_t x = threadIdx.x; x < nwords; x += B) lh[x] = 0u;
             __syncthreads();
             long long inr = 0;                              // draws counted in this range
@@ -221,7 +253,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                 int64_t kk[kFUnroll];
 #pragma unroll
                 for (int u = 0; u < kFUnroll; ++u) {
-                    kk[u] = (int64_t)rank[ii[u]] - k0;
+                    kk[u] = byidx ? (int64_t)ii[u] : (int64_t)rank[ii[u]] - k0;
                     if (!live[u]) kk[u] = -1;                // past the row: no draw
                 }
 #pragma unroll
@@ -261,7 +293,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                 // a full run of kFScanPer positions starts on a multiple of 4
                 // (pass starts are multiples of 2^14): one 16-byte load each
                 // of Ts and qslot and two of sw instead of an element each
-                int32_t tv[kFScanPer], qv[kFScanPer];
+                int32_t tv[kFScanPer], qv[kFScanPer], pv[kFScanPer];
                 double wv4[kFScanPer];
                 if (kl + kFScanPer <= nk) {
                     static_assert(kFScanPer == 4, "the vector loads below read 4 positions");
@@ -272,6 +304,10 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                     tv[0] = t4.x; tv[1] = t4.y; tv[2] = t4.z; tv[3] = t4.w;
                     qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
                     wv4[0] = w0.x; wv4[1] = w0.y; wv4[2] = w1.x; wv4[3] = w1.y;
+                    if (byidx) {
+                        const int4 p4 = *reinterpret_cast<const int4 *>(perm + k0 + kl);
+                        pv[0] = p4.x; pv[1] = p4.y; pv[2] = p4.z; pv[3] = p4.w;
+                    }
                 } else {
 #pragma unroll
                     for (int q = 0; q < kFScanPer; ++q) {
@@ -279,6 +315,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                         tv[q] = (k < nk) ? Ts[k0 + k] : 0;
                         qv[q] = (k < nk) ? qslot[k0 + k] : -1;
                         wv4[q] = (k < nk) ? sw[k0 + k] : 0.0;
+                        if (byidx) pv[q] = (k < nk) ? perm[k0 + k] : 0;
                     }
                 }
 #pragma unroll
@@ -286,7 +323,9 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                     const int64_t k = kl + q;
                     const bool in = k < nk;
                     uint32_t c = 0u;
-                    if (in) c = wide ? lh[k] : (lh[k / kFPerWord] >> (kFBits * (int)(k % kFPerWord))) & kFMask;
+                    // the counter of position k, or of the base sample there
+                    const int64_t ck = byidx ? (int64_t)((uint32_t)pv[q] < (uint32_t)n ? pv[q] : 0) : k;
+                    if (in) c = wide ? lh[k] : (lh[ck / kFPerWord] >> (kFBits * (int)(ck % kFPerWord))) & kFMask;
                     const unsigned long long cwq =
                         in ? (unsigned long long)c * (unsigned long long)tv[q] : 0ull;
                     cw[q] = cwq;
@@ -500,8 +539,8 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     for (int64_t r0 = 0; r0 < R; r0 += ws.Rb) {
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
         hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFPThreads), 0, stream,
-                           src.idx, n, m, r0, ws.rank, ws.Ts, ws.sw, ws.qslot, ws.nqs, ws.TN, ws.TS,
-                           ws.tot, status);
+                           src.idx, n, m, r0, ws.rank, ws.sort.vals[cur], ws.Ts, ws.sw, ws.qslot,
+                           ws.nqs, ws.TN, ws.TS, ws.tot, status);
         if (FL == 16)
             hipLaunchKernelGGL(factored_policy_kernel<16>, dim3((unsigned)(rb * ntl)),
                                dim3(kFPolThreads), 0, stream, ws.TN, ws.TS, ws.nqs, ws.tot, m, r0,

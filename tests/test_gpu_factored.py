@@ -130,11 +130,13 @@ def test_factored_domain_errors(kvr):
 
 @pytest.mark.parametrize("n", [1000, 100000])
 def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
-    """Rows that draw one base sample 255 or 256 times (at each of the four
-    sorted positions that share an LDS word), 65,535, 65,536 or 70,000 times,
-    so that an 8-bit multiplicity counter wraps (or just does not): the kernel
-    must detect a wrap and recount the row with 32-bit counters.  With
-    n = 100,000 the positions take two counting passes."""
+    """Rows that draw one base sample 15 or 16 times (the largest count a 4-bit
+    multiplicity counter holds, and one more, in the lowest, a middle and the
+    top field of an LDS word), 256, 65,535, 65,536 or 70,000 times, so that a
+    narrow counter wraps (or just does not): the kernel must detect a wrap
+    and recount the row with 32-bit counters.  With n = 1,000 the draws are
+    counted by base sample; with n = 100,000 by sorted position, in two
+    passes."""
     m = 70000
     wl = workloads.random_case(208, n, 1, 9, 3, resamples=10, m=m, ties=True)
     order = np.argsort(wl.wait_s, kind="stable")
@@ -146,10 +148,11 @@ def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
     idx[2, :65536] = pos(10)                          # exactly 65,536
     idx[3, :65536] = pos(11)
     idx[4, :65535] = pos(11)
-    idx[5, :255] = pos(12)                            # the largest count an 8-bit counter holds
-    idx[6, :256] = pos(13)                            # one more, at each byte of a word
-    idx[7, :256] = pos(14)
-    idx[8, :256] = pos(15)                            # (the top byte carries out of the word)
+    for row, (sample, times) in zip((5, 6, 7), ((8, 15), (12, 16), (15, 16))):
+        idx[row][idx[row] == sample] = sample + 1     # exactly `times` draws of `sample`:
+        idx[row, :times] = sample                     # 15 fit a 4-bit field (word 1, field 0),
+                                                      # 16 wrap a middle and the top field
+    idx[8, :256] = pos(13)
     wl.idx = idx                                      # row 9 stays random
     best, bc, cost = _factored(kvr, wl, want_cost=True)
     pr = oracle_mod.workload_prices(wl)
