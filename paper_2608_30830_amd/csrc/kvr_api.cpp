@@ -225,19 +225,22 @@ kvr::R3Ws r3_view(void *ws, const BrutePlan &bp)
     return v;
 }
 
-// Workspace of the four-launch brute force for one small sample
+// Workspace of the one-launch brute force for one small sample
 // (kvr::small_path_fits): after bp's tables, the pre-pass blocks' rows of the
 // recompute histogram over the F finite deadlines, each policy's deadline
-// bin, the per-block X/G partials and the grid kernel's split partials
-// (always written, even for one split).
+// bin, the per-block X/G partials, the histogram's suffix sums, X and G, the
+// grid blocks' split partials (always written, even for one split) and the
+// arrival counters.
 struct SmallPlan {
-    size_t off_hist, off_lb, off_xgp, off_part, total;
+    size_t off_hist, off_lb, off_xgp, off_S, off_XG, off_part, off_ctr, total;
     size_t part_bytes;
+    int nctr;
 };
 
 bool small_plan_applies(const BrutePlan &bp, const kvr_policy_grid &g, int64_t n)
 {
-    return kvr::small_path_fits(g.n_t1, g.n_t2, bp.r3_bins, n);
+    return kvr::small_path_fits(g.n_t1, g.n_t2, bp.r3_bins, n) &&
+           bp.gp.ngroups * bp.gp.ntiles <= kvr::kSmallMaxGroupTiles;
 }
 
 // Splits of the small-sample path: blocks of kSmallWaves waves add their
@@ -271,9 +274,14 @@ SmallPlan plan_small(const BrutePlan &bp, int64_t n, const kvr_policy_grid &g)
                        kvr::small_sample_blocks(n));
     sp.off_lb = take(sizeof(int32_t) * P);
     sp.off_xgp = take(sizeof(double) * 2 * g.n_t1 * kvr::small_sample_blocks(n));
+    sp.off_S = take(sizeof(uint64_t) * std::max<int64_t>(1, bp.r3_bins));
+    sp.off_XG = take(sizeof(double) * 2 * g.n_t1);
+    const int64_t nbatch = cdiv(cdiv(bp.gp.nsplit, bp.gp.wpb), kvr::kSmallBatchGroups);
+    sp.nctr = (int)(1 + bp.gp.ngroups * bp.gp.ntiles * (1 + nbatch));
+    sp.off_ctr = take(sizeof(unsigned) * sp.nctr);
     const int64_t nsg = cdiv(bp.gp.nsplit, bp.gp.wpb);
     sp.part_bytes = sizeof(double) * (size_t)nsg * bp.gp.ntiles * bp.gp.LT * P;
-    sp.off_part = take(sp.part_bytes);
+    sp.off_part = take(sp.part_bytes);   // last: the part a workspace bound trims
     sp.total = off;
     return sp;
 }
@@ -287,9 +295,10 @@ int hip_ok(hipError_t e) { return e == hipSuccess ? KVR_OK : KVR_E_HIP; }
     } while (0)
 
 // Uploads t1, t2 (canonical zeros) and the padded a2 table and clears the status
-// word (one launch when the tables are small).
+// word and zero[0..nzero) (one launch when the tables are small).
 int stage_tables(void *ws, size_t off_t1, size_t off_t2, size_t off_a2, int32_t Lpad,
-                 const kvr_prices &p, const kvr_policy_grid &g, hipStream_t s, Tables &tb)
+                 const kvr_prices &p, const kvr_policy_grid &g, hipStream_t s, Tables &tb,
+                 unsigned *zero = nullptr, int nzero = 0)
 {
     std::vector<double> t1(g.t1, g.t1 + g.n_t1), t2(g.t2, g.t2 + g.n_t2), a2;
     for (double &v : t1) v = v + 0.0;
@@ -297,7 +306,7 @@ int stage_tables(void *ws, size_t off_t1, size_t off_t2, size_t off_a2, int32_t 
     double *const dst[3] = {at<double>(ws, off_t1), at<double>(ws, off_t2), at<double>(ws, off_a2)};
     const double *const src[3] = {t1.data(), t2.data(), a2.data()};
     const int64_t cnt[3] = {g.n_t1, g.n_t2, Lpad};
-    KVR_TRY(kvr::launch_stage(static_cast<int *>(ws), dst, src, cnt, s));
+    KVR_TRY(kvr::launch_stage(static_cast<int *>(ws), dst, src, cnt, zero, nzero, s));
     tb.t1 = at<double>(ws, off_t1);
     tb.t2 = at<double>(ws, off_t2);
     tb.a2 = at<double>(ws, off_a2);
@@ -417,21 +426,24 @@ int kvr::cost_grid_entry(const double *d_wait_s, const int32_t *d_ctx_tokens, in
     const PriceDev pr = device_prices(p);
     Tables tb{};
     if (method == KVR_BRUTE && small) {
-        unsigned long long *hist = at<unsigned long long>(d_ws, sp.off_hist);
-        if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb)) != KVR_OK)
+        kvr::SmallWs sw{};
+        sw.hist = at<unsigned long long>(d_ws, sp.off_hist);
+        sw.lb = at<int32_t>(d_ws, sp.off_lb);
+        sw.xgp = at<double>(d_ws, sp.off_xgp);
+        sw.S = at<unsigned long long>(d_ws, sp.off_S);
+        sw.XG = at<double>(d_ws, sp.off_XG);
+        sw.partials = at<double>(d_ws, sp.off_part);
+        sw.ctr = at<unsigned>(d_ws, sp.off_ctr);
+        sw.nbins = bp.r3_bins;
+        sw.nsb = kvr::small_sample_blocks(n);
+        sw.npb = kvr::small_policy_blocks((int64_t)g->n_t1 * g->n_t2);
+        if ((rc = stage_tables(d_ws, bp.off_t1, bp.off_t2, bp.off_a2, bp.Lpad, *p, *g, s, tb, sw.ctr,
+                               sp.nctr)) != KVR_OK)
             return rc;
-        int32_t *lb = at<int32_t>(d_ws, sp.off_lb);
-        double *xgp = at<double>(d_ws, sp.off_xgp), *part = at<double>(d_ws, sp.off_part);
-        KVR_TRY(kvr::launch_small_prep(d_wait_s, d_ctx_tokens, n, tb, bp.r3_bins, hist, lb, xgp,
-                                       status, s));
         SampleSrc src{d_wait_s, d_ctx_tokens, nullptr, n, n};
-        kvr::R3Ws none{};
         KVR_MARK(g_prof_begin, s);
-        KVR_TRY(kvr::launch_grid(src, tb, pr, bp.gp, nullptr, nullptr, none, nullptr, nullptr, part,
-                                 status, s));
+        KVR_TRY(kvr::launch_small(src, tb, pr, bp.gp, sw, d_cost, status, s));
         KVR_MARK(g_prof_end, s);
-        KVR_TRY(kvr::launch_small_finalize(bp.gp, tb, pr, n, bp.r3_bins, hist, lb, xgp, part, d_cost,
-                                           s));
         return KVR_OK;
     }
     if (method == KVR_BRUTE) {

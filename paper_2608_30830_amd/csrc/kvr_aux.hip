@@ -43,16 +43,19 @@ hipError_t launch_export_status(const int *status, int32_t *out, hipStream_t str
     return hipGetLastError();
 }
 
-// Clears the status word and stores up to three host tables in one launch
-// when they fit one payload together.
+// Clears the status word and a range of counters, and stores up to three host
+// tables in one launch when they fit one payload together.
 struct StagePlan {
     double *dst[3];
     int cnt[3];
+    unsigned *zero;
+    int nzero;
 };
 
 __global__ void stage_kernel(int *status, StagePlan sp, UploadPayload p)
 {
     if (threadIdx.x == 0) status[0] = 0;
+    for (int i = threadIdx.x; i < sp.nzero; i += blockDim.x) sp.zero[i] = 0u;
     int off = 0;
     for (int t = 0; t < 3; ++t) {
         for (int i = threadIdx.x; i < sp.cnt[t]; i += blockDim.x) sp.dst[t][i] = p.v[off + i];
@@ -61,23 +64,24 @@ __global__ void stage_kernel(int *status, StagePlan sp, UploadPayload p)
 }
 
 hipError_t launch_stage(int *status, double *const dst[3], const double *const src[3],
-                        const int64_t cnt[3], hipStream_t stream)
+                        const int64_t cnt[3], unsigned *zero, int nzero, hipStream_t stream)
 {
-    if (cnt[0] + cnt[1] + cnt[2] <= kUploadMax) {
-        StagePlan sp;
-        UploadPayload p;
-        int off = 0;
-        for (int t = 0; t < 3; ++t) {
-            sp.dst[t] = dst[t];
-            sp.cnt[t] = (int)cnt[t];
-            for (int64_t i = 0; i < cnt[t]; ++i) p.v[off++] = src[t][i];
-        }
-        for (int i = off; i < kUploadMax; ++i) p.v[i] = 0.0;
-        hipLaunchKernelGGL(stage_kernel, dim3(1), dim3(256), 0, stream, status, sp, p);
-        return hipGetLastError();
+    const bool one = cnt[0] + cnt[1] + cnt[2] <= kUploadMax;
+    StagePlan sp;
+    UploadPayload p;
+    sp.zero = zero;
+    sp.nzero = zero != nullptr ? nzero : 0;
+    int off = 0;
+    for (int t = 0; t < 3; ++t) {   // the tables ride along when they fit, else follow
+        sp.dst[t] = dst[t];
+        sp.cnt[t] = one ? (int)cnt[t] : 0;
+        for (int64_t i = 0; i < sp.cnt[t]; ++i) p.v[off++] = src[t][i];
     }
-    hipError_t err = launch_clear_status(status, stream);
-    for (int t = 0; t < 3 && err == hipSuccess; ++t) err = launch_upload(dst[t], src[t], cnt[t], stream);
+    for (int i = off; i < kUploadMax; ++i) p.v[i] = 0.0;
+    hipLaunchKernelGGL(stage_kernel, dim3(1), dim3(256), 0, stream, status, sp, p);
+    hipError_t err = hipGetLastError();
+    for (int t = 0; t < 3 && !one && err == hipSuccess; ++t)
+        err = launch_upload(dst[t], src[t], cnt[t], stream);
     return err;
 }
 

@@ -42,13 +42,11 @@ namespace kvr {
 // Rounding note: min(fl(max(w,t1) - t1), fl(e - t1)) equals
 // fl(min(max(w,t1), e) - t1) because rounding is monotone.
 // Four resident waves per SIMD: the register budget is capped at 128 VGPRs
-// (the accumulators and loads of LT = 32 fit without spilling).
-// WPB > 1 (small samples, where a wave per split leaves most SIMDs idle): a
-// block holds WPB waves of one (group, tile), wave w taking split
-// sg * WPB + w, and adds the waves' accumulators in wave order in LDS before
-// writing one partial per block (split partials only).
-template <int LT, int MODE, int WPB>
-__global__ void __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_eu(4))) grid_kernel(SampleSrc src, Tables tb, PriceDev pr,
+// (the accumulators and loads of LT = 32 fit without spilling).  One wave per
+// block; small samples, where a wave per split leaves most SIMDs idle, take
+// the blocks of several waves of kvr_small.hip instead.
+template <int LT, int MODE>
+__global__ void __launch_bounds__(kWave) __attribute__((amdgpu_waves_per_eu(4))) grid_kernel(SampleSrc src, Tables tb, PriceDev pr,
                                                      GridPlan plan, const double *__restrict__ X,
                                                      const double *__restrict__ G, R3Ws r3s,
                                                      double *__restrict__ cost_out,
@@ -62,19 +60,14 @@ __global__ void __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_e
     constexpr int kPer = kCh / kWave;                  // samples each lane stages per stream
     // per-lane d: (w, T) of each sample; staged d: (T, d) of each sample for
     // combination A and for B, so a lane reads one 16-byte record per sample
-    __shared__ double2 wt_all[WPB][2][kStaged ? 1 : kCh];
-    __shared__ double2 td_all[WPB][2][kStaged ? kCh : 1][2];
-    const int wv = WPB > 1 ? (int)threadIdx.x / kWave : 0;
-    auto &wt = wt_all[wv];
-    auto &td = td_all[wv];
+    __shared__ double2 wt[2][kStaged ? 1 : kCh];
+    __shared__ double2 td[2][kStaged ? kCh : 1][2];
 
-    const int nsg = (plan.nsplit + WPB - 1) / WPB;   // split groups (one per block)
     const int64_t logical = xcd_logical_block(blockIdx.x, nlogical);
     const int tile = (int)(logical % plan.ntiles);
     int64_t rest = logical / plan.ntiles;
-    const int sg = (int)(rest % nsg);
-    const int64_t grp = rest / nsg;
-    const int split = sg * WPB + wv;
+    const int split = (int)(rest % plan.nsplit);
+    const int64_t grp = rest / plan.nsplit;
 
     const int lane = (int)threadIdx.x % kWave;
     const int64_t P = (int64_t)tb.K1 * tb.K2;
@@ -118,13 +111,10 @@ __global__ void __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_e
         acc[l] = 0.0;
     }
 
-    int64_t j0 = (int64_t)split * plan.split_len;     // a block's last waves may have no samples
-    if (j0 > src.m) j0 = src.m;
+    const int64_t j0 = (int64_t)split * plan.split_len;
     int64_t j1 = j0 + plan.split_len;
     if (j1 > src.m) j1 = src.m;
-    // with several waves per block every wave takes the same number of chunks
-    // (the block's barriers), padding the short ones with zeros
-    const int64_t nch = WPB > 1 ? (plan.split_len + kCh - 1) / kCh : (j1 - j0 + kCh - 1) / kCh;
+    const int64_t nch = (j1 - j0 + kCh - 1) / kCh;
     const int64_t offA = (kStaged ? rA : r) * src.m;   // index-row offsets of the streams
     const int64_t offB = rB * src.m;
 
@@ -185,27 +175,6 @@ __global__ void __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_e
         __syncthreads();
     }
 
-    if (WPB > 1) {   // the block's splits in wave order, then one partial
-        __shared__ double red[LT][kWave];
-        for (int w = 1; w < WPB; ++w) {
-            if (wv == w) {
-#pragma unroll
-                for (int l = 0; l < LT; ++l) red[l][lane] = acc[l];
-            }
-            __syncthreads();
-            if (wv == 0) {
-#pragma unroll
-                for (int l = 0; l < LT; ++l) acc[l] += red[l][lane];
-            }
-            __syncthreads();
-        }
-        if (wv == 0 && valid) {
-            const int64_t base_row = (((int64_t)sg * plan.R + r) * plan.ntiles + tile) * LT;
-#pragma unroll
-            for (int l = 0; l < LT; ++l) partials[(base_row + l) * P + f] = acc[l];
-        }
-        return;
-    }
     if (partials == nullptr) {   // one split: the costs are finished here
         const double md = (double)src.m;
         const double x = valid ? X[r * tb.K1 + a] : 0.0;
@@ -244,17 +213,15 @@ __global__ void __launch_bounds__(kWave * WPB) __attribute__((amdgpu_waves_per_e
     }
 }
 
-template <int LT, int MODE, int WPB>
+template <int LT, int MODE>
 static hipError_t launch_grid_m(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
                                 const GridPlan &plan, const double *X, const double *G,
                                 const R3Ws &r3, double *cost_out, ArgminCand *cand,
                                 double *partials, int *status, hipStream_t stream)
 {
-    const int64_t nsg = (plan.nsplit + WPB - 1) / WPB;
-    const int64_t nlogical = plan.ngroups * nsg * plan.ntiles;
-    hipLaunchKernelGGL((grid_kernel<LT, MODE, WPB>), dim3((unsigned)nlogical), dim3(kWave * WPB),
-                       0, stream, src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status,
-                       nlogical);
+    const int64_t nlogical = plan.ngroups * plan.nsplit * plan.ntiles;
+    hipLaunchKernelGGL((grid_kernel<LT, MODE>), dim3((unsigned)nlogical), dim3(kWave), 0, stream,
+                       src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, nlogical);
     return hipGetLastError();
 }
 
@@ -264,24 +231,14 @@ static hipError_t launch_grid_t(const SampleSrc &src, const Tables &tb, const Pr
                                 const R3Ws &r3, double *cost_out, ArgminCand *cand,
                                 double *partials, int *status, hipStream_t stream)
 {
-    if (plan.wpb == kSmallWaves) {   // one resample: never two sample streams
-        if (partials == nullptr) return hipErrorInvalidValue;
-        switch (plan.mode) {
-        case kModePerLane:
-            return launch_grid_m<LT, kModePerLane, kSmallWaves>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
-        case kModeRows1:
-            return launch_grid_m<LT, kModeRows1, kSmallWaves>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
-        default: return hipErrorInvalidValue;
-        }
-    }
     if (plan.wpb != 1) return hipErrorInvalidValue;
     switch (plan.mode) {
     case kModePerLane:
-        return launch_grid_m<LT, kModePerLane, 1>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModePerLane>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     case kModeRows1:
-        return launch_grid_m<LT, kModeRows1, 1>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModeRows1>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     case kModeRows2:
-        return launch_grid_m<LT, kModeRows2, 1>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
+        return launch_grid_m<LT, kModeRows2>(src, tb, pr, plan, X, G, r3, cost_out, cand, partials, status, stream);
     default: return hipErrorInvalidValue;
     }
 }

@@ -11,7 +11,9 @@ namespace kvr {
 constexpr int kWave = 64;          // CDNA wavefront width
 constexpr int kChunk = 128;        // samples staged in LDS per buffer (grid kernel)
 constexpr int kStatusDomain = 1;   // value of the workspace status word on a domain error
-constexpr int kSmallWaves = 8;     // waves per grid block on the small-sample path
+constexpr int kSmallWaves = 8;     // waves per block of the small-sample kernel
+constexpr int kSmallMaxGroupTiles = 4096;   // (group, load tile)s of one small-sample launch
+constexpr int kSmallBatchGroups = 8;        // split groups per batch in that launch
 
 // Where a call's samples come from: the base arrays, optionally through
 // bootstrap index rows idx[R][m].
@@ -45,8 +47,8 @@ struct GridPlan {
     int ntiles;          // ceil(L / LT)
     int nblk;            // groups per resample, kModePerLane: ceil(K1*K2 / 64)
     int nsplit;          // sample splits per resample
-    int wpb;             // waves per block (1, or kSmallWaves: consecutive splits
-                         // of one group, added in LDS before one partial is written)
+    int wpb;             // splits per block: 1 (grid_kernel), or kSmallWaves (the
+                         // small-sample kernel adds a block's splits in LDS)
     int mode;            // kModePerLane, kModeRows1 or kModeRows2
     int64_t ngroups;     // 64-lane groups: R*nblk (per lane) or ceil(R*K1*K2 / 64)
     int64_t split_len;   // samples per split (multiple of kChunk)
@@ -96,8 +98,9 @@ hipError_t launch_clear_status(int *status, hipStream_t stream);
 // out[0] = KVR_OK or KVR_E_DOMAIN from a workspace status word.
 hipError_t launch_export_status(const int *status, int32_t *out, hipStream_t stream);
 hipError_t launch_upload(double *dst, const double *host_src, int64_t count, hipStream_t stream);
+// Clears the status word and zero[0..nzero), and stores three host tables.
 hipError_t launch_stage(int *status, double *const dst[3], const double *const src[3],
-                        const int64_t cnt[3], hipStream_t stream);
+                        const int64_t cnt[3], unsigned *zero, int nzero, hipStream_t stream);
 
 // X and G per (resample, t1); with few resamples the samples are cut into
 // parts (partials in xgp[parts][R][K1][2], summed in part order).
@@ -149,18 +152,26 @@ hipError_t launch_controller_final(const int64_t *restored, const int64_t *admit
                                    double t2, double t_star, double b2, double b3,
                                    kvr_controller_out *out, hipStream_t stream);
 
-// Brute-force grid of one sample with few t1 timers and deadlines in four
-// launches (kvr_small.hip): stage, pre-pass, grid kernel with split partials,
-// finalize.
+// Brute-force grid of one sample with few t1 timers and deadlines in one
+// launch after the table staging (kvr_small.hip).  Workspace of that launch:
+struct SmallWs {
+    unsigned long long *hist;   // [nsb][nbins] pre-pass blocks' recompute histograms
+    int32_t *lb;                // [K1*K2] grid deadlines strictly below each policy's
+    double *xgp;                // [nsb][K1][2] pre-pass blocks' X and G
+    unsigned long long *S;      // [nbins] suffix sums of the histogram
+    double *XG;                 // [K1][2] X and G of the sample
+    double *partials;           // [ceil(nsplit / kSmallWaves)][ntiles][LT][K1*K2]
+    unsigned *ctr;              // arrival counters, zero at launch: the pre-pass, each
+                                // (group, tile), each batch of a (group, tile)'s split groups
+    int64_t nbins;              // F, the number of finite grid deadlines
+    int nsb, npb;               // pre-pass sample blocks and policy blocks
+};
 bool small_path_fits(int K1, int K2, int64_t nbins, int64_t n);
 int small_sample_blocks(int64_t n);
-hipError_t launch_small_prep(const double *w, const int32_t *T, int64_t n, const Tables &tb,
-                             int64_t nbins, unsigned long long *hist, int32_t *lb, double *xgp,
-                             int *status, hipStream_t stream);
-hipError_t launch_small_finalize(const GridPlan &plan, const Tables &tb, const PriceDev &pr,
-                                 int64_t m, int64_t nbins, const unsigned long long *hist,
-                                 const int32_t *lb, const double *xgp, const double *partials,
-                                 double *cost_out, hipStream_t stream);
+int small_policy_blocks(int64_t P);
+hipError_t launch_small(const SampleSrc &src, const Tables &tb, const PriceDev &pr,
+                        const GridPlan &plan, const SmallWs &ws, double *cost_out, int *status,
+                        hipStream_t stream);
 
 // Sorted path.
 struct SortWs {

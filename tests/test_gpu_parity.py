@@ -91,7 +91,7 @@ RANDOM_CASES = [  # seed, n, K1, K2, L, ties  (ragged n, K2 below/at/above one w
     (107, 2500, 4, 70, 9, True),
     (108, 300, 5, 2, 4, True),
     # eight t1 rows and ~4,000 finite deadlines over 16 pre-pass blocks: the
-    # largest grid of the four-launch path for one sample
+    # largest grid of the two-launch path for one sample
     (109, 16000, 8, 500, 5, True),
 ]
 
@@ -302,7 +302,7 @@ def test_identity_rows_equal_cost_grid(kvr, k1):
     """A bootstrap row drawing every sample once in order is the plain grid:
     bit for bit where both calls run the same kernels in the same order (nine
     GPU-tier timers), within 1e-12 where the plain grid of one small sample
-    adds its splits in blocks (two timers, the four-launch path)."""
+    adds its splits in blocks (two timers, the two-launch path)."""
     wl = workloads.random_case(301, 5000, k1, 66, 6)
     g = kvr.PolicyGrid(wl.t1, wl.t2, wl.lam)
     idx = np.tile(np.arange(wl.n, dtype=np.int32), (3, 1))
