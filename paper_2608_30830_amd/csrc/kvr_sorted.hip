@@ -29,7 +29,6 @@ namespace kvr {
 constexpr int kSortThreads = 256;
 constexpr int kSortKPT = 8;                                   // keys per thread
 constexpr int kSortTile = kSortThreads * kSortKPT;            // 2048 keys per tile
-constexpr int kWaveKeys = kWave * kSortKPT;                   // 512 keys per wave
 constexpr int kScanThreads = 256;
 constexpr int kScanIPT = 8;
 constexpr int kScanTile = kScanThreads * kScanIPT;
@@ -400,20 +399,30 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
 // in sort_scatter_kernel with the tile as the whole array (a stable counting
 // sort per digit); then the sorted keys and payload are stored, and, with
 // Nsum, the inclusive prefix arrays of T and T*w in a fixed order (each thread
-// its kSortKPT consecutive positions, the thread totals across the block).
-__global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
+// its kOneKPT consecutive positions, the thread totals across the block).
+// Sixteen waves of two keys per lane: each wave's ranking is a chain of two
+// dependent LDS updates per pass instead of eight, and the sixteen chains
+// overlap (four waves of eight keys took 29 us for 1,000 keys on MI355X).
+constexpr int kOneThreads = 1024;
+constexpr int kOneKPT = kSortTile / kOneThreads;   // keys per thread
+constexpr int kOneWaves = kOneThreads / kWave;
+constexpr int kOneWaveKeys = kWave * kOneKPT;      // consecutive keys of one wave
+
+__global__ void __launch_bounds__(kOneThreads) sort_small_kernel(
     const double *__restrict__ w, const int32_t *__restrict__ T, int64_t n,
     uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, int64_t *__restrict__ Nsum,
     double *__restrict__ Ssum, int32_t *__restrict__ perm_out, int *status)
 {
     __shared__ uint64_t lk[2][kSortTile];
     __shared__ int32_t lv[2][kSortTile];
-    __shared__ uint32_t wcnt[4][256];
-    __shared__ uint32_t wofs[4][256];
-    __shared__ uint32_t dbase[256];
+    // per-wave digit counts, then their wave prefixes; two sets, so that the
+    // next pass's set is cleared while this pass uses the other
+    __shared__ uint16_t wcnt[2][kOneWaves][256];
+    __shared__ uint32_t lexcl[256];             // digit's start within its group of 64 digits
+    __shared__ uint32_t dsum[256 / kWave];       // keys in each group of 64 digits
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
     const int nn = (int)n;   // at most kSortTile
-    for (int i = threadIdx.x; i < nn; i += kSortThreads) {
+    for (int i = threadIdx.x; i < nn; i += kOneThreads) {
         uint64_t b = (uint64_t)__double_as_longlong(w[i]);
         if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
         if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
@@ -424,49 +433,61 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
         lk[0][i] = b;
         lv[0][i] = i;
     }
+    for (int q = threadIdx.x; q < kOneWaves * 256; q += kOneThreads) (&wcnt[0][0][0])[q] = 0;
+    __syncthreads();
     int cur = 0;
     for (int pass = 0; pass < 8; ++pass) {
-        const int shift = 8 * pass;
+        const int shift = 8 * pass, wb = pass & 1;
+        // the other set was last read before the previous pass's final barrier
+        for (int q = threadIdx.x; q < kOneWaves * 256; q += kOneThreads) (&wcnt[wb ^ 1][0][0])[q] = 0;
+        uint64_t key[kOneKPT];
+        int32_t val[kOneKPT];
+        uint32_t local[kOneKPT];
 #pragma unroll
-        for (int q = 0; q < 4; ++q) wcnt[q][threadIdx.x] = 0;
-        __syncthreads();
-        uint64_t key[kSortKPT];
-        int32_t val[kSortKPT];
-        uint32_t local[kSortKPT];
-#pragma unroll
-        for (int j = 0; j < kSortKPT; ++j) {
-            const int i = wave * kWaveKeys + j * kWave + lane;
+        for (int j = 0; j < kOneKPT; ++j) {
+            const int i = wave * kOneWaveKeys + j * kWave + lane;
             const bool valid = i < nn;
             key[j] = valid ? lk[cur][i] : 0;
             val[j] = valid ? lv[cur][i] : 0;
             const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
             const uint64_t peers = digit_peers(d, valid);
             const uint32_t rank = lanes_below(peers);
-            const uint32_t before = wcnt[wave][d];
+            const uint32_t before = wcnt[wb][wave][d];
             local[j] = before + rank;
             __builtin_amdgcn_wave_barrier();
-            if (valid && rank == 0) wcnt[wave][d] = before + (uint32_t)__popcll(peers);
+            if (valid && rank == 0) wcnt[wb][wave][d] = (uint16_t)(before + (uint32_t)__popcll(peers));
             __builtin_amdgcn_wave_barrier();
         }
         __syncthreads();
-        {
+        // digit d (threads below 256): the waves' counts in wave order become
+        // each wave's offset within the digit; the digit totals are scanned
+        // within each group of 64 digits (one wave), the groups' totals kept
+        if ((int)threadIdx.x < 256) {
             const int d = threadIdx.x;
-            uint32_t run = 0;
+            uint32_t c[kOneWaves], tot = 0;
 #pragma unroll
-            for (int q = 0; q < 4; ++q) {
-                wofs[q][d] = run;
-                run += wcnt[q][d];
+            for (int q = 0; q < kOneWaves; ++q) c[q] = wcnt[wb][q][d];   // all loads in flight
+#pragma unroll
+            for (int q = 0; q < kOneWaves; ++q) {
+                wcnt[wb][q][d] = (uint16_t)tot;
+                tot += c[q];
             }
-            uint32_t all;
-            dbase[d] = block_exclusive_scan(run, &all);   // run = the count of digit d
+            uint32_t incl = tot;
+            for (int off = 1; off < kWave; off <<= 1) {
+                const uint32_t y = __shfl_up(incl, off, kWave);
+                if (lane >= off) incl += y;
+            }
+            lexcl[d] = incl - tot;
+            if (lane == kWave - 1) dsum[wave] = incl;
         }
         __syncthreads();
 #pragma unroll
-        for (int j = 0; j < kSortKPT; ++j) {
-            const int i = wave * kWaveKeys + j * kWave + lane;
+        for (int j = 0; j < kOneKPT; ++j) {
+            const int i = wave * kOneWaveKeys + j * kWave + lane;
             if (i < nn) {
                 const uint32_t d = (uint32_t)(key[j] >> shift) & 255u;
-                const uint32_t pos = dbase[d] + wofs[wave][d] + local[j];
+                uint32_t pos = lexcl[d] + wcnt[wb][wave][d] + local[j];
+                for (uint32_t g = 0; g < d / kWave; ++g) pos += dsum[g];
                 if (pos < (uint32_t)nn) {                 // always true; never write outside
                     lk[cur ^ 1][pos] = key[j];
                     lv[cur ^ 1][pos] = val[j];
@@ -476,18 +497,18 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
         __syncthreads();
         cur ^= 1;
     }
-    for (int i = threadIdx.x; i < nn; i += kSortThreads) {
+    for (int i = threadIdx.x; i < nn; i += kOneThreads) {
         keys_out[i] = lk[cur][i];
         vals_out[i] = lv[cur][i];
     }
     if (Nsum == nullptr) return;   // uniform: the sort alone
-    const int k0 = (int)threadIdx.x * kSortKPT;
-    int64_t tn[kSortKPT];
-    double ts[kSortKPT];
+    const int k0 = (int)threadIdx.x * kOneKPT;
+    int64_t tn[kOneKPT];
+    double ts[kOneKPT];
     int64_t sn = 0;
     double ss = 0.0;
 #pragma unroll
-    for (int q = 0; q < kSortKPT; ++q) {
+    for (int q = 0; q < kOneKPT; ++q) {
         const int k = k0 + q;
         if (k < nn) {
             const int32_t pj = lv[cur][k];
@@ -516,8 +537,8 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
         en = 0;
         es = 0.0;
     }
-    __shared__ int64_t wn[kSortThreads / kWave];
-    __shared__ double wsm[kSortThreads / kWave];
+    __shared__ int64_t wn[kOneWaves];
+    __shared__ double wsm[kOneWaves];
     if (lane == kWave - 1) {
         wn[wave] = xn;
         wsm[wave] = xs;
@@ -532,7 +553,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_small_kernel(
     pn += en;
     ps += es;
 #pragma unroll
-    for (int q = 0; q < kSortKPT; ++q) {
+    for (int q = 0; q < kOneKPT; ++q) {
         const int k = k0 + q;
         if (k < nn) {
             Nsum[k] = pn + tn[q];
@@ -999,7 +1020,7 @@ hipError_t launch_sort_keys(const double *w, const int32_t *T, int64_t n, SortWs
 {
     *cur_out = 0;
     if (n <= kSortTile) {   // one block
-        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
+        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kOneThreads), 0, stream, w, T, n,
                            ws.keys[0], ws.vals[0], nullptr, nullptr, nullptr, status);
         return hipGetLastError();
     }
@@ -1011,7 +1032,7 @@ hipError_t launch_sorted_path(const double *w, const int32_t *T, int64_t n, cons
                               int32_t *perm_out, int *status, hipStream_t stream)
 {
     if (n <= kSortTile) {   // sort and prefix arrays in one block
-        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kSortThreads), 0, stream, w, T, n,
+        hipLaunchKernelGGL(sort_small_kernel, dim3(1), dim3(kOneThreads), 0, stream, w, T, n,
                            ws.keys[0], ws.vals[0], ws.Nsum, ws.Ssum, perm_out, status);
         const hipError_t err = hipGetLastError();
         if (err != hipSuccess) return err;
