@@ -588,8 +588,7 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     const size_t off_u1 = take(sizeof(int32_t) * g->n_t1);
     const size_t off_ue = take(sizeof(int32_t) * P);
     const size_t off_qslot = take(sizeof(int32_t) * (n + 1));
-    const size_t off_TN = take(sizeof(uint64_t) * Rb * nqs);
-    const size_t off_TS = take(sizeof(double) * Rb * nqs);
+    const size_t off_TQ = take(sizeof(double) * 2 * Rb * nqs);
     const size_t off_tot = take(sizeof(uint64_t) * Rb);
     const size_t need = off;
     if (d_ws == nullptr) {
@@ -613,8 +612,7 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     fw.ue = at<int32_t>(d_ws, off_ue);
     fw.qslot = at<int32_t>(d_ws, off_qslot);
     fw.nqs = nqs;
-    fw.TN = at<unsigned long long>(d_ws, off_TN);
-    fw.TS = at<double>(d_ws, off_TS);
+    fw.TQ = at<double2>(d_ws, off_TQ);
     fw.tot = at<unsigned long long>(d_ws, off_tot);
     fw.Rb = Rb;
     SampleSrc src{d_wait_s, d_ctx_tokens, d_idx, n, m};

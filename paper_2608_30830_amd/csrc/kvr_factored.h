@@ -15,8 +15,8 @@ struct FactoredWs {
     int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2, then its query slot
     int32_t *qslot;           // [n+1] query slot of each sorted position, -1 if none
     int64_t nqs;              // query slots per row (an upper bound on the distinct positions)
-    unsigned long long *TN;   // [Rb][nqs] N at each query slot: prefix of mult x T
-    double *TS;               // [Rb][nqs] S at each query slot: prefix of mult x T x w
+    double2 *TQ;              // [Rb][nqs] (N, S) at each query slot: prefixes of mult x T
+                              // (N, rounded to double as the closed form uses it) and of mult x T x w
     unsigned long long *tot;  // [Rb] N over every position
     int64_t Rb;               // resamples per batch
 };

@@ -36,7 +36,7 @@ constexpr int kFLdsWords = 8192;        // 32 KiB of LDS counters per block
 constexpr int kFBits = 4;               // bits of a narrow multiplicity counter
 constexpr int kFPerWord = 32 / kFBits;  // narrow counters per LDS word
 constexpr uint32_t kFMask = (1u << kFBits) - 1u;
-constexpr int kFScanPer = 4;            // consecutive positions per thread in the scan
+constexpr int kFScanPer = 8;            // consecutive positions per thread in the scan
 constexpr int kFUnroll = 4;             // draws per thread and step, fetched together
 constexpr int kFLoads = 32;             // loads per policy-kernel block (16 when L <= 16)
 constexpr int kFPolThreads = 256;
@@ -44,6 +44,47 @@ constexpr int kFPolThreads = 256;
 // policies' dependent gathers more in flight, at the same three waves per
 // SIMD), 2 with 16-load tiles (where 4 would cost a wave).
 template <int FL> constexpr int kFPU = FL == 16 ? 2 : 4;
+
+// DPP moves of a 64-bit value as two 32-bit halves; a lane the control gives
+// no source (or masks off) reads 0.
+template <int CTRL, int ROWM>
+__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long v)
+{
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROWM, 0xf, true);
+    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROWM, 0xf, true);
+    return ((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo;
+}
+template <int CTRL, int ROWM>
+__device__ __forceinline__ double dpp_f64(double v)
+{
+    return __longlong_as_double((long long)dpp_u64<CTRL, ROWM>((unsigned long long)__double_as_longlong(v)));
+}
+
+// Inclusive scan of (n, s) over the 64 lanes of a wave with DPP moves (VALU
+// operations, no LDS round trip): within each row of 16 lanes the values 1,
+// 2, 4 and 8 lanes back are added (row_shr), then lane 15's sum into the
+// next row (row_bcast:15, rows 1 and 3) and lane 31's into rows 2 and 3
+// (row_bcast:31).  The additions follow a fixed tree, so equal inputs give
+// equal sums.  en, es: the exclusive values (the inclusive ones one lane back,
+// wave_shr:1, 0 in lane 0).
+__device__ __forceinline__ void wave_scan_dpp(unsigned long long &n, double &s,
+                                              unsigned long long &en, double &es)
+{
+    n += dpp_u64<0x111, 0xf>(n);
+    s += dpp_f64<0x111, 0xf>(s);
+    n += dpp_u64<0x112, 0xf>(n);
+    s += dpp_f64<0x112, 0xf>(s);
+    n += dpp_u64<0x114, 0xf>(n);
+    s += dpp_f64<0x114, 0xf>(s);
+    n += dpp_u64<0x118, 0xf>(n);
+    s += dpp_f64<0x118, 0xf>(s);
+    n += dpp_u64<0x142, 0xa>(n);
+    s += dpp_f64<0x142, 0xa>(s);
+    n += dpp_u64<0x143, 0xc>(n);
+    s += dpp_f64<0x143, 0xc>(s);
+    en = dpp_u64<0x138, 0xf>(n);
+    es = dpp_f64<0x138, 0xf>(s);
+}
 
 // Per sorted position k: the sorted wait and the context size there (below
 // 1 counts as 1; sort_prep_kernel has flagged it); per base sample: its
@@ -176,11 +217,14 @@ __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict
 // One block per resample of the batch.  Per pass over a range of sorted
 // positions: the number of the resample's draws of each position, counted in
 // LDS, then a scan over the range in a fixed order (each thread its
-// kFScanPer consecutive positions, the thread totals across the block: waves
-// in order, lanes of a wave in order, then the earlier passes), which records
-// at every query position k N(k) = sum_{j < k} c_j T_j (exact) and S(k) =
-// sum_{j < k} c_j T_j w_j (reproducible) in the query row.  Position n (every
-// wait) closes the row; tot[rb] = N(n).
+// kFScanPer consecutive positions, the thread totals across the block: the
+// lanes of a wave in wave_scan_dpp's tree, the waves in order, then the
+// earlier passes), which records
+// at every query position k N(k) = sum_{j < k} c_j T_j (exact, then rounded
+// to double as the closed form uses it) and S(k) = sum_{j < k} c_j T_j w_j
+// (reproducible) in the query row, one 16-byte record per slot so that a
+// policy's two lookups are two loads.  Position n (every wait) closes the
+// row; tot[rb] = N(n).
 //
 // Counters: kFBits-bit fields of 32-bit LDS words, kFLdsWords * kFPerWord
 // positions per pass (32 KiB, so that four blocks share a CU and one's
@@ -198,8 +242,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     const int32_t *__restrict__ rank, const int32_t *__restrict__ perm,
     const int32_t *__restrict__ Ts,
     const double *__restrict__ sw, const int32_t *__restrict__ qslot, int64_t nqs,
-    unsigned long long *__restrict__ TN, double *__restrict__ TS,
-    unsigned long long *__restrict__ tot, int *status)
+    double2 *__restrict__ TQ, unsigned long long *__restrict__ tot, int *status)
 {
     constexpr int nw = kFPThreads / kWave;
     constexpr int kTile = kFPThreads * kFScanPer;
@@ -209,8 +252,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     __shared__ long long wchk[nw];
     const int64_t rb = blockIdx.x;
     const int64_t r = r0 + rb;
-    unsigned long long *nrow = TN + rb * nqs;
-    double *srow = TS + rb * nqs;
+    double2 *qrow = TQ + rb * nqs;
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
     const int64_t B = blockDim.x;
     unsigned long long carry_n = 0ull;   // totals of the earlier positions (same in every thread)
@@ -290,23 +332,27 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                 int32_t qs[kFScanPer];
                 unsigned long long tn = 0ull;
                 double ts = 0.0;
-                // a full run of kFScanPer positions starts on a multiple of 4
-                // (pass starts are multiples of 2^14): one 16-byte load each
-                // of Ts and qslot and two of sw instead of an element each
+                // a full run of kFScanPer positions starts on a multiple of
+                // kFScanPer (pass starts are multiples of 2^14): 16-byte loads
+                // of Ts, qslot and perm (4 positions) and of sw (2) instead of
+                // an element each
                 int32_t tv[kFScanPer], qv[kFScanPer], pv[kFScanPer];
                 double wv4[kFScanPer];
                 if (kl + kFScanPer <= nk) {
-                    static_assert(kFScanPer == 4, "the vector loads below read 4 positions");
-                    const int4 t4 = *reinterpret_cast<const int4 *>(Ts + k0 + kl);
-                    const int4 q4 = *reinterpret_cast<const int4 *>(qslot + k0 + kl);
-                    const double2 w0 = reinterpret_cast<const double2 *>(sw + k0 + kl)[0];
-                    const double2 w1 = reinterpret_cast<const double2 *>(sw + k0 + kl)[1];
-                    tv[0] = t4.x; tv[1] = t4.y; tv[2] = t4.z; tv[3] = t4.w;
-                    qv[0] = q4.x; qv[1] = q4.y; qv[2] = q4.z; qv[3] = q4.w;
-                    wv4[0] = w0.x; wv4[1] = w0.y; wv4[2] = w1.x; wv4[3] = w1.y;
-                    if (byidx) {
-                        const int4 p4 = *reinterpret_cast<const int4 *>(perm + k0 + kl);
-                        pv[0] = p4.x; pv[1] = p4.y; pv[2] = p4.z; pv[3] = p4.w;
+                    static_assert(kFScanPer % 4 == 0, "the vector loads below read 4 positions");
+#pragma unroll
+                    for (int h = 0; h < kFScanPer; h += 4) {
+                        const int4 t4 = *reinterpret_cast<const int4 *>(Ts + k0 + kl + h);
+                        const int4 q4 = *reinterpret_cast<const int4 *>(qslot + k0 + kl + h);
+                        const double2 w0 = reinterpret_cast<const double2 *>(sw + k0 + kl + h)[0];
+                        const double2 w1 = reinterpret_cast<const double2 *>(sw + k0 + kl + h)[1];
+                        tv[h] = t4.x; tv[h + 1] = t4.y; tv[h + 2] = t4.z; tv[h + 3] = t4.w;
+                        qv[h] = q4.x; qv[h + 1] = q4.y; qv[h + 2] = q4.z; qv[h + 3] = q4.w;
+                        wv4[h] = w0.x; wv4[h + 1] = w0.y; wv4[h + 2] = w1.x; wv4[h + 3] = w1.y;
+                        if (byidx) {
+                            const int4 p4 = *reinterpret_cast<const int4 *>(perm + k0 + kl + h);
+                            pv[h] = p4.x; pv[h + 1] = p4.y; pv[h + 2] = p4.z; pv[h + 3] = p4.w;
+                        }
                     }
                 } else {
 #pragma unroll
@@ -334,22 +380,9 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                     tn += cwq;
                     ts += sv[q];
                 }
-                unsigned long long xn = tn;            // inclusive scan of the thread totals
-                double xs = ts;
-                for (int off = 1; off < kWave; off <<= 1) {
-                    const unsigned long long on = __shfl_up(xn, off, kWave);
-                    const double os = __shfl_up(xs, off, kWave);
-                    if (lane >= off) {
-                        xn += on;
-                        xs += os;
-                    }
-                }
-                unsigned long long en = __shfl_up(xn, 1, kWave);   // exclusive within the wave
-                double es = __shfl_up(xs, 1, kWave);
-                if (lane == 0) {
-                    en = 0ull;
-                    es = 0.0;
-                }
+                unsigned long long xn = tn, en;        // scan of the thread totals in the wave
+                double xs = ts, es;
+                wave_scan_dpp(xn, xs, en, es);
                 if (lane == kWave - 1) {
                     wn[wv] = xn;
                     wsd[wv] = xs;
@@ -369,10 +402,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                 }
 #pragma unroll
                 for (int q = 0; q < kFScanPer; ++q) {
-                    if (qs[q] >= 0 && qs[q] < nqs) {
-                        nrow[qs[q]] = pn;
-                        srow[qs[q]] = ps;
-                    }
+                    if (qs[q] >= 0 && qs[q] < nqs) qrow[qs[q]] = make_double2((double)pn, ps);
                     pn += cw[q];
                     ps += sv[q];
                 }
@@ -383,10 +413,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     }
     if (threadIdx.x == 0) {
         const int32_t q = qslot[n];
-        if (q >= 0 && q < nqs) {
-            nrow[q] = carry_n;
-            srow[q] = carry_s;
-        }
+        if (q >= 0 && q < nqs) qrow[q] = make_double2((double)carry_n, carry_s);
         tot[rb] = carry_n;
     }
 }
@@ -398,7 +425,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
 // totals and only the selected one is divided.
 template <int FL>
 __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
-    const unsigned long long *__restrict__ TN, const double *__restrict__ TS, int64_t nqs,
+    const double2 *__restrict__ TQ, int64_t nqs,
     const unsigned long long *__restrict__ totN, int64_t m, int64_t r0, int ntl, Tables tb,
     PriceDev pr, const int32_t *__restrict__ u1, const int32_t *__restrict__ ue,
     int32_t *__restrict__ best, double *__restrict__ best_cost, double *__restrict__ cost_out)
@@ -409,8 +436,7 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
     const int64_t rb = blockIdx.x / ntl;
     const int tile = (int)(blockIdx.x % ntl);
     const int64_t r = r0 + rb;
-    const unsigned long long *nrow = TN + rb * nqs;   // N and S at the query slots
-    const double *srow = TS + rb * nqs;
+    const double2 *qrow = TQ + rb * nqs;   // (N, S) at the query slots
     const int64_t P = (int64_t)tb.K1 * tb.K2;
     const int l0 = tile * FL;
     const int nl = (tb.L - l0 < FL) ? tb.L - l0 : FL;
@@ -442,11 +468,12 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
         }
         double n1[kFPU<FL>], ne[kFPU<FL>], s1[kFPU<FL>], se[kFPU<FL>];
 #pragma unroll
-        for (int u = 0; u < kFPU<FL>; ++u) {
-            n1[u] = (double)nrow[p1[u]];
-            ne[u] = (double)nrow[pe[u]];
-            s1[u] = srow[p1[u]];
-            se[u] = srow[pe[u]];
+        for (int u = 0; u < kFPU<FL>; ++u) {   // one 16-byte record per slot
+            const double2 q1 = qrow[p1[u]], qe = qrow[pe[u]];
+            n1[u] = q1.x;
+            s1[u] = q1.y;
+            ne[u] = qe.x;
+            se[u] = qe.y;
         }
 #pragma unroll
         for (int u = 0; u < kFPU<FL>; ++u) {
@@ -462,12 +489,13 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
             }
             // every load of the tile (a2 is zero-padded past L; those lanes are
             // never stored); a thread visits its policies in increasing f, so
-            // "not larger" keeps the larger index on a tie, as the total order asks
+            // "not larger" keeps the larger index on a tie, as the total order
+            // asks; the running minimum itself is a min (equal on a tie)
 #pragma unroll
             for (int l = 0; l < FL; ++l) {
                 const double tc = fixed + a2[l] * hold;
                 const bool take = tc <= bc[l];
-                bc[l] = take ? tc : bc[l];
+                bc[l] = fmin(bc[l], tc);
                 bf[l] = take ? (int32_t)f : bf[l];
             }
         }
@@ -540,14 +568,14 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
         hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFPThreads), 0, stream,
                            src.idx, n, m, r0, ws.rank, ws.sort.vals[cur], ws.Ts, ws.sw, ws.qslot,
-                           ws.nqs, ws.TN, ws.TS, ws.tot, status);
+                           ws.nqs, ws.TQ, ws.tot, status);
         if (FL == 16)
             hipLaunchKernelGGL(factored_policy_kernel<16>, dim3((unsigned)(rb * ntl)),
-                               dim3(kFPolThreads), 0, stream, ws.TN, ws.TS, ws.nqs, ws.tot, m, r0,
+                               dim3(kFPolThreads), 0, stream, ws.TQ, ws.nqs, ws.tot, m, r0,
                                ntl, tb, pr, ws.u1, ws.ue, best, best_cost, cost_out);
         else
             hipLaunchKernelGGL(factored_policy_kernel<kFLoads>, dim3((unsigned)(rb * ntl)),
-                               dim3(kFPolThreads), 0, stream, ws.TN, ws.TS, ws.nqs, ws.tot, m, r0,
+                               dim3(kFPolThreads), 0, stream, ws.TQ, ws.nqs, ws.tot, m, r0,
                                ntl, tb, pr, ws.u1, ws.ue, best, best_cost, cost_out);
         if ((err = hipGetLastError()) != hipSuccess) return err;
     }
