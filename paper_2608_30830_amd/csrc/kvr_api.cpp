@@ -588,6 +588,8 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     const size_t off_u1 = take(sizeof(int32_t) * g->n_t1);
     const size_t off_ue = take(sizeof(int32_t) * P);
     const size_t off_qslot = take(sizeof(int32_t) * (n + 1));
+    const size_t off_qbits = take(sizeof(uint32_t) * ((n + 32) / 32));
+    const size_t off_qbase = take(sizeof(int32_t) * ((n + 32) / 32));
     const size_t off_TQ = take(sizeof(double) * 2 * Rb * nqs);
     const size_t off_tot = take(sizeof(uint64_t) * Rb);
     const size_t need = off;
@@ -611,6 +613,8 @@ int kvr_bootstrap_factored(const double *d_wait_s, const int32_t *d_ctx_tokens, 
     fw.u1 = at<int32_t>(d_ws, off_u1);
     fw.ue = at<int32_t>(d_ws, off_ue);
     fw.qslot = at<int32_t>(d_ws, off_qslot);
+    fw.qbits = at<uint32_t>(d_ws, off_qbits);
+    fw.qbase = at<int32_t>(d_ws, off_qbase);
     fw.nqs = nqs;
     fw.TQ = at<double2>(d_ws, off_TQ);
     fw.tot = at<unsigned long long>(d_ws, off_tot);

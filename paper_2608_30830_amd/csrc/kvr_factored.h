@@ -14,6 +14,8 @@ struct FactoredWs {
     int32_t *u1;              // [K1] sorted waits <= t1, then that position's query slot
     int32_t *ue;              // [K1*K2] sorted waits <= t1 + t2, then its query slot
     int32_t *qslot;           // [n+1] query slot of each sorted position, -1 if none
+    uint32_t *qbits;          // [(n+32)/32] bit k: sorted position k is a query position
+    int32_t *qbase;           // [(n+32)/32] query positions below each word of qbits
     int64_t nqs;              // query slots per row (an upper bound on the distinct positions)
     double2 *TQ;              // [Rb][nqs] (N, S) at each query slot: prefixes of mult x T
                               // (N, rounded to double as the closed form uses it) and of mult x T x w

@@ -37,7 +37,7 @@ constexpr int kFBits = 4;               // bits of a narrow multiplicity counter
 constexpr int kFPerWord = 32 / kFBits;  // narrow counters per LDS word
 constexpr uint32_t kFMask = (1u << kFBits) - 1u;
 constexpr int kFScanPer = 8;            // consecutive positions per thread in the scan
-constexpr int kFUnroll = 4;             // draws per thread and step, fetched together
+constexpr int kFUnroll = 8;             // draws per thread and step, fetched together
 constexpr int kFLoads = 32;             // loads per policy-kernel block (16 when L <= 16)
 constexpr int kFPolThreads = 256;
 // Policies per thread and step in the policy kernel: 4 with 32-load tiles (two
@@ -134,84 +134,83 @@ __global__ void __launch_bounds__(256) factored_bounds_kernel(const double *__re
     }
 }
 
-__global__ void __launch_bounds__(256) factored_fill_kernel(int32_t *__restrict__ qslot,
-                                                            int64_t len)
+__global__ void __launch_bounds__(256) factored_fill_kernel(uint32_t *__restrict__ qbits,
+                                                            int64_t nwords)
 {
     const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (i < len) qslot[i] = -1;
+    if (i < nwords) qbits[i] = 0u;
 }
 
-// Marks every query position (several threads may store the same 0).
+// Marks every query position: bit k of the position bitmask.
 __global__ void __launch_bounds__(256) factored_mark_kernel(const int32_t *__restrict__ u1,
                                                             const int32_t *__restrict__ ue,
                                                             int32_t K1, int64_t P,
-                                                            int32_t *__restrict__ qslot)
+                                                            uint32_t *__restrict__ qbits)
 {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (g < K1) qslot[u1[g]] = 0;
-    else if (g - K1 < P) qslot[ue[g - K1]] = 0;
+    int64_t k = -1;
+    if (g < K1) k = u1[g];
+    else if (g - K1 < P) k = ue[g - K1];
+    if (k >= 0) atomicOr(&qbits[k >> 5], 1u << (k & 31));
 }
 
-// One block: numbers the marked positions 0, 1, ... in position order
-// (exclusive count of marks below), unmarked positions stay -1.  Each wave
-// takes one contiguous segment of the positions, read 64 consecutive
-// positions per lane step with eight steps' loads in flight: it counts its
-// marks, one scan across the waves gives each segment its first number, and
-// a second pass numbers the marks (ballot and lane prefix counts).
-__global__ void __launch_bounds__(kFThreads) factored_slot_kernel(int32_t *__restrict__ qslot,
-                                                                  int64_t len)
+// One block: qbase[w] = the marked positions in words 0 .. w-1 (an exclusive
+// scan of the words' bit counts; each thread a run of consecutive words, the
+// runs across the block in order).
+__global__ void __launch_bounds__(kFThreads) factored_slot_kernel(const uint32_t *__restrict__ qbits,
+                                                                  int32_t *__restrict__ qbase,
+                                                                  int64_t nwords)
 {
-    constexpr int nw = kFThreads / kWave, kIn = 8;
+    constexpr int nw = kFThreads / kWave;
     __shared__ int32_t wsum[nw];
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
-    const int64_t seg = (len + nw - 1) / nw;
-    const int64_t s0 = (int64_t)wv * seg;
-    const int64_t s1 = (s0 + seg < len) ? s0 + seg : len;
-    int32_t cnt = 0;   // this lane's marks (summed over the wave below)
-    for (int64_t b = s0; b < s1; b += kIn * kWave) {
-        int32_t v[kIn];
-#pragma unroll
-        for (int u = 0; u < kIn; ++u) {
-            const int64_t p = b + u * kWave + lane;
-            v[u] = p < s1 ? qslot[p] : -1;
-        }
-#pragma unroll
-        for (int u = 0; u < kIn; ++u) cnt += v[u] >= 0 ? 1 : 0;
+    const int64_t per = (nwords + kFThreads - 1) / kFThreads;
+    const int64_t w0 = (int64_t)threadIdx.x * per;
+    const int64_t w1 = (w0 + per < nwords) ? w0 + per : nwords;
+    int32_t cnt = 0;
+    for (int64_t w = w0; w < w1; ++w) cnt += __popc(qbits[w]);
+    int32_t x = cnt;   // inclusive scan of the run totals within the wave
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int32_t y = __shfl_up(x, off, kWave);
+        if (lane >= off) x += y;
     }
-    cnt = wave_sum(cnt);
-    if (lane == 0) wsum[wv] = cnt;
+    if (lane == kWave - 1) wsum[wv] = x;
     __syncthreads();
-    int32_t next = 0;   // marks in the earlier segments
+    int32_t next = x - cnt;
     for (int q = 0; q < wv; ++q) next += wsum[q];
-    for (int64_t b = s0; b < s1; b += kIn * kWave) {
-        int32_t v[kIn];
-#pragma unroll
-        for (int u = 0; u < kIn; ++u) {
-            const int64_t p = b + u * kWave + lane;
-            v[u] = p < s1 ? qslot[p] : -1;
-        }
-#pragma unroll
-        for (int u = 0; u < kIn; ++u) {
-            const int64_t p = b + u * kWave + lane;
-            const bool marked = v[u] >= 0;
-            const uint64_t bal = __ballot(marked);
-            const int32_t below = (int32_t)__builtin_amdgcn_mbcnt_hi(
-                (uint32_t)(bal >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)bal, 0u));
-            if (marked) qslot[p] = next + below;
-            next += (int32_t)__popcll(bal);
-        }
+    for (int64_t w = w0; w < w1; ++w) {
+        qbase[w] = next;
+        next += __popc(qbits[w]);
     }
 }
 
-// u1[a] and ue[f] from sorted positions to slots.
+// Slot of a marked position k: the marks below it.
+__device__ __forceinline__ int32_t slot_of(const uint32_t *__restrict__ qbits,
+                                           const int32_t *__restrict__ qbase, int64_t k)
+{
+    const uint32_t below = (1u << (k & 31)) - 1u;
+    return qbase[k >> 5] + __popc(qbits[k >> 5] & below);
+}
+
+// Items 0..K1-1 and K1..K1+P-1: u1[a] and ue[f] from sorted positions to
+// slots; items K1+P .. K1+P+n: the slot of each sorted position 0..n, -1 if
+// it is no query position.
 __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict__ u1,
                                                              int32_t *__restrict__ ue, int32_t K1,
-                                                             int64_t P,
-                                                             const int32_t *__restrict__ qslot)
+                                                             int64_t P, int64_t n,
+                                                             const uint32_t *__restrict__ qbits,
+                                                             const int32_t *__restrict__ qbase,
+                                                             int32_t *__restrict__ qslot)
 {
     const int64_t g = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (g < K1) u1[g] = qslot[u1[g]];
-    else if (g - K1 < P) ue[g - K1] = qslot[ue[g - K1]];
+    if (g < K1) {
+        u1[g] = slot_of(qbits, qbase, u1[g]);
+    } else if (g - K1 < P) {
+        ue[g - K1] = slot_of(qbits, qbase, ue[g - K1]);
+    } else if (g - K1 - P <= n) {
+        const int64_t k = g - K1 - P;
+        qslot[k] = ((qbits[k >> 5] >> (k & 31)) & 1u) ? slot_of(qbits, qbase, k) : -1;
+    }
 }
 
 // One block per resample of the batch.  Per pass over a range of sorted
@@ -554,12 +553,15 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     const unsigned gq = (unsigned)((tb.K1 + P + 255) / 256);
     hipLaunchKernelGGL(factored_bounds_kernel, dim3(gq), dim3(256), 0, stream, ws.sw, n, tb, ws.u1,
                        ws.ue);
-    hipLaunchKernelGGL(factored_fill_kernel, dim3((unsigned)((n + 1 + 255) / 256)), dim3(256), 0,
-                       stream, ws.qslot, n + 1);
+    const int64_t nwords = (n + 1 + 31) / 32;
+    hipLaunchKernelGGL(factored_fill_kernel, dim3((unsigned)((nwords + 255) / 256)), dim3(256), 0,
+                       stream, ws.qbits, nwords);
     hipLaunchKernelGGL(factored_mark_kernel, dim3(gq), dim3(256), 0, stream, ws.u1, ws.ue, tb.K1, P,
-                       ws.qslot);
-    hipLaunchKernelGGL(factored_slot_kernel, dim3(1), dim3(kFThreads), 0, stream, ws.qslot, n + 1);
-    hipLaunchKernelGGL(factored_remap_kernel, dim3(gq), dim3(256), 0, stream, ws.u1, ws.ue, tb.K1, P,
+                       ws.qbits);
+    hipLaunchKernelGGL(factored_slot_kernel, dim3(1), dim3(kFThreads), 0, stream, ws.qbits, ws.qbase,
+                       nwords);
+    hipLaunchKernelGGL(factored_remap_kernel, dim3((unsigned)((tb.K1 + P + n + 1 + 255) / 256)),
+                       dim3(256), 0, stream, ws.u1, ws.ue, tb.K1, P, n, ws.qbits, ws.qbase,
                        ws.qslot);
     if ((err = hipGetLastError()) != hipSuccess) return err;
     const int FL = tb.L <= 16 ? 16 : kFLoads;                 // loads per policy block
