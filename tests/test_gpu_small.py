@@ -1,7 +1,8 @@
 """The one-launch small-sample brute force (kvr_cost_grid, BRUTE, one sample
 within the small-sample limits): sample split groups below, at and off the
 batches of eight that the launch adds up, several load tiles, eight t1 timers,
-no finite deadline, the largest pre-pass histogram the path takes, and a
+no finite deadline, the largest pre-pass histogram and the most pre-pass blocks
+and (group, load tile)s the path takes (and one grid past that limit), and a
 workspace that holds another call's counters and partials; costs against the
 oracle's double loop within 1e-9 relative."""
 import numpy as np
@@ -20,6 +21,9 @@ CASES = [
     ("tiles", 5000, 3, 100, 70, True, 74),
     ("no-finite-deadline", 4000, 2, 1, 5, True, 75),        # t2 = [inf]: no recompute bins
     ("histogram-64x1024", 65536, 4, 256, 2, False, 76),     # 64 pre-pass rows of 1,024 bins
+    ("prepass-256-blocks", 262144, 1, 200, 40, True, 77),   # the most pre-pass blocks, 256
+    ("group-tiles-4096", 100, 8, 512, 2048, True, 78),      # 64 groups x 64 tiles of 32 loads
+    ("group-tiles-4160", 100, 8, 512, 2080, True, 79),      # 65 tiles: past the limit, the multi-launch path
 ]
 
 
