@@ -86,6 +86,34 @@ __device__ __forceinline__ void wave_scan_dpp(unsigned long long &n, double &s,
     es = dpp_f64<0x138, 0xf>(s);
 }
 
+// One step of a wave arg-min by DPP: the (cost, index) pair CTRL names is
+// merged into this lane's under the library's total order; a lane the
+// control gives no source (or masks off) reads the identity (+inf, -1).
+template <int CTRL, int ROWM>
+__device__ __forceinline__ void dpp_argmin_step(double &c, int32_t &f)
+{
+    const unsigned long long cb = (unsigned long long)__double_as_longlong(c);
+    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)cb, CTRL, ROWM, 0xf, false);
+    const int hi = __builtin_amdgcn_update_dpp(0x7ff00000, (int)(uint32_t)(cb >> 32), CTRL, ROWM,
+                                               0xf, false);
+    const int32_t of = __builtin_amdgcn_update_dpp(-1, f, CTRL, ROWM, 0xf, false);
+    const double oc = __longlong_as_double((long long)(((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo));
+    argmin_merge(c, f, oc, of);
+}
+
+// Arg-min of (c, f) over the 64 lanes of a wave, left in lane 63: the steps
+// of wave_scan_dpp with the merge for the sum (the total order makes the
+// result independent of the merge order).
+__device__ __forceinline__ void wave_argmin_dpp(double &c, int32_t &f)
+{
+    dpp_argmin_step<0x111, 0xf>(c, f);
+    dpp_argmin_step<0x112, 0xf>(c, f);
+    dpp_argmin_step<0x114, 0xf>(c, f);
+    dpp_argmin_step<0x118, 0xf>(c, f);
+    dpp_argmin_step<0x142, 0xa>(c, f);
+    dpp_argmin_step<0x143, 0xc>(c, f);
+}
+
 // Per sorted position k: the sorted wait and the context size there (below
 // 1 counts as 1; sort_prep_kernel has flagged it); per base sample: its
 // sorted position.
@@ -502,8 +530,8 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
 #pragma unroll
     for (int l = 0; l < FL; ++l) {
-        wave_argmin(bc[l], bf[l]);
-        if (lane == 0) {
+        wave_argmin_dpp(bc[l], bf[l]);
+        if (lane == kWave - 1) {
             rc[wv][l] = bc[l];
             rf[wv][l] = bf[l];
         }
