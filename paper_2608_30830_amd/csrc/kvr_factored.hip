@@ -26,6 +26,7 @@
 // block per (resample, tile of 32 or 16 loads): every policy from its two slots,
 // fused arg-min on the numerators m*C).
 #include "kvr_device.h"
+#include "kvr_dpp.h"
 #include "kvr_factored.h"
 
 namespace kvr {
@@ -45,73 +46,28 @@ constexpr int kFPolThreads = 256;
 // SIMD), 2 with 16-load tiles (where 4 would cost a wave).
 template <int FL> constexpr int kFPU = FL == 16 ? 2 : 4;
 
-// DPP moves of a 64-bit value as two 32-bit halves; a lane the control gives
-// no source (or masks off) reads 0.
-template <int CTRL, int ROWM>
-__device__ __forceinline__ unsigned long long dpp_u64(unsigned long long v)
-{
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)v, CTRL, ROWM, 0xf, true);
-    const int hi = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)(v >> 32), CTRL, ROWM, 0xf, true);
-    return ((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo;
-}
-template <int CTRL, int ROWM>
-__device__ __forceinline__ double dpp_f64(double v)
-{
-    return __longlong_as_double((long long)dpp_u64<CTRL, ROWM>((unsigned long long)__double_as_longlong(v)));
-}
-
-// Inclusive scan of (n, s) over the 64 lanes of a wave with DPP moves (VALU
-// operations, no LDS round trip): within each row of 16 lanes the values 1,
-// 2, 4 and 8 lanes back are added (row_shr), then lane 15's sum into the
-// next row (row_bcast:15, rows 1 and 3) and lane 31's into rows 2 and 3
-// (row_bcast:31).  The additions follow a fixed tree, so equal inputs give
-// equal sums.  en, es: the exclusive values (the inclusive ones one lane back,
-// wave_shr:1, 0 in lane 0).
-__device__ __forceinline__ void wave_scan_dpp(unsigned long long &n, double &s,
-                                              unsigned long long &en, double &es)
-{
-    n += dpp_u64<0x111, 0xf>(n);
-    s += dpp_f64<0x111, 0xf>(s);
-    n += dpp_u64<0x112, 0xf>(n);
-    s += dpp_f64<0x112, 0xf>(s);
-    n += dpp_u64<0x114, 0xf>(n);
-    s += dpp_f64<0x114, 0xf>(s);
-    n += dpp_u64<0x118, 0xf>(n);
-    s += dpp_f64<0x118, 0xf>(s);
-    n += dpp_u64<0x142, 0xa>(n);
-    s += dpp_f64<0x142, 0xa>(s);
-    n += dpp_u64<0x143, 0xc>(n);
-    s += dpp_f64<0x143, 0xc>(s);
-    en = dpp_u64<0x138, 0xf>(n);
-    es = dpp_f64<0x138, 0xf>(s);
-}
-
 // One step of a wave arg-min by DPP: the (cost, index) pair CTRL names is
 // merged into this lane's under the library's total order; a lane the
 // control gives no source (or masks off) reads the identity (+inf, -1).
 template <int CTRL, int ROWM>
 __device__ __forceinline__ void dpp_argmin_step(double &c, int32_t &f)
 {
-    const unsigned long long cb = (unsigned long long)__double_as_longlong(c);
-    const int lo = __builtin_amdgcn_update_dpp(0, (int)(uint32_t)cb, CTRL, ROWM, 0xf, false);
-    const int hi = __builtin_amdgcn_update_dpp(0x7ff00000, (int)(uint32_t)(cb >> 32), CTRL, ROWM,
-                                               0xf, false);
-    const int32_t of = __builtin_amdgcn_update_dpp(-1, f, CTRL, ROWM, 0xf, false);
-    const double oc = __longlong_as_double((long long)(((unsigned long long)(uint32_t)hi << 32) | (uint32_t)lo));
+    const double oc = dpp_move<CTRL, ROWM>(c, 0x7ff0000000000000ull);
+    const int32_t of = dpp_move<CTRL, ROWM>(f, 0xffffffffull);
     argmin_merge(c, f, oc, of);
 }
 
 // Arg-min of (c, f) over the 64 lanes of a wave, left in lane 63: the steps
-// of wave_scan_dpp with the merge for the sum (the total order makes the
+// of wave_incl_scan with the merge for the sum (the total order makes the
 // result independent of the merge order).
 __device__ __forceinline__ void wave_argmin_dpp(double &c, int32_t &f)
 {
-    dpp_argmin_step<0x111, 0xf>(c, f);
-    dpp_argmin_step<0x112, 0xf>(c, f);
-    dpp_argmin_step<0x114, 0xf>(c, f);
-    dpp_argmin_step<0x118, 0xf>(c, f);
-    dpp_argmin_step<0x142, 0xa>(c, f);
-    dpp_argmin_step<0x143, 0xc>(c, f);
+    dpp_argmin_step<kDppRowShr1, 0xf>(c, f);
+    dpp_argmin_step<kDppRowShr2, 0xf>(c, f);
+    dpp_argmin_step<kDppRowShr4, 0xf>(c, f);
+    dpp_argmin_step<kDppRowShr8, 0xf>(c, f);
+    dpp_argmin_step<kDppRowBcast15, 0xa>(c, f);
+    dpp_argmin_step<kDppRowBcast31, 0xc>(c, f);
 }
 
 // Per sorted position k: the sorted wait and the context size there (below
@@ -245,7 +201,7 @@ __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict
 // positions: the number of the resample's draws of each position, counted in
 // LDS, then a scan over the range in a fixed order (each thread its
 // kFScanPer consecutive positions, the thread totals across the block: the
-// lanes of a wave in wave_scan_dpp's tree, the waves in order, then the
+// lanes of a wave in wave_incl_scan's tree, the waves in order, then the
 // earlier passes), which records
 // at every query position k N(k) = sum_{j < k} c_j T_j (exact, then rounded
 // to double as the closed form uses it) and S(k) = sum_{j < k} c_j T_j w_j
@@ -407,9 +363,9 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                     tn += cwq;
                     ts += sv[q];
                 }
-                unsigned long long xn = tn, en;        // scan of the thread totals in the wave
-                double xs = ts, es;
-                wave_scan_dpp(xn, xs, en, es);
+                // scan of the thread totals in the wave (DPP moves, a fixed tree)
+                const unsigned long long xn = wave_incl_scan(tn), en = wave_lane_back(xn);
+                const double xs = wave_incl_scan(ts), es = wave_lane_back(xs);
                 if (lane == kWave - 1) {
                     wn[wv] = xn;
                     wsd[wv] = xs;

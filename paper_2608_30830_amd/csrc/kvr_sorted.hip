@@ -23,6 +23,7 @@
 // positions; with an order requested (or very many policies) the full
 // inclusive prefix arrays are written and read.
 #include "kvr_device.h"
+#include "kvr_dpp.h"
 
 namespace kvr {
 
@@ -199,11 +200,7 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *t
 {
     __shared__ uint32_t wsum[4];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    uint32_t x = v;
-    for (int off = 1; off < kWave; off <<= 1) {
-        uint32_t y = __shfl_up(x, off, kWave);
-        if (lane >= off) x += y;
-    }
+    const uint32_t x = wave_incl_scan(v);
     if (lane == kWave - 1) wsum[wave] = x;
     __syncthreads();
     uint32_t before = 0;
@@ -214,18 +211,15 @@ __device__ __forceinline__ uint32_t block_exclusive_scan(uint32_t v, uint32_t *t
 }
 
 // Exclusive scan over the 1,024 threads of a block of one value per thread
-// (a fixed order: shuffles within each wave, then the wave totals in order);
-// *total receives the block's sum.
+// (a fixed order: wave_incl_scan's tree within each wave, then the wave totals
+// in order); *total receives the block's sum.
 template <typename V>
 __device__ __forceinline__ V block1024_exclusive_scan(V v, V *total)
 {
     __shared__ V wsum[1024 / kWave];
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    V x = v;
-    for (int off = 1; off < kWave; off <<= 1) {
-        const V y = __shfl_up(x, off, kWave);
-        if (lane >= off) x += y;
-    }
+    const V x = wave_incl_scan(v);
+    const V ex = wave_lane_back(x);
     if (lane == kWave - 1) wsum[wave] = x;
     __syncthreads();
     V before = 0, all = 0;
@@ -235,7 +229,7 @@ __device__ __forceinline__ V block1024_exclusive_scan(V v, V *total)
     }
     *total = all;
     __syncthreads();
-    return before + (x - v);
+    return before + ex;
 }
 
 // One block of 1,024 threads per digit: exclusive scan of that digit's
@@ -472,11 +466,7 @@ __global__ void __launch_bounds__(kOneThreads) sort_small_kernel(
                 wcnt[wb][q][d] = (uint16_t)tot;
                 tot += c[q];
             }
-            uint32_t incl = tot;
-            for (int off = 1; off < kWave; off <<= 1) {
-                const uint32_t y = __shfl_up(incl, off, kWave);
-                if (lane >= off) incl += y;
-            }
+            const uint32_t incl = wave_incl_scan(tot);
             lexcl[d] = incl - tot;
             if (lane == kWave - 1) dsum[wave] = incl;
         }
@@ -521,22 +511,9 @@ __global__ void __launch_bounds__(kOneThreads) sort_small_kernel(
         tn[q] = sn;
         ts[q] = ss;
     }
-    int64_t xn = sn;                 // inclusive scan of the thread totals in the wave
-    double xs = ss;
-    for (int off = 1; off < kWave; off <<= 1) {
-        const int64_t yn = __shfl_up(xn, off, kWave);
-        const double ys = __shfl_up(xs, off, kWave);
-        if (lane >= off) {
-            xn += yn;
-            xs += ys;
-        }
-    }
-    int64_t en = __shfl_up(xn, 1, kWave);   // exclusive within the wave
-    double es = __shfl_up(xs, 1, kWave);
-    if (lane == 0) {
-        en = 0;
-        es = 0.0;
-    }
+    // scan of the thread totals in the wave: inclusive, then exclusive
+    const int64_t xn = wave_incl_scan(sn), en = wave_lane_back(xn);
+    const double xs = wave_incl_scan(ss), es = wave_lane_back(xs);
     __shared__ int64_t wn[kOneWaves];
     __shared__ double wsm[kOneWaves];
     if (lane == kWave - 1) {
@@ -746,16 +723,8 @@ __global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
     }
     // exclusive scan of the per-thread totals across the block
     const int lane = threadIdx.x % kWave, wave = threadIdx.x / kWave;
-    int64_t xn = sn;
-    double xs = ss;
-    for (int off = 1; off < kWave; off <<= 1) {
-        int64_t yn = __shfl_up(xn, off, kWave);
-        double ys = __shfl_up(xs, off, kWave);
-        if (lane >= off) {
-            xn += yn;
-            xs += ys;
-        }
-    }
+    const int64_t xn = wave_incl_scan(sn), en = wave_lane_back(xn);
+    const double xs = wave_incl_scan(ss), es = wave_lane_back(xs);
     __shared__ int64_t wn[4];
     __shared__ double wsm[4];
     if (lane == kWave - 1) {
@@ -769,8 +738,8 @@ __global__ void __launch_bounds__(kScanThreads) scan_final_kernel(
         pn += wn[q];
         ps += wsm[q];
     }
-    pn += xn - sn;
-    ps += xs - ss;
+    pn += en;
+    ps += es;
     if (full) {
         longlong2 *np = reinterpret_cast<longlong2 *>(Nsum + base);
         double2 *sp = reinterpret_cast<double2 *>(Ssum + base);
