@@ -289,12 +289,14 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
     uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
 {
-    // 16-bit counters and 32-bit bases keep a block at 29 KiB of LDS (five
-    // resident blocks per CU at 2,048-key tiles): a wave holds at most 64 * KPT
-    // keys, a tile at most 4,096,
-    // and a destination fits 32 bits (n < 2^31)
+    // 16-bit counters and 32-bit bases keep a block at 27.5 KiB of LDS at
+    // 2,048-key tiles (five resident blocks per CU) and at 51.5 KiB at 4,096
+    // (three; with a separate offset table, 53.5 KiB, two): a wave holds at
+    // most 64 * KPT keys, a tile at most 4,096, and a destination fits 32 bits
+    // (n < 2^31).  wcnt holds the waves' digit counts, then, in place, each
+    // wave's first tile position within its digit (wofs)
     __shared__ uint16_t wcnt[4][256];
-    __shared__ uint16_t wofs[4][256];
+    auto &wofs = wcnt;
     __shared__ int32_t gbase[256];                   // destination of digit d's first tile key
     constexpr int kTile = kSortThreads * KPT, kWaveK = kWave * KPT;
     __shared__ uint64_t lkey[kTile];
@@ -948,6 +950,15 @@ static hipError_t launch_closed_form(const uint64_t *skeys, const SortWs &ws, in
     return hipGetLastError();
 }
 
+// Unused dynamic LDS that holds the 4,096-key scatter at two blocks per CU
+// from 2^24 keys: three blocks per CU (52 KiB each) measured faster at 2^23
+// (0.585 against 0.634 ms per call on MI355X) but slower at 2^24 (1.287
+// against 1.256 ms, the same box).
+static size_t scatter_lds_pad(int kpt, int64_t n)
+{
+    return (kpt == 16 && n >= (int64_t(1) << 24)) ? 4096 : 0;
+}
+
 template <int KPT>
 static hipError_t launch_digit_passes(const double *w, const int32_t *T, int64_t n, SortWs &ws,
                                       int payload_T, int *status, hipStream_t stream)
@@ -963,9 +974,9 @@ static hipError_t launch_digit_passes(const double *w, const int32_t *T, int64_t
                                stream, ws.keys[cur], n, shift, ws.hist, ws.nblocks);
         hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(1024), 0, stream, ws.hist,
                            ws.nblocks, ws.counts);
-        hipLaunchKernelGGL(sort_scatter_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0,
-                           stream, ws.keys[cur], ws.vals[cur], n, shift, ws.hist, ws.counts,
-                           ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        hipLaunchKernelGGL(sort_scatter_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads),
+                           scatter_lds_pad(KPT, n), stream, ws.keys[cur], ws.vals[cur], n, shift,
+                           ws.hist, ws.counts, ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
         err = hipGetLastError();
         cur ^= 1;
     }
