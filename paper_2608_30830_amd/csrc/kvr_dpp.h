@@ -67,6 +67,29 @@ __device__ __forceinline__ V wave_incl_scan(V x)
     return x;
 }
 
+// Sum over the 64 lanes in wave_incl_scan's tree, returned to every lane
+// (lane 63's inclusive value, read as a scalar).
+template <typename V>
+__device__ __forceinline__ V wave_total(V x)
+{
+    static_assert(sizeof(V) == 4 || sizeof(V) == 8, "4- or 8-byte values");
+    x = wave_incl_scan(x);
+    if constexpr (sizeof(V) == 4) {
+        uint32_t u;
+        __builtin_memcpy(&u, &x, 4);
+        u = (uint32_t)__builtin_amdgcn_readlane((int)u, 63);
+        __builtin_memcpy(&x, &u, 4);
+    } else {
+        uint64_t u;
+        __builtin_memcpy(&u, &x, 8);
+        const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, 63);
+        const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), 63);
+        u = ((uint64_t)hi << 32) | lo;
+        __builtin_memcpy(&x, &u, 8);
+    }
+    return x;
+}
+
 // The value one lane back (zero in lane 0): with an inclusive scan, the
 // exclusive one.
 template <typename V>

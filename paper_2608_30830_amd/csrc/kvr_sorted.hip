@@ -580,11 +580,11 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
             en = t;
             es = (double)t * __longlong_as_double((long long)skeys[j]);
         }
-        if (CHUNKS) {   // this wave's 64 positions of row q, then into the wave's total
-            en = wave_sum(en);
-            es = wave_sum(es);
+        if (CHUNKS) {   // this wave's 64 positions of row q (their sum in lane 63), then into the wave's total
+            en = wave_incl_scan(en);
+            es = wave_incl_scan(es);
             const int64_t c = ((int64_t)blockIdx.x * kScanIPT + q) * (kScanThreads / kWave) + wave;
-            if (lane == 0 && c * kWave < n) {
+            if (lane == kWave - 1 && c * kWave < n) {
                 chunkN[c] = en;
                 chunkS[c] = es;
             }
@@ -592,15 +592,15 @@ __global__ void __launch_bounds__(kScanThreads) scan_reduce_kernel(
         sn += en;
         ss += es;
     }
-    // fixed-order tree: butterfly within each wave (done per chunk with
-    // CHUNKS), then the four waves in order
+    // fixed-order tree: wave_incl_scan's within each wave (done per chunk
+    // with CHUNKS), the total in lane 63, then the four waves in order
     if (!CHUNKS) {
-        sn = wave_sum(sn);
-        ss = wave_sum(ss);
+        sn = wave_incl_scan(sn);
+        ss = wave_incl_scan(ss);
     }
     __shared__ int64_t rn[kScanThreads / kWave];
     __shared__ double rs[kScanThreads / kWave];
-    if (lane == 0) {
+    if (lane == kWave - 1) {
         rn[wave] = sn;
         rs[wave] = ss;
     }
@@ -832,8 +832,8 @@ __device__ __forceinline__ void closed_form_policy(const int64_t *__restrict__ N
 
 // N and S over the sorted positions [0, p), by one wave: the tile's exclusive
 // prefix, the 64-position chunk sums of the tile before p and the positions of
-// p's own chunk, each group added across the lanes in a fixed order; every
-// lane returns the same values, and equal p give equal values.
+// p's own chunk, each group added across the lanes in wave_total's fixed tree;
+// every lane returns the same values, and equal p give equal values.
 __device__ __forceinline__ void wave_prefix_at(int64_t p, int nb, const int64_t *__restrict__ blkN,
                                                const double *__restrict__ blkS,
                                                const int64_t *__restrict__ chunkN,
@@ -860,10 +860,10 @@ __device__ __forceinline__ void wave_prefix_at(int64_t p, int nb, const int64_t 
         en = t;
         es = (double)t * __longlong_as_double((long long)skeys[j]);
     }
-    cn = wave_sum(cn);
-    cs = wave_sum(cs);
-    en = wave_sum(en);
-    es = wave_sum(es);
+    cn = wave_total(cn);
+    cs = wave_total(cs);
+    en = wave_total(en);
+    es = wave_total(es);
     N = blkN[tile] + cn + en;
     S = (blkS[tile] + cs) + es;
 }
