@@ -296,13 +296,20 @@ def time_paths(kvr, workloads, torch):
     return res
 
 
-# Algorithmic bytes per key of the SORTED path (no order requested): key
-# preparation, which also counts the first digit (12 B read: wait and context
-# size; 12 B written: key and payload); seven histogram reads of the keys for
-# the other digits (8 B each); eight scatters (12 B read, 12 B written each);
-# the tile and 64-key chunk sums (12 B read, 16 B written per 64 keys).  The
-# closed form then reads N and S at its query positions only.
-SORT_BYTES_PER_KEY = 24 + 7 * 8 + 8 * 24 + 12 + 16 / 64
+# Algorithmic bytes per key of the SORTED path (no order requested): the first
+# digit's tile histograms from the waits (8 B read); the histograms of the
+# other seven digits (below 2^22 keys each reads the 8-byte keys; from 2^22 the
+# one-byte digits that the previous scatter wrote: 1 B read, and 1 B written
+# by each of the first seven scatters); eight scatters (12 B read, 12 B
+# written each; the first reads the waits and context sizes); the tile and
+# 64-key chunk sums (12 B read, 16 B written per 64 keys).  The closed form
+# then reads N and S at its query positions only.
+SORT_DIGIT_BYTES_FROM = 1 << 22
+
+
+def sort_bytes_per_key(n: int) -> float:
+    hist = 7 * (1 + 1) if n >= SORT_DIGIT_BYTES_FROM else 7 * 8
+    return 8 + hist + 8 * 24 + 12 + 16 / 64
 
 
 def time_factored(kvr, workloads, torch):
@@ -341,7 +348,7 @@ def time_sort_scale(kvr, workloads, torch):
         T = torch.as_tensor(wl.ctx_tokens).cuda()
         call = kvr.CostGridCall(w, T, pr, g, method=kvr.KVR_SORTED)
         ms = _median_ms(torch, call.launch, 11)
-        bps = SORT_BYTES_PER_KEY * wl.n / (ms * 1e-3)
+        bps = sort_bytes_per_key(wl.n) * wl.n / (ms * 1e-3)
         res[wl.name] = {"ms": ms, "keys_per_s": wl.n / (ms * 1e-3), "algorithmic_bytes_per_s": bps,
                         "hbm_frac": bps / (HBM_PEAK_TBS * 1e12)}
         log(f"[bench] sorted {wl.name}: {ms:.3f} ms, {bps / 1e12:.2f} TB/s algorithmic")

@@ -25,6 +25,8 @@
 #include "kvr_device.h"
 #include "kvr_dpp.h"
 
+#include <type_traits>
+
 namespace kvr {
 
 constexpr int kSortThreads = 256;
@@ -97,43 +99,44 @@ __device__ __forceinline__ int sort_tile(int nblocks)
     return (int)xcd_logical_block(blockIdx.x, nblocks);
 }
 
-// Keys from waits (domain-checked on the bits), the payload (the context size
-// when the caller needs only the prefix sums, else the base index), and the
-// tile histograms of the first digit pass, so that pass reads no keys again.
-// Tiles are those of the digit passes (256 * KPT keys); digit-major histogram
-// hist[d * nblocks + tile].
+// Key of a wait: its bits, with -0.0 as +0.0 (waits are >= 0, so the
+// unsigned order of the bits is numeric order); a NaN, an infinity or a
+// negative wait sets bad and becomes key 0.
+__device__ __forceinline__ uint64_t wait_key(double x, bool &bad)
+{
+    uint64_t b = (uint64_t)__double_as_longlong(x);
+    if (b == 0x8000000000000000ull) b = 0;
+    if (b >= 0x7ff0000000000000ull) {
+        bad = true;
+        b = 0;
+    }
+    return b;
+}
+
+// Tile histograms of the first digit straight from the waits (domain-checked
+// on the bits), so that the first scatter can read the waits and context
+// sizes itself and no key array is written before it.  Tiles are those of the
+// digit passes (256 * KPT keys); digit-major histogram hist[d * nblocks + tile].
 template <int KPT>
-__global__ void __launch_bounds__(kSortThreads) sort_prep_kernel(
-    const double *__restrict__ w, const int32_t *__restrict__ T, int64_t n, int payload_T,
-    uint64_t *__restrict__ keys, int32_t *__restrict__ vals, uint32_t *__restrict__ hist,
-    int nblocks, int *status)
+__global__ void __launch_bounds__(kSortThreads) sort_first_hist_kernel(
+    const double *__restrict__ w, int64_t n, uint32_t *__restrict__ hist, int nblocks,
+    int *status)
 {
     __shared__ uint32_t h[256];
     h[threadIdx.x] = 0;
     __syncthreads();
     const int tile = sort_tile(nblocks);
     const int64_t base = (int64_t)tile * (kSortThreads * KPT);
+    double x[KPT];
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {   // every load in flight before counting
+        const int64_t i = base + q * kSortThreads + threadIdx.x;
+        x[q] = i < n ? w[i] : 0.0;
+    }
     bool bad = false;
 #pragma unroll
-    for (int q = 0; q < KPT; ++q) {
-        const int64_t i = base + q * kSortThreads + threadIdx.x;
-        if (i < n) {
-            uint64_t b = (uint64_t)__double_as_longlong(w[i]);
-            int32_t t = T[i];
-            if (b == 0x8000000000000000ull) b = 0;  // -0.0 sorts as +0.0
-            if (b >= 0x7ff0000000000000ull) {        // NaN, inf or negative
-                bad = true;
-                b = 0;
-            }
-            if (t < 1) {
-                bad = true;
-                t = 1;
-            }
-            keys[i] = b;
-            vals[i] = payload_T ? t : (int32_t)i;
-            atomicAdd(&h[b & 255u], 1u);
-        }
-    }
+    for (int q = 0; q < KPT; ++q)
+        if (base + q * kSortThreads + threadIdx.x < n) atomicAdd(&h[wait_key(x[q], bad) & 255u], 1u);
     if (bad) flag_domain(status);
     __syncthreads();
     hist[(int64_t)threadIdx.x * nblocks + tile] = h[threadIdx.x];
@@ -185,6 +188,43 @@ __global__ void __launch_bounds__(kSortThreads) sort_hist_kernel(const uint64_t 
     for (int q = 0; q < KPT; ++q) {
         const bool valid = base + q * kSortThreads + threadIdx.x < n;
         const uint32_t d = (uint32_t)(key[q] >> shift) & 255u;
+        const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
+        const uint64_t same = __ballot(valid && d == d0);
+        if (lane == 0 && same != 0) atomicAdd(&h[d0], (uint32_t)__popcll(same));
+        else if (valid && d != d0) atomicAdd(&h[d], 1u);
+    }
+    __syncthreads();
+    hist[(int64_t)threadIdx.x * nblocks + tile] = h[threadIdx.x];
+}
+
+// The same histogram from the digit bytes that the previous pass's scatter
+// wrote beside the keys (dig[i] = this pass's digit of the key at i): one
+// byte per key read instead of eight.  A tile's count does not depend on the
+// order of its keys, so each thread reads KPT consecutive bytes in one load;
+// bytes past n (up to the end of the last tile, inside the buffer) are not
+// counted.
+template <int KPT>
+__global__ void __launch_bounds__(kSortThreads) sort_hist_bytes_kernel(
+    const uint8_t *__restrict__ dig, int64_t n, uint32_t *__restrict__ hist, int nblocks)
+{
+    using Vec = typename std::conditional<
+        KPT == 16, uint4,
+        typename std::conditional<KPT == 8, uint2,
+                                  typename std::conditional<KPT == 4, uint32_t, uint16_t>::type>::type>::type;
+    static_assert(sizeof(Vec) == KPT, "one load of KPT bytes");
+    __shared__ uint32_t h[256];
+    h[threadIdx.x] = 0;
+    __syncthreads();
+    const int tile = sort_tile(nblocks);
+    const int64_t i0 = (int64_t)tile * (kSortThreads * KPT) + (int64_t)threadIdx.x * KPT;
+    const Vec v = *reinterpret_cast<const Vec *>(dig + i0);
+    uint8_t b[KPT];
+    __builtin_memcpy(b, &v, KPT);
+    const int lane = threadIdx.x % kWave;
+#pragma unroll
+    for (int q = 0; q < KPT; ++q) {
+        const bool valid = i0 + q < n;
+        const uint32_t d = b[q];
         const uint32_t d0 = __builtin_amdgcn_readfirstlane(d);
         const uint64_t same = __ballot(valid && d == d0);
         if (lane == 0 && same != 0) atomicAdd(&h[d0], (uint32_t)__popcll(same));
@@ -283,11 +323,13 @@ __global__ void __launch_bounds__(1024) digit_scan_kernel(uint32_t *__restrict__
 // digit_scan_kernel) + (keys with its digit earlier in this tile).  The tile
 // is first reordered by digit in LDS, then written out in that order, so
 // consecutive threads store consecutive addresses within each digit's run.
-template <int KPT>
+template <int KPT, bool FIRST>
 __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
-    const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in, int64_t n, int shift,
-    const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
-    uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out)
+    const uint64_t *__restrict__ keys_in, const int32_t *__restrict__ vals_in,
+    const double *__restrict__ w, const int32_t *__restrict__ T, int payload_T, int64_t n,
+    int shift, const uint32_t *__restrict__ offs, const uint32_t *__restrict__ totals, int nblocks,
+    uint64_t *__restrict__ keys_out, int32_t *__restrict__ vals_out, uint8_t *__restrict__ dig_out,
+    int *status)
 {
     // 16-bit counters and 32-bit bases keep a block at 27.5 KiB of LDS at
     // 2,048-key tiles (five resident blocks per CU) and at 51.5 KiB at 4,096
@@ -319,11 +361,33 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
     uint64_t key[KPT];
     int32_t val[KPT];
     uint32_t local[KPT];
+    if (FIRST) {   // keys from the waits, payload the context size (payload_T) or the base index
+        double x[KPT];
+        int32_t t[KPT];
 #pragma unroll
-    for (int j = 0; j < KPT; ++j) {   // every load of the wave in flight before ranking
-        const int64_t i = base + j * kWave + lane;
-        key[j] = i < n ? keys_in[i] : 0;
-        val[j] = i < n ? vals_in[i] : 0;
+        for (int j = 0; j < KPT; ++j) {   // every load of the wave in flight before ranking
+            const int64_t i = base + j * kWave + lane;
+            x[j] = i < n ? w[i] : 0.0;
+            t[j] = i < n ? T[i] : 1;
+        }
+        bool bad = false;
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {
+            key[j] = wait_key(x[j], bad);
+            if (t[j] < 1) {
+                bad = true;
+                t[j] = 1;
+            }
+            val[j] = payload_T ? t[j] : (int32_t)(base + j * kWave + lane);
+        }
+        if (bad) flag_domain(status);
+    } else {
+#pragma unroll
+        for (int j = 0; j < KPT; ++j) {   // every load of the wave in flight before ranking
+            const int64_t i = base + j * kWave + lane;
+            key[j] = i < n ? keys_in[i] : 0;
+            val[j] = i < n ? vals_in[i] : 0;
+        }
     }
 #pragma unroll
     for (int j = 0; j < KPT; ++j) {
@@ -384,6 +448,7 @@ __global__ void __launch_bounds__(kSortThreads) sort_scatter_kernel(
             if (dest >= 0 && dest < n) {  // always true when the histograms agree
                 keys_out[dest] = k;
                 vals_out[dest] = lval[pos];
+                if (dig_out != nullptr) dig_out[dest] = (uint8_t)(k >> (shift + 8));   // uniform
             }
         }
     }
@@ -954,6 +1019,8 @@ static hipError_t launch_closed_form(const uint64_t *skeys, const SortWs &ws, in
 // from 2^24 keys: three blocks per CU (52 KiB each) measured faster at 2^23
 // (0.585 against 0.634 ms per call on MI355X) but slower at 2^24 (1.287
 // against 1.256 ms, the same box).
+constexpr int64_t kDigitBytesFrom = int64_t(1) << 22;
+
 static size_t scatter_lds_pad(int kpt, int64_t n)
 {
     return (kpt == 16 && n >= (int64_t(1) << 24)) ? 4096 : 0;
@@ -963,22 +1030,44 @@ template <int KPT>
 static hipError_t launch_digit_passes(const double *w, const int32_t *T, int64_t n, SortWs &ws,
                                       int payload_T, int *status, hipStream_t stream)
 {
-    hipLaunchKernelGGL(sort_prep_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0, stream, w,
-                       T, n, payload_T, ws.keys[0], ws.vals[0], ws.hist, ws.nblocks, status);
-    hipError_t err = hipGetLastError();
-    int cur = 0;
+    // From 2^22 keys each scatter also writes the next pass's digit bytes, to
+    // the prefix-sum buffer (unused until the sort is done; 8 n bytes hold the
+    // bytes of whole tiles, n > kSortTile), and the histograms read those.
+    // Measured on MI355X: at 2^24 a pass's histogram 31.8 -> 13.0 us, its
+    // scatter 99.3 -> 107.7 us, the call 1.227 -> 1.160 ms; at 2^20 the
+    // scatter's extra stores cost more than the histogram saves (12.8 -> 15.3
+    // against 4.9 -> 4.2 us).
+    uint8_t *const dig = n >= kDigitBytesFrom ? reinterpret_cast<uint8_t *>(ws.Nsum) : nullptr;
+    if ((int64_t)ws.nblocks * kSortThreads * KPT > 8 * n) return hipErrorInvalidValue;
+    const size_t pad = scatter_lds_pad(KPT, n);
+    hipError_t err = hipSuccess;
+    // pass p reads buffer (p & 1) and writes the other; the first reads the
+    // waits and context sizes and writes buffer 1, so the eighth writes buffer 0
     for (int pass = 0; pass < 8 && err == hipSuccess; ++pass) {
-        const int shift = 8 * pass;
-        if (pass > 0)   // the first pass's histograms come from sort_prep_kernel
+        const int shift = 8 * pass, in = pass & 1, out = in ^ 1;
+        if (pass == 0)
+            hipLaunchKernelGGL(sort_first_hist_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads),
+                               0, stream, w, n, ws.hist, ws.nblocks, status);
+        else if (dig != nullptr)
+            hipLaunchKernelGGL(sort_hist_bytes_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads),
+                               0, stream, dig, n, ws.hist, ws.nblocks);
+        else
             hipLaunchKernelGGL(sort_hist_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads), 0,
-                               stream, ws.keys[cur], n, shift, ws.hist, ws.nblocks);
+                               stream, ws.keys[in], n, shift, ws.hist, ws.nblocks);
         hipLaunchKernelGGL(digit_scan_kernel, dim3(256), dim3(1024), 0, stream, ws.hist,
                            ws.nblocks, ws.counts);
-        hipLaunchKernelGGL(sort_scatter_kernel<KPT>, dim3(ws.nblocks), dim3(kSortThreads),
-                           scatter_lds_pad(KPT, n), stream, ws.keys[cur], ws.vals[cur], n, shift,
-                           ws.hist, ws.counts, ws.nblocks, ws.keys[cur ^ 1], ws.vals[cur ^ 1]);
+        uint8_t *const dnext = pass < 7 ? dig : nullptr;
+        if (pass == 0)
+            hipLaunchKernelGGL((sort_scatter_kernel<KPT, true>), dim3(ws.nblocks),
+                               dim3(kSortThreads), pad, stream, nullptr, nullptr, w, T, payload_T,
+                               n, shift, ws.hist, ws.counts, ws.nblocks, ws.keys[out],
+                               ws.vals[out], dnext, status);
+        else
+            hipLaunchKernelGGL((sort_scatter_kernel<KPT, false>), dim3(ws.nblocks),
+                               dim3(kSortThreads), pad, stream, ws.keys[in], ws.vals[in], nullptr,
+                               nullptr, 0, n, shift, ws.hist, ws.counts, ws.nblocks, ws.keys[out],
+                               ws.vals[out], dnext, status);
         err = hipGetLastError();
-        cur ^= 1;
     }
     return err;
 }

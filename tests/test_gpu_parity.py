@@ -193,6 +193,27 @@ def test_max_size_2p24_waits(kvr, oracle_mod):
                                                            g.last_inf)[0]), rb)
 
 
+@pytest.mark.parametrize("n", [(1 << 22) + 1001, (1 << 23) + 4095],
+                         ids=["2p22+1001-kpt8", "2p23+4095-kpt16"])
+def test_sorted_digit_byte_passes(kvr, oracle_mod, n):
+    """From 2^22 waits each digit pass counts the digit bytes that the
+    previous scatter wrote instead of reading the keys: ragged samples at 8 and
+    16 keys per thread, with duplicated and zero waits; the stable order bit
+    for bit, and the costs with and without a requested order against the
+    oracle's closed form."""
+    wl = workloads.random_case(300 + n % 97, n, 2, 40, 4, ties=True)
+    pr = oracle_mod.workload_prices(wl)
+    cs, perm, g = run_grid(kvr, wl, "sorted")
+    ref_perm = oracle_mod.stable_order(wl.wait_s)
+    assert np.array_equal(perm, ref_perm)
+    closed = oracle_mod.closed_form_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                         perm=ref_perm)
+    assert_costs(cs, closed)
+    cost = kvr.kvr_cost_grid(_dev(wl.wait_s, _f64()), _dev(wl.ctx_tokens, _i32()),
+                             _lib_prices(kvr, wl), g, method=kvr.KVR_SORTED)
+    assert_costs(_np(cost), closed)
+
+
 @pytest.mark.parametrize("case", [(201, 500, 2, 70, 5, 3, None), (202, 1300, 1, 65, 16, 4, 777),
                                   (203, 64, 3, 9, 3, 5, 200), (204, 2000, 2, 128, 33, 2, None),
                                   # few resamples, many draws: several recompute-share blocks
