@@ -466,9 +466,10 @@ __global__ void __launch_bounds__(kFPolThreads) factored_policy_kernel(
             double hold = (se[u] - s1[u]) - t1[u] * (ne[u] - n1[u]);
             if (!isinf(e[u])) hold = hold + (e[u] - t1[u]) * (tot - ne[u]);
             const double fixed = pr.a1 * hbm + pr.b2 * (ne[u] - n1[u]) + pr.b3 * (tot - ne[u]);
-            if (cost_out != nullptr) {
-                for (int l = 0; l < nl; ++l)
-                    cost_out[(r * tb.L + l0 + l) * P + f] = (fixed + a2[l] * hold) / md;
+            if (cost_out != nullptr) {   // unrolled, so that a2 stays in registers
+#pragma unroll
+                for (int l = 0; l < FL; ++l)
+                    if (l < nl) cost_out[(r * tb.L + l0 + l) * P + f] = (fixed + a2[l] * hold) / md;
             }
             // every load of the tile (a2 is zero-padded past L; those lanes are
             // never stored); a thread visits its policies in increasing f, so
