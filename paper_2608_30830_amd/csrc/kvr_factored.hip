@@ -45,6 +45,9 @@ constexpr int kFPolThreads = 256;
 // policies' dependent gathers more in flight, at the same three waves per
 // SIMD), 2 with 16-load tiles (where 4 would cost a wave).
 template <int FL> constexpr int kFPU = FL == 16 ? 2 : 4;
+// Draws per resample up to which every N sum (m times a context size below
+// 2^31) is an integer below 2^53, exact in double.
+constexpr int64_t kFExactDoubleDraws = int64_t(1) << 22;
 
 // One step of a wave arg-min by DPP: the (cost, index) pair CTRL names is
 // merged into this lane's under the library's total order; a lane the
@@ -220,6 +223,11 @@ __global__ void __launch_bounds__(256) factored_remap_kernel(int32_t *__restrict
 // exactly) detects it; the resample then restarts with 32-bit counters by
 // sorted position, kFLdsWords positions per pass.  A bootstrap row's
 // multiplicities are Poisson(1)-like, so 4-bit fields almost never wrap.
+// NT carries the N sums: double when every sum is an integer below 2^53 (the
+// host picks it for m <= 2^22, a context size being below 2^31), where it is
+// exact in any order and costs fewer instructions than 64-bit integers;
+// unsigned 64-bit otherwise.
+template <typename NT>
 __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     const int32_t *__restrict__ idx, int64_t n, int64_t m, int64_t r0,
     const int32_t *__restrict__ rank, const int32_t *__restrict__ perm,
@@ -230,7 +238,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     constexpr int nw = kFPThreads / kWave;
     constexpr int kTile = kFPThreads * kFScanPer;
     __shared__ uint32_t lh[kFLdsWords];
-    __shared__ unsigned long long wn[nw];
+    __shared__ NT wn[nw];
     __shared__ double wsd[nw];
     __shared__ long long wchk[nw];
     const int64_t rb = blockIdx.x;
@@ -238,12 +246,12 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     double2 *qrow = TQ + rb * nqs;
     const int lane = threadIdx.x % kWave, wv = threadIdx.x / kWave;
     const int64_t B = blockDim.x;
-    unsigned long long carry_n = 0ull;   // totals of the earlier positions (same in every thread)
+    NT carry_n = 0;   // totals of the earlier positions (same in every thread)
     double carry_s = 0.0;
     for (int wide = 0; wide < 2; ++wide) {
         const int64_t PP = wide ? kFLdsWords : kFPerWord * (int64_t)kFLdsWords;   // positions per pass
         bool overflow = false;
-        carry_n = 0ull;
+        carry_n = 0;
         carry_s = 0.0;
         for (int64_t k0 = 0; k0 < n && !overflow; k0 += PP) {
             const int64_t nk = (n - k0 < PP) ? n - k0 : PP;
@@ -310,10 +318,10 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
             }
             for (int64_t base = 0; base < nk; base += kTile) {
                 const int64_t kl = base + (int64_t)threadIdx.x * kFScanPer;   // position in the pass
-                unsigned long long cw[kFScanPer];
+                NT cw[kFScanPer];
                 double sv[kFScanPer];
                 int32_t qs[kFScanPer];
-                unsigned long long tn = 0ull;
+                NT tn = 0;
                 double ts = 0.0;
                 // a full run of kFScanPer positions starts on a multiple of
                 // kFScanPer (pass starts are multiples of 2^14): 16-byte loads
@@ -355,23 +363,22 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
                     // the counter of position k, or of the base sample there
                     const int64_t ck = byidx ? (int64_t)((uint32_t)pv[q] < (uint32_t)n ? pv[q] : 0) : k;
                     if (in) c = wide ? lh[k] : (lh[ck / kFPerWord] >> (kFBits * (int)(ck % kFPerWord))) & kFMask;
-                    const unsigned long long cwq =
-                        in ? (unsigned long long)c * (unsigned long long)tv[q] : 0ull;
+                    const NT cwq = in ? (NT)c * (NT)tv[q] : (NT)0;   // exact
                     cw[q] = cwq;
-                    sv[q] = in ? (double)cwq * wv4[q] : 0.0;
+                    sv[q] = (double)cwq * wv4[q];
                     qs[q] = in ? qv[q] : -1;
                     tn += cwq;
                     ts += sv[q];
                 }
                 // scan of the thread totals in the wave (DPP moves, a fixed tree)
-                const unsigned long long xn = wave_incl_scan(tn), en = wave_lane_back(xn);
+                const NT xn = wave_incl_scan(tn), en = wave_lane_back(xn);
                 const double xs = wave_incl_scan(ts), es = wave_lane_back(xs);
                 if (lane == kWave - 1) {
                     wn[wv] = xn;
                     wsd[wv] = xs;
                 }
                 __syncthreads();
-                unsigned long long pn = carry_n;
+                NT pn = carry_n;
                 double ps = carry_s;
                 for (int q = 0; q < wv; ++q) {
                     pn += wn[q];
@@ -397,7 +404,7 @@ __global__ void __launch_bounds__(kFPThreads) factored_prefix_kernel(
     if (threadIdx.x == 0) {
         const int32_t q = qslot[n];
         if (q >= 0 && q < nqs) qrow[q] = make_double2((double)carry_n, carry_s);
-        tot[rb] = carry_n;
+        tot[rb] = (unsigned long long)carry_n;
     }
 }
 
@@ -553,9 +560,16 @@ hipError_t launch_factored(const SampleSrc &src, int64_t R, const Tables &tb, co
     const int ntl = (tb.L + FL - 1) / FL;
     for (int64_t r0 = 0; r0 < R; r0 += ws.Rb) {
         const int64_t rb = (R - r0 < ws.Rb) ? R - r0 : ws.Rb;
-        hipLaunchKernelGGL(factored_prefix_kernel, dim3((unsigned)rb), dim3(kFPThreads), 0, stream,
-                           src.idx, n, m, r0, ws.rank, ws.sort.vals[cur], ws.Ts, ws.sw, ws.qslot,
-                           ws.nqs, ws.TQ, ws.tot, status);
+        if (m <= kFExactDoubleDraws)
+            hipLaunchKernelGGL(factored_prefix_kernel<double>, dim3((unsigned)rb),
+                               dim3(kFPThreads), 0, stream, src.idx, n, m, r0, ws.rank,
+                               ws.sort.vals[cur], ws.Ts, ws.sw, ws.qslot, ws.nqs, ws.TQ, ws.tot,
+                               status);
+        else
+            hipLaunchKernelGGL(factored_prefix_kernel<unsigned long long>, dim3((unsigned)rb),
+                               dim3(kFPThreads), 0, stream, src.idx, n, m, r0, ws.rank,
+                               ws.sort.vals[cur], ws.Ts, ws.sw, ws.qslot, ws.nqs, ws.TQ, ws.tot,
+                               status);
         if (FL == 16)
             hipLaunchKernelGGL(factored_policy_kernel<16>, dim3((unsigned)(rb * ntl)),
                                dim3(kFPolThreads), 0, stream, ws.TQ, ws.nqs, ws.tot, m, r0,

@@ -165,6 +165,24 @@ def test_factored_heavy_multiplicities(kvr, oracle_mod, n):
         assert_costs(_np(bc)[r], rbc)
 
 
+def test_factored_many_draws_integer_sums(kvr, oracle_mod):
+    """More than 2^22 draws per resample: the prefix kernel carries the N sums
+    in 64-bit integers (below that, in doubles, exact while m times a context
+    size stays below 2^53); costs and selections against the oracle's double
+    loop."""
+    m = (1 << 22) + 7
+    wl = workloads.random_case(210, 3000, 1, 9, 3, resamples=2, m=m, ties=True)
+    best, bc, cost = _factored(kvr, wl, want_cost=True)
+    pr = oracle_mod.workload_prices(wl)
+    for r in range(2):
+        ref = oracle_mod.cost_grid(wl.wait_s, wl.ctx_tokens, pr, wl.t1, wl.t2, wl.lam,
+                                   idx_row=wl.idx[r])
+        assert_costs(_np(cost)[r], ref)
+        rb, rbc, _ = oracle_mod.select(ref, wl.t2)
+        assert_selection(ref, _np(best)[r], rb)
+        assert_costs(_np(bc)[r], rbc)
+
+
 @pytest.mark.parametrize("name", sorted(__import__("tests.test_gpu_parity",
                                                    fromlist=["DEGENERATE"]).DEGENERATE))
 def test_factored_degenerate_inputs(kvr, oracle_mod, name):
