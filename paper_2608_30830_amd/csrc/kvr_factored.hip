@@ -74,7 +74,7 @@ __device__ __forceinline__ void wave_argmin_dpp(double &c, int32_t &f)
 }
 
 // Per sorted position k: the sorted wait and the context size there (below
-// 1 counts as 1; the first scatter of the sort has flagged it); per base sample: its
+// 1 counts as 1; the sort has flagged it); per base sample: its
 // sorted position.
 __global__ void __launch_bounds__(256) factored_rank_kernel(const uint64_t *__restrict__ skeys,
                                                             const int32_t *__restrict__ perm,
