@@ -193,14 +193,14 @@ def test_max_size_2p24_waits(kvr, oracle_mod):
                                                            g.last_inf)[0]), rb)
 
 
-@pytest.mark.parametrize("n", [(1 << 22) + 1001, (1 << 23) + 4095],
-                         ids=["2p22+1001-kpt8", "2p23+4095-kpt16"])
+@pytest.mark.parametrize("n", [(1 << 22) - 1, (1 << 22) + 1001, (1 << 23) + 4095],
+                         ids=["2p22-1-keys", "2p22+1001-kpt8", "2p23+4095-kpt16"])
 def test_sorted_digit_byte_passes(kvr, oracle_mod, n):
     """From 2^22 waits each digit pass counts the digit bytes that the
-    previous scatter wrote instead of reading the keys: ragged samples at 8 and
-    16 keys per thread, with duplicated waits and both signed zeros; the
-    stable order bit for bit, and the costs with and without a requested order
-    against the oracle's closed form."""
+    previous scatter wrote instead of reading the keys (one below that, the
+    keys): ragged samples at 8 and 16 keys per thread, with duplicated waits
+    and both signed zeros; the stable order bit for bit, and the costs with
+    and without a requested order against the oracle's closed form."""
     wl = workloads.random_case(300 + n % 97, n, 2, 40, 4, ties=True)
     rng = np.random.default_rng(n)
     wl.wait_s[rng.integers(0, n, n // 64)] = -0.0   # sorts as +0.0, in input order
