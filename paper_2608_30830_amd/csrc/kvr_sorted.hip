@@ -15,7 +15,10 @@
 // passes, each reduce-then-scan (tile histograms, one exclusive scan, a
 // ranking scatter); no inter-workgroup waiting, so no forward-progress
 // assumption.  Ranking inside a tile is stable: a wave ranks its keys with a
-// ballot match on the digit, in input order.
+// ballot match on the digit, in input order.  The first pass reads the waits
+// themselves (its histograms come straight from them, so no key array is
+// written before it); from 2^22 keys each scatter also writes the next digit
+// as one byte per key, which the next histogram reads instead of the keys.
 //
 // Scans: the closed form needs N and S only at t1, at each deadline and at
 // the whole sample.  Without a requested order they are formed there, from
